@@ -1,0 +1,152 @@
+/*
+ * cp_attn.h — C ABI of the mixed prefill/decode paged-attention step of one
+ * chunked-prefill scheduling iteration, for AMD Instinct MI355X (gfx950).
+ *
+ * The paper's scheduler (Aging ordering, LPRS target-time chunk selection,
+ * APC activity control; Sec. 3) finalises a batch every round and submits it
+ * to the backend (Sec. 3.2.2, the four-step online procedure).  A batch holds
+ * every running decode request as a one-token row (decode-first admission,
+ * Sec. 3.1.3) plus at most one prefill chunk per selected request (Sec. 3.1.3;
+ * Algorithm 1 returns one chunk size per request).  This library executes the
+ * attention part of that batch on the GPU:
+ *
+ *   cp_kv_append   writes the batch's new K/V rows into the paged cache;
+ *   cp_attn_mixed  computes, for every scheduled query token, causal
+ *                  attention over its request's cached keys.
+ *
+ * Scheduling never changes how chunks are executed or how the KV cache is
+ * managed (Sec. 3.1.3), so this is a pure execution interface: the caller owns
+ * every buffer and decides what goes in the batch.
+ *
+ * Definition computed (the paper names the operation but does not write it
+ * out; this is standard scaled-dot-product attention with grouped KV heads):
+ * for row r with metadata (req, start, len, ctx), query j < len sits at
+ * absolute position p = start + j and q head h reads kv head g = h / (Hq/Hkv);
+ *     out[t][h] = sum_{i<=p} softmax_i(sm_scale * q[t][h] . K_i) V_i
+ * where K_i, V_i are the keys/values of request req at logical position i,
+ * t = (sum of len over rows before r) + j.  Softmax is evaluated in fp32 with
+ * bf16 inputs, products accumulated in fp32, and the output rounded to bf16.
+ *
+ * Layouts (all bf16 tensors are dense, row-major, 16-byte aligned):
+ *   q, out        [T][Hq][D]        T = sum of chunk_len over rows, rows packed
+ *                                   in the order of the rows array
+ *   k_new, v_new  [T][Hkv][D]
+ *   k_cache       [num_blocks][Hkv][B][D]   token-major inside a block
+ *   v_cache       [num_blocks][Hkv][D][B]   feature-major inside a block
+ *   block_tables  int32 [num_reqs_in_table][max_blocks_per_req]; entry
+ *                 [req][i] is the physical block of logical block i
+ *   rows          host array of cp_row_meta, read only during the call
+ *
+ * Ownership: every device buffer is allocated and owned by the caller.  The
+ * library never allocates device memory in these calls; it keeps one pinned
+ * host staging ring (allocated on first use, reused afterwards) for plan
+ * uploads.  The workspace is caller-provided, device memory, at least
+ * cp_workspace_bytes() bytes, 256-byte aligned; it must not be used by any
+ * other call that is in flight at the same time.
+ *
+ * Errors: functions return CP_OK (0) or a negative CP_ERR_* code.  All
+ * validation happens before anything is enqueued: a call that fails enqueues
+ * no work and writes nothing.  No C++ exception crosses this interface.
+ * Block-table entries live on the device and are not inspected on the host;
+ * entries a batch reads must be in [0, num_blocks).
+ *
+ * Asynchrony: both compute calls are asynchronous on `stream` (a hipStream_t;
+ * NULL is the legacy default stream).  cp_attn_mixed reads only the caches:
+ * append the batch's K/V first, on the same stream.
+ */
+#ifndef CP_ATTN_H
+#define CP_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CP_OK 0
+#define CP_ERR_INVALID_ARG (-1) /* null pointer, bad size, misaligned buffer   */
+#define CP_ERR_BAD_META (-2)    /* malformed row metadata                      */
+#define CP_ERR_WORKSPACE (-3)   /* workspace smaller than cp_workspace_bytes() */
+#define CP_ERR_UNSUPPORTED (-4) /* head_dim / block_size / group not supported */
+#define CP_ERR_HIP (-5)         /* a HIP runtime call failed                   */
+
+/* One scheduled row: a decode step (chunk_len == 1 at the end of a finished
+ * prompt) or a prefill chunk.  Required: chunk_start >= 0, chunk_len >= 0,
+ * ctx_len == chunk_start + chunk_len, ctx_len <= max_blocks_per_req *
+ * block_size, 0 <= req_id < num_reqs_in_table, and no req_id twice in one
+ * batch (one chunk per request per round, Sec. 3.1.3).  A row with
+ * chunk_len == 0 is a legal no-op (Algorithm 1 and the APC rule of Eq. 14
+ * may assign a zero chunk).  Rows may come in any order. */
+typedef struct {
+    int32_t req_id;
+    int32_t chunk_start; /* tokens of this request already in the cache     */
+    int32_t chunk_len;   /* new tokens processed in this iteration          */
+    int32_t ctx_len;     /* keys visible to the row's last query            */
+} cp_row_meta;
+
+/* Geometry of the attention layer and of the paged pool.  Supported:
+ * head_dim in {64, 128}; block_size in {16, 32}; num_q_heads / num_kv_heads
+ * in {1, 2, 4, 8}; sm_scale finite and > 0 (1/sqrt(head_dim) is usual). */
+typedef struct {
+    int32_t num_q_heads;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t block_size;
+    int32_t num_blocks;
+    int32_t max_blocks_per_req;
+    int32_t num_reqs_in_table;
+    float sm_scale;
+} cp_attn_desc;
+
+/* Library version as major*10000 + minor*100 + patch. */
+int cp_version(void);
+
+/* Static string for a CP_* code ("unknown error" for anything else). */
+const char *cp_strerror(int code);
+
+/* Workspace bytes cp_attn_mixed and cp_kv_append need for this batch, or 0 if
+ * desc/rows are invalid (call cp_check_batch for the reason).  Depends only
+ * on desc and the rows' metadata, never on tensor contents. */
+size_t cp_workspace_bytes(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows);
+
+/* Host-only validation of desc and rows; returns CP_OK or the code the
+ * compute calls would return for them. */
+int cp_check_batch(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows);
+
+/* Paged append: for every row and j < chunk_len, position p = chunk_start + j
+ * of request req_id receives token t's K and V for every kv head:
+ *   k_cache[bt[req][p / B]][h][p % B][:]  = k_new[t][h][:]
+ *   v_cache[bt[req][p / B]][h][:][p % B]  = v_new[t][h][:]
+ * A bit copy; every other cache slot is left untouched. */
+int cp_kv_append(const cp_attn_desc *desc, const void *k_new, const void *v_new, void *k_cache,
+                 void *v_cache, const int32_t *block_tables, const cp_row_meta *rows,
+                 int32_t n_rows, void *ws, size_t ws_bytes, void *stream);
+
+/* Mixed prefill/decode causal attention over the paged cache (definition in
+ * the file header).  Writes out[T][Hq][D]; reads q, the caches and the
+ * tables.  Rows with chunk_len >= 2 run on the bf16-MFMA chunk kernel, one-
+ * token rows on the split-K decode kernel; long key ranges are split and
+ * merged by a log-sum-exp pass. */
+int cp_attn_mixed(const cp_attn_desc *desc, const void *q, const void *k_cache,
+                  const void *v_cache, const int32_t *block_tables, const cp_row_meta *rows,
+                  int32_t n_rows, void *out, void *ws, size_t ws_bytes, void *stream);
+
+/* Plan summary for diagnostics and tests (host only, enqueues nothing).
+ * counts[0..5] receive: prefill work items, decode work items, merge groups,
+ * partial rows, workspace bytes, decode blocks per split. */
+int cp_plan_summary(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows,
+                    int64_t counts[6]);
+
+/* Host-only copy of the plan's work items, for coverage tests.  Each item is
+ * 8 int32: {kind (0 prefill, 1 decode), first token, tokens, first position,
+ * req_id, kv head, key begin, key end}.  Writes min(cap, n) items to items
+ * and returns n (the full count), or a negative CP_ERR_* code. */
+int64_t cp_plan_items(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows,
+                      int32_t *items, int64_t cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CP_ATTN_H */

@@ -1,0 +1,22 @@
+"""MI355X-native mixed prefill/decode paged attention for chunked-prefill serving.
+
+The HIP library (libcpattn.so, built from csrc/ for gfx950) holds the whole
+path: the varlen planner, the paged KV append, the bf16-MFMA prefill-chunk
+kernel, the split-K decode kernel and the merge pass.  ``binding`` is the
+ctypes layer over its C ABI (include/cp_attn.h); ``step`` drives one
+scheduling iteration's attention step on torch tensors.
+"""
+
+from .binding import (  # noqa: F401
+    CpError,
+    Desc,
+    attn_mixed,
+    check_batch,
+    desc_for,
+    kv_append,
+    make_desc,
+    plan_items,
+    plan_summary,
+    version,
+    workspace_bytes,
+)

@@ -1,0 +1,187 @@
+"""ctypes binding of libcpattn.so: argument marshalling only.
+
+Every step of the attention path runs in the library's HIP kernels; this
+module turns torch tensors into device pointers, the row metadata into the
+packed host array, and error codes into exceptions.  There is no fallback:
+if the library is not built, every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcpattn.so")
+
+CP_OK = 0
+CP_ERR_INVALID_ARG = -1
+CP_ERR_BAD_META = -2
+CP_ERR_WORKSPACE = -3
+CP_ERR_UNSUPPORTED = -4
+CP_ERR_HIP = -5
+
+
+class CpError(RuntimeError):
+    def __init__(self, code, what):
+        self.code = code
+        super().__init__(f"{what}: {strerror(code)} ({code})")
+
+
+class Desc(ctypes.Structure):
+    """cp_attn_desc"""
+
+    _fields_ = [
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("num_blocks", ctypes.c_int32),
+        ("max_blocks_per_req", ctypes.c_int32),
+        ("num_reqs_in_table", ctypes.c_int32),
+        ("sm_scale", ctypes.c_float),
+    ]
+
+
+_lib = None
+
+
+def load():
+    """Loads the built library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build the HIP extension first "
+            "(python -m paper_2606_09061_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    dp = ctypes.POINTER(Desc)
+    lib.cp_version.argtypes, lib.cp_version.restype = [], ctypes.c_int
+    lib.cp_strerror.argtypes, lib.cp_strerror.restype = [ctypes.c_int], ctypes.c_char_p
+    lib.cp_workspace_bytes.argtypes, lib.cp_workspace_bytes.restype = [dp, vp, i32], sz
+    lib.cp_check_batch.argtypes, lib.cp_check_batch.restype = [dp, vp, i32], ctypes.c_int
+    lib.cp_kv_append.argtypes = [dp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
+    lib.cp_kv_append.restype = ctypes.c_int
+    lib.cp_attn_mixed.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp]
+    lib.cp_attn_mixed.restype = ctypes.c_int
+    lib.cp_plan_summary.argtypes = [dp, vp, i32, vp]
+    lib.cp_plan_summary.restype = ctypes.c_int
+    lib.cp_plan_items.argtypes = [dp, vp, i32, vp, i64]
+    lib.cp_plan_items.restype = i64
+    _lib = lib
+    return lib
+
+
+def exported_symbols():
+    return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch", "cp_kv_append",
+            "cp_attn_mixed", "cp_plan_summary", "cp_plan_items"]
+
+
+def strerror(code: int) -> str:
+    try:
+        return load().cp_strerror(int(code)).decode()
+    except RuntimeError:
+        return f"code {code}"
+
+
+def version() -> int:
+    return load().cp_version()
+
+
+def make_desc(num_q_heads, num_kv_heads, head_dim, block_size, num_blocks, max_blocks_per_req,
+              num_reqs_in_table, sm_scale) -> Desc:
+    return Desc(int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size),
+                int(num_blocks), int(max_blocks_per_req), int(num_reqs_in_table), float(sm_scale))
+
+
+def desc_for(batch) -> Desc:
+    """Desc of a workloads.Batch-like object."""
+    return make_desc(batch.num_q_heads, batch.num_kv_heads, batch.head_dim, batch.block_size,
+                     batch.num_blocks, batch.max_blocks_per_req, batch.num_reqs_in_table,
+                     batch.sm_scale)
+
+
+def _rows(rows) -> np.ndarray:
+    r = np.ascontiguousarray(rows, dtype=np.int32).reshape(-1, 4)
+    return r
+
+
+def _ptr(x):
+    """Device/host pointer of a tensor, an int address or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def check_batch(desc: Desc, rows) -> int:
+    r = _rows(rows)
+    return load().cp_check_batch(ctypes.byref(desc), r.ctypes.data, r.shape[0])
+
+
+def workspace_bytes(desc: Desc, rows) -> int:
+    r = _rows(rows)
+    n = load().cp_workspace_bytes(ctypes.byref(desc), r.ctypes.data, r.shape[0])
+    if n == 0:
+        raise CpError(check_batch(desc, rows), "cp_workspace_bytes")
+    return int(n)
+
+
+def kv_append(desc: Desc, k_new, v_new, k_cache, v_cache, block_tables, rows, ws, ws_bytes=None,
+              stream=None) -> None:
+    r = _rows(rows)
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    rc = load().cp_kv_append(ctypes.byref(desc), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
+                             _ptr(v_cache), _ptr(block_tables), r.ctypes.data, r.shape[0],
+                             _ptr(ws), nbytes, _stream(stream))
+    if rc != CP_OK:
+        raise CpError(rc, "cp_kv_append")
+
+
+def attn_mixed(desc: Desc, q, k_cache, v_cache, block_tables, rows, out, ws, ws_bytes=None,
+               stream=None) -> None:
+    r = _rows(rows)
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    rc = load().cp_attn_mixed(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                              _ptr(block_tables), r.ctypes.data, r.shape[0], _ptr(out), _ptr(ws),
+                              nbytes, _stream(stream))
+    if rc != CP_OK:
+        raise CpError(rc, "cp_attn_mixed")
+
+
+def plan_summary(desc: Desc, rows) -> dict:
+    r = _rows(rows)
+    c = np.zeros(6, dtype=np.int64)
+    rc = load().cp_plan_summary(ctypes.byref(desc), r.ctypes.data, r.shape[0], c.ctypes.data)
+    if rc != CP_OK:
+        raise CpError(rc, "cp_plan_summary")
+    keys = ["prefill_items", "decode_items", "merge_groups", "partial_rows", "workspace_bytes",
+            "decode_split_blocks"]
+    return dict(zip(keys, (int(x) for x in c)))
+
+
+def plan_items(desc: Desc, rows) -> np.ndarray:
+    """[n, 8] int32: kind, tok0, n_tok, pos0, req, kv head, key begin, key end."""
+    r = _rows(rows)
+    lib = load()
+    n = lib.cp_plan_items(ctypes.byref(desc), r.ctypes.data, r.shape[0], None, 0)
+    if n < 0:
+        raise CpError(int(n), "cp_plan_items")
+    out = np.zeros((max(n, 1), 8), dtype=np.int32)
+    n2 = lib.cp_plan_items(ctypes.byref(desc), r.ctypes.data, r.shape[0], out.ctypes.data, n)
+    assert n2 == n
+    return out[:n]

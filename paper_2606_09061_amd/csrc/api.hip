@@ -1,0 +1,313 @@
+// C ABI of libcpattn: validation, planning, plan upload and launches.
+#include <hip/hip_runtime.h>
+
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "cp_attn.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+using namespace cpattn;
+
+namespace {
+
+constexpr int kRingSlots = 8;
+
+// Pinned host staging for plan uploads.  A slot is reused only after the
+// copy that last read it has completed (its event), so a host write never
+// races an in-flight DMA.
+struct Stage {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+
+struct DeviceCtx {
+  Stage ring[kRingSlots];
+  int next = 0;
+};
+
+std::mutex g_mu;
+std::vector<DeviceCtx*> g_devs;
+
+int num_cus_setting() {
+  static const int n = [] {
+    const char* s = std::getenv("CP_NUM_CUS");
+    const int v = s ? std::atoi(s) : 0;
+    return v > 0 ? v : 256;  // MI355X
+  }();
+  return n;
+}
+
+bool debug_sync() {
+  static const bool on = [] {
+    const char* s = std::getenv("CP_DEBUG");
+    return s && s[0] == '1';
+  }();
+  return on;
+}
+
+// Requires g_mu held.
+DeviceCtx* device_ctx(int* err) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    *err = CP_ERR_HIP;
+    return nullptr;
+  }
+  if ((int)g_devs.size() <= dev) g_devs.resize(dev + 1, nullptr);
+  if (!g_devs[dev]) g_devs[dev] = new (std::nothrow) DeviceCtx();
+  if (!g_devs[dev]) *err = CP_ERR_HIP;
+  return g_devs[dev];
+}
+
+int upload(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return CP_OK;
+  std::lock_guard<std::mutex> lk(g_mu);
+  int err = CP_OK;
+  DeviceCtx* c = device_ctx(&err);
+  if (!c) return err;
+  Stage& st = c->ring[c->next];
+  c->next = (c->next + 1) % kRingSlots;
+  if (st.pending) {
+    if (hipEventSynchronize(st.ev) != hipSuccess) return CP_ERR_HIP;
+    st.pending = false;
+  }
+  if (!st.ev && hipEventCreateWithFlags(&st.ev, hipEventDisableTiming) != hipSuccess)
+    return CP_ERR_HIP;
+  if (st.cap < bytes) {
+    if (st.host) (void)hipHostFree(st.host);
+    st.host = nullptr;
+    st.cap = 0;
+    size_t cap = 64 << 10;
+    while (cap < bytes) cap *= 2;
+    if (hipHostMalloc(&st.host, cap, hipHostMallocDefault) != hipSuccess) return CP_ERR_HIP;
+    st.cap = cap;
+  }
+  std::memcpy(st.host, src, bytes);
+  if (hipMemcpyAsync(dst, st.host, bytes, hipMemcpyHostToDevice, s) != hipSuccess)
+    return CP_ERR_HIP;
+  if (hipEventRecord(st.ev, s) != hipSuccess) return CP_ERR_HIP;
+  st.pending = true;
+  return CP_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int64_t total_tokens(const cp_row_meta* rows, int32_t n) {
+  int64_t t = 0;
+  for (int32_t i = 0; i < n; ++i) t += rows[i].chunk_len;
+  return t;
+}
+
+int finish(hipError_t e, hipStream_t s) {
+  if (e != hipSuccess) return CP_ERR_HIP;
+  if (debug_sync()) {
+    if (hipStreamSynchronize(s) != hipSuccess) return CP_ERR_HIP;
+    if (hipGetLastError() != hipSuccess) return CP_ERR_HIP;
+  }
+  return CP_OK;
+}
+
+void serialize(const Plan& p, std::vector<uint8_t>& buf) {
+  buf.assign(p.plan_bytes, 0);
+  if (!p.prefill.empty())
+    std::memcpy(buf.data() + p.off_prefill, p.prefill.data(),
+                p.prefill.size() * sizeof(PrefillItem));
+  if (!p.decode.empty())
+    std::memcpy(buf.data() + p.off_decode, p.decode.data(), p.decode.size() * sizeof(DecodeItem));
+  if (!p.merge.empty())
+    std::memcpy(buf.data() + p.off_merge, p.merge.data(), p.merge.size() * sizeof(MergeGroup));
+}
+
+}  // namespace
+
+extern "C" {
+
+int cp_version(void) { return 1 * 10000 + 0 * 100 + 0; }
+
+const char* cp_strerror(int code) {
+  switch (code) {
+    case CP_OK: return "success";
+    case CP_ERR_INVALID_ARG: return "invalid argument (null pointer, size or alignment)";
+    case CP_ERR_BAD_META: return "malformed row metadata";
+    case CP_ERR_WORKSPACE: return "workspace too small";
+    case CP_ERR_UNSUPPORTED: return "unsupported head_dim, block_size or head group";
+    case CP_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown error";
+}
+
+int cp_check_batch(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows) {
+  return validate(desc, rows, n_rows);
+}
+
+size_t cp_workspace_bytes(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows) {
+  if (validate(desc, rows, n_rows) != CP_OK) return 0;
+  try {
+    Plan p;
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    AppendPlan a;
+    build_append_plan(*desc, rows, n_rows, a);
+    return p.ws_bytes > a.ws_bytes ? p.ws_bytes : a.ws_bytes;
+  } catch (...) {
+    return 0;
+  }
+}
+
+int cp_plan_summary(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows,
+                    int64_t counts[6]) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  if (!counts) return CP_ERR_INVALID_ARG;
+  try {
+    Plan p;
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    counts[0] = (int64_t)p.prefill.size();
+    counts[1] = (int64_t)p.decode.size();
+    counts[2] = (int64_t)p.merge.size();
+    counts[3] = p.partial_rows;
+    counts[4] = (int64_t)cp_workspace_bytes(desc, rows, n_rows);
+    counts[5] = p.decode_split_blocks;
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
+  return CP_OK;
+}
+
+int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows,
+                      int32_t* items, int64_t cap) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  if (cap > 0 && !items) return CP_ERR_INVALID_ARG;
+  try {
+    Plan p;
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    int64_t n = 0;
+    auto put = [&](int32_t kind, int32_t tok, int32_t ntok, int32_t pos, int32_t req, int32_t kvh,
+                   int32_t kb, int32_t ke) {
+      if (n < cap) {
+        int32_t* o = items + 8 * n;
+        o[0] = kind, o[1] = tok, o[2] = ntok, o[3] = pos, o[4] = req, o[5] = kvh, o[6] = kb,
+        o[7] = ke;
+      }
+      ++n;
+    };
+    for (const PrefillItem& it : p.prefill)
+      put(0, it.tok0, it.n_tok, it.pos0, it.req, it.kvh, it.kv_begin, it.kv_end);
+    for (const DecodeItem& it : p.decode) {
+      // position of the decode query: its row's ctx_len - 1, recovered from the row
+      int32_t pos = -1;
+      int64_t t = 0;
+      for (int32_t r = 0; r < n_rows; ++r) {
+        if (t == it.tok && rows[r].chunk_len > 0) {
+          pos = rows[r].chunk_start;
+          break;
+        }
+        t += rows[r].chunk_len;
+      }
+      put(1, it.tok, 1, pos, it.req, it.kvh, it.kv_begin, it.kv_end);
+    }
+    return n;
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
+}
+
+int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new, void* k_cache,
+                 void* v_cache, const int32_t* block_tables, const cp_row_meta* rows,
+                 int32_t n_rows, void* ws, size_t ws_bytes, void* stream) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  if (total_tokens(rows, n_rows) == 0) return CP_OK;
+  if (!k_new || !v_new || !k_cache || !v_cache || !block_tables || !ws) return CP_ERR_INVALID_ARG;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) ||
+      !aligned(v_cache, 16) || !aligned(ws, 256) || !aligned(block_tables, 4))
+    return CP_ERR_INVALID_ARG;
+  try {
+    AppendPlan p;
+    build_append_plan(*desc, rows, n_rows, p);
+    if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    int rc = upload(ws, p.items.data(), p.items.size() * sizeof(AppendItem), s);
+    if (rc != CP_OK) return rc;
+    AppendArgs a;
+    a.items = reinterpret_cast<const AppendItem*>(ws);
+    a.n_items = (int)p.items.size();
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
+    a.k_cache = static_cast<uint16_t*>(k_cache);
+    a.v_cache = static_cast<uint16_t*>(v_cache);
+    a.bt = block_tables;
+    a.hkv = desc->num_kv_heads;
+    a.mbr = desc->max_blocks_per_req;
+    return finish(launch_append(desc->head_dim, desc->block_size, a, s), s);
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
+}
+
+int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
+                  const void* v_cache, const int32_t* block_tables, const cp_row_meta* rows,
+                  int32_t n_rows, void* out, void* ws, size_t ws_bytes, void* stream) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  if (total_tokens(rows, n_rows) == 0) return CP_OK;
+  if (!q || !k_cache || !v_cache || !block_tables || !out || !ws) return CP_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
+      !aligned(ws, 256) || !aligned(block_tables, 4))
+    return CP_ERR_INVALID_ARG;
+  try {
+    Plan p;
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
+    thread_local std::vector<uint8_t> buf;
+    serialize(p, buf);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    int rc = upload(ws, buf.data(), buf.size(), s);
+    if (rc != CP_OK) return rc;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    AttnArgs a;
+    a.prefill = reinterpret_cast<const PrefillItem*>(base + p.off_prefill);
+    a.n_prefill = (int)p.prefill.size();
+    a.decode = reinterpret_cast<const DecodeItem*>(base + p.off_decode);
+    a.n_decode = (int)p.decode.size();
+    a.merge = reinterpret_cast<const MergeGroup*>(base + p.off_merge);
+    a.n_merge = (int)p.merge.size();
+    a.q = static_cast<const uint16_t*>(q);
+    a.k_cache = static_cast<const uint16_t*>(k_cache);
+    a.v_cache = static_cast<const uint16_t*>(v_cache);
+    a.bt = block_tables;
+    a.out = static_cast<uint16_t*>(out);
+    a.part_o = reinterpret_cast<float*>(base + p.off_part_o);
+    a.part_lse = reinterpret_cast<float*>(base + p.off_part_lse);
+    a.hq = desc->num_q_heads;
+    a.hkv = desc->num_kv_heads;
+    a.block_size = desc->block_size;
+    a.mbr = desc->max_blocks_per_req;
+    a.scale_log2 = desc->sm_scale * 1.4426950408889634f;
+    const int D = desc->head_dim;
+    const int G = desc->num_q_heads / desc->num_kv_heads;
+    if (a.n_prefill > 0) {
+      rc = finish(launch_prefill(D, G, a, s), s);
+      if (rc != CP_OK) return rc;
+    }
+    if (a.n_decode > 0) {
+      rc = finish(launch_decode(D, desc->block_size, G, a, s), s);
+      if (rc != CP_OK) return rc;
+    }
+    if (a.n_merge > 0) {
+      rc = finish(launch_merge(D, G, a, s), s);
+      if (rc != CP_OK) return rc;
+    }
+    return CP_OK;
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
+}
+
+}  // extern "C"

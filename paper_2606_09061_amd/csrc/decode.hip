@@ -1,0 +1,328 @@
+// Split-K decode attention (one query token per row, G q heads per kv head).
+//
+// Decode is memory-bandwidth bound (Sec. 1 and 2.1 of the paper): every key
+// and value of the context is read once per kv head and used by only G q
+// heads, so the kernel is organised around streaming the paged blocks at
+// full HBM rate and keeping the VALU work per byte small.
+//
+// Work item: (row, kv head, range of whole blocks).  A workgroup of 4 waves
+// takes one item; wave w walks blocks w, w+4, ... of the range, one block per
+// step, with the next block's loads issued before the current one is used.
+//
+// Per block (one "tile" of B keys) every lane issues NL 16-byte loads of K
+// and NL of V; instruction i of the wave reads bytes [1024 i, 1024 i + 1024)
+// of the block, so each load instruction is one contiguous 1 KiB segment.
+//   K tile [B][D]: lane holds 8 features (chunk lane % (D/8)) of NL keys.
+//     Scores: bf16 dot2 against the lane's 8 features of each of the G q
+//     heads, then a butterfly reduce-scatter over the D/8 lanes of a key row
+//     (DPP inside rows of 16) leaves each lane with whole scores.
+//   V tile [D][B]: lane holds 8 consecutive keys (chunk lane % (B/8)) of NL
+//     feature rows.  Weights of those 8 keys come from a per-wave LDS slot,
+//     and the weighted sum is again bf16 dot2 with fp32 accumulation.
+// Online softmax runs in base 2 with a lazily updated running max per head.
+// The 4 waves' (max, sum, output) states are combined through LDS; an item
+// covering the whole context writes the bf16 output, a split item writes its
+// normalised fp32 output and log2-sum-exp for the merge pass.
+#include "device.hpp"
+#include "kernels.hpp"
+
+namespace cpattn {
+
+namespace {
+
+// Butterfly reduce-scatter of N partial sums over the lanes selected by
+// lane bits Dist, Dist/2, ..., 1.  While more than one value is left the
+// lane keeps the half picked by its own bit and adds its partner's copy of
+// that half; once one value is left the remaining bits are all-reduced.
+template <int N, int Dist>
+__device__ __forceinline__ void reduce_scatter(float* v, int lane) {
+  if constexpr (Dist >= 1) {
+    if constexpr (N > 1) {
+      constexpr int H = N / 2;
+      const bool hi = (lane & Dist) != 0;
+#pragma unroll
+      for (int k = 0; k < H; ++k) {
+        const float keep = hi ? v[H + k] : v[k];
+        const float send = hi ? v[k] : v[H + k];
+        v[k] = keep + lane_partner<Dist>(send);
+      }
+      reduce_scatter<H, Dist / 2>(v, lane);
+    } else {
+      v[0] += lane_partner<Dist>(v[0]);
+      reduce_scatter<1, Dist / 2>(v, lane);
+    }
+  }
+}
+
+}  // namespace
+
+template <int D, int B, int G>
+__global__ __launch_bounds__(256) void decode_kernel(
+    const DecodeItem* __restrict__ items, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
+    float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
+  constexpr int NL = B * D * 2 / 1024;  // 16-byte loads per lane per tile, K and V each
+  constexpr int LPR = D / 8;            // lanes sharing one K row
+  constexpr int TPI = 64 / LPR;         // K rows per load instruction
+  constexpr int LPD = B / 8;            // lanes sharing one V feature row
+  constexpr int DPI = 64 / LPD;         // V feature rows per load instruction
+  constexpr int NV = NL * G;            // partial scores per lane
+  constexpr int NVL = NV >= LPR ? NV / LPR : 1;
+  constexpr int DUP = NV >= LPR ? 1 : LPR / NV;  // lanes holding the same score
+  constexpr int kWaves = kDecodeWaves;
+  static_assert(NL * TPI == B && NL * DPI == D, "tile geometry");
+
+  __shared__ __attribute__((aligned(16))) uint16_t p_lds[kWaves][G][B];
+  __shared__ float red_o[kWaves][G][D];
+  __shared__ float red_m[kWaves][G];
+  __shared__ float red_l[kWaves][G];
+
+  const DecodeItem it = items[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int sub = lane % LPR;
+  const int krow = lane / LPR;
+  const int tc = lane % LPD;
+  const int vrow = lane / LPD;
+
+  uint4 qv[G];
+  {
+    const uint16_t* qb = q + ((int64_t)it.tok * hq + it.kvh * G) * D + sub * 8;
+#pragma unroll
+    for (int h = 0; h < G; ++h) qv[h] = ld_global16(qb + h * D);
+  }
+
+  // reduced-score slot k of this lane -> (head, key within tile)
+  int s_head[NVL], s_key[NVL];
+#pragma unroll
+  for (int k = 0; k < NVL; ++k) {
+    const int v = NV >= LPR ? sub * NVL + k : sub / DUP;
+    s_head[k] = v % G;
+    s_key[k] = (v / G) * TPI + krow;
+  }
+  const bool owner = (sub % DUP) == 0;
+
+  float m_run[G], m_lane[NVL], l_lane[NVL], o[G][NL];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m_run[h] = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) o[h][i] = 0.f;
+  }
+#pragma unroll
+  for (int k = 0; k < NVL; ++k) {
+    m_lane[k] = -INFINITY;
+    l_lane[k] = 0.f;
+  }
+
+  const int64_t head_elems = (int64_t)B * D;
+  const int kb0 = it.kv_begin / B;
+  const int kb1 = (it.kv_end + B - 1) / B;
+  const int32_t* bt_row = bt + (int64_t)it.req * mbr;
+
+  uint4 kr[NL], vr[NL];
+  int kb = kb0 + wave;
+  if (kb < kb1) {
+    const int64_t base = ((int64_t)bt_row[kb] * hkv + it.kvh) * head_elems + lane * 8;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) kr[i] = ld_global16(k_cache + base + i * 512);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) vr[i] = ld_global16(v_cache + base + i * 512);
+  }
+
+  for (; kb < kb1; kb += kWaves) {
+    const int nkb = kb + kWaves;
+    uint4 kn[NL], vn[NL];
+    if (nkb < kb1) {
+      const int64_t base = ((int64_t)bt_row[nkb] * hkv + it.kvh) * head_elems + lane * 8;
+#pragma unroll
+      for (int i = 0; i < NL; ++i) kn[i] = ld_global16(k_cache + base + i * 512);
+#pragma unroll
+      for (int i = 0; i < NL; ++i) vn[i] = ld_global16(v_cache + base + i * 512);
+    }
+    const int valid = min(B, it.kv_end - kb * B);
+
+    // ---- scores
+    float sv[NV];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float acc = 0.f;
+        acc = dot2_bf16(kr[i].x, qv[h].x, acc);
+        acc = dot2_bf16(kr[i].y, qv[h].y, acc);
+        acc = dot2_bf16(kr[i].z, qv[h].z, acc);
+        acc = dot2_bf16(kr[i].w, qv[h].w, acc);
+        sv[i * G + h] = acc;
+      }
+    }
+    reduce_scatter<NV, LPR / 2>(sv, lane);
+    float s[NVL];
+    bool grow = false;
+#pragma unroll
+    for (int k = 0; k < NVL; ++k) {
+      s[k] = s_key[k] < valid ? sv[k] * scale_log2 : -INFINITY;
+      grow |= s[k] > m_lane[k] + kRescaleThreshold;
+    }
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float x = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < NVL; ++k)
+          if (s_head[k] == h) x = fmaxf(x, s[k]);
+        x = wave_max(x);
+        const float mnew = fmaxf(m_run[h], x);
+        const float alpha = (m_run[h] == -INFINITY) ? 0.f : exp2f(m_run[h] - mnew);
+        m_run[h] = mnew;
+#pragma unroll
+        for (int i = 0; i < NL; ++i) o[h][i] *= alpha;
+#pragma unroll
+        for (int k = 0; k < NVL; ++k)
+          if (s_head[k] == h) {
+            l_lane[k] *= alpha;
+            m_lane[k] = mnew;
+          }
+      }
+    }
+    // ---- weights -> LDS
+#pragma unroll
+    for (int k = 0; k < NVL; ++k) {
+      const float p = exp2f(s[k] - m_lane[k]);
+      const uint16_t pb = to_bf16(p);
+      if (owner) {
+        l_lane[k] += __uint_as_float((uint32_t)pb << 16);
+        p_lds[wave][s_head[k]][s_key[k]] = pb;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    uint4 pv[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) pv[h] = *reinterpret_cast<const uint4*>(&p_lds[wave][h][tc * 8]);
+
+    // ---- zero values of keys past the end of the range (may hold NaN)
+    if (valid < B) {
+      const int t0 = tc * 8;
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        uint32_t* w = reinterpret_cast<uint32_t*>(&vr[i]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = (t0 + 2 * e) < valid ? 0x0000ffffu : 0u;
+          const uint32_t hi = (t0 + 2 * e + 1) < valid ? 0xffff0000u : 0u;
+          w[e] &= (lo | hi);
+        }
+      }
+    }
+    // ---- weighted values
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float acc = o[h][i];
+        acc = dot2_bf16(vr[i].x, pv[h].x, acc);
+        acc = dot2_bf16(vr[i].y, pv[h].y, acc);
+        acc = dot2_bf16(vr[i].z, pv[h].z, acc);
+        acc = dot2_bf16(vr[i].w, pv[h].w, acc);
+        o[h][i] = acc;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      kr[i] = kn[i];
+      vr[i] = vn[i];
+    }
+  }
+
+  // ---- combine inside the wave: feature rows are split over LPD lanes
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      float x = o[h][i];
+      x += dpp<kXor1>(x);
+      if constexpr (LPD == 4) x += dpp<kXor2>(x);
+      o[h][i] = x;
+    }
+  float lsum[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float x = 0.f;
+#pragma unroll
+    for (int k = 0; k < NVL; ++k)
+      if (s_head[k] == h && owner) x += l_lane[k];
+    lsum[h] = wave_sum(x);
+  }
+  if (tc == 0) {
+#pragma unroll
+    for (int i = 0; i < NL; ++i)
+#pragma unroll
+      for (int h = 0; h < G; ++h) red_o[wave][h][i * DPI + vrow] = o[h][i];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      red_m[wave][h] = m_run[h];
+      red_l[wave][h] = lsum[h];
+    }
+  }
+  __syncthreads();
+
+  // ---- combine the waves and write
+  for (int x = tid; x < G * D; x += 256) {
+    const int h = x / D;
+    const int d = x % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red_m[w][h]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float mw = red_m[w][h];
+      const float f = mw == -INFINITY ? 0.f : exp2f(mw - M);
+      L += f * red_l[w][h];
+      O += f * red_o[w][h][d];
+    }
+    const float val = L > 0.f ? O / L : 0.f;
+    if (it.part < 0) {
+      out[((int64_t)it.tok * hq + it.kvh * G + h) * D + d] = to_bf16(val);
+    } else {
+      part_o[(int64_t)(it.part + h) * D + d] = val;
+      if (d == 0) part_lse[it.part + h] = L > 0.f ? M + __log2f(L) : -INFINITY;
+    }
+  }
+}
+
+template <int D, int B, int G>
+static hipError_t launch_decode_t(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((decode_kernel<D, B, G>), dim3(a.n_decode), dim3(256), 0, s, a.decode, a.q,
+                     a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv, a.mbr,
+                     a.scale_log2);
+  return hipGetLastError();
+}
+
+template <int D, int B>
+static hipError_t launch_decode_g(int G, const AttnArgs& a, hipStream_t s) {
+  switch (G) {
+    case 1: return launch_decode_t<D, B, 1>(a, s);
+    case 2: return launch_decode_t<D, B, 2>(a, s);
+    case 4: return launch_decode_t<D, B, 4>(a, s);
+    case 8: return launch_decode_t<D, B, 8>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_decode(int D, int B, int G, const AttnArgs& a, hipStream_t s) {
+  if (D == 128 && B == 16) return launch_decode_g<128, 16>(G, a, s);
+  if (D == 128 && B == 32) return launch_decode_g<128, 32>(G, a, s);
+  if (D == 64 && B == 16) return launch_decode_g<64, 16>(G, a, s);
+  if (D == 64 && B == 32) return launch_decode_g<64, 32>(G, a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace cpattn

@@ -1,0 +1,102 @@
+// Varlen tile planner for one mixed prefill/decode batch (host side, no HIP).
+//
+// The scheduler packs rows of very different shapes into one iteration:
+// single-token decode rows over contexts of 16..32k keys, and prefill chunks
+// of a few to thousands of tokens over prior contexts of 0..32k keys (the
+// intra-batch heterogeneity of Sec. 1; micro-chunks of Sec. 3.3.1).  The
+// planner turns that ragged mix into three flat work lists of near-equal
+// cost: prefill tiles for the MFMA kernel, decode ranges for the split-K
+// kernel, and merge groups for rows whose key range was split.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "cp_attn.h"
+
+namespace cpattn {
+
+// Query rows per prefill workgroup: 4 waves x 32 rows.  A row is one
+// (query token, q head) pair of a single kv-head group, so a tile holds
+// kPrefillRows / G tokens of one chunk.
+constexpr int kPrefillRows = 128;
+// Keys per prefill main-loop iteration.
+constexpr int kPrefillKeys = 64;
+// Waves per decode workgroup (each wave walks every kDecodeWaves-th block).
+constexpr int kDecodeWaves = 4;
+
+struct PrefillItem {  // 32 bytes
+  int32_t tok0;       // first query token (index into q / out)
+  int32_t n_tok;      // tokens in the tile, 1 .. kPrefillRows / G
+  int32_t pos0;       // absolute position of tok0 inside its request
+  int32_t req;        // block-table row
+  int32_t kvh;        // kv head
+  int32_t kv_begin;   // keys [kv_begin, kv_end) of the request
+  int32_t kv_end;
+  int32_t part;       // -1: final output; else first partial row of this split
+};
+
+struct DecodeItem {   // 32 bytes
+  int32_t tok;        // query token
+  int32_t req;
+  int32_t kvh;
+  int32_t kv_begin;
+  int32_t kv_end;
+  int32_t part;       // -1: final output; else first partial row (G rows)
+  int32_t pad0, pad1;
+};
+
+struct MergeGroup {   // 32 bytes
+  int32_t tok0;       // first token of the group
+  int32_t n_tok;      // tokens (rows = n_tok * G)
+  int32_t kvh;
+  int32_t n_split;    // partials to combine per row
+  int32_t part0;      // row r of split s lives at part0 + s * n_tok * G + r
+  int32_t pad0, pad1, pad2;
+};
+
+struct AppendItem {   // 16 bytes: one request's new tokens inside one block
+  int32_t tok0;       // first new token (index into k_new / v_new)
+  int32_t n_tok;      // tokens, 1 .. block_size
+  int32_t block;      // logical block index of the request
+  int32_t req_slot0;  // req << 8 | first slot inside the block
+};
+
+struct Tuning {
+  int prefill_min_len = 2;      // rows with chunk_len >= this go to the MFMA kernel
+  int decode_target_items = 0;  // 0: derived from the CU count
+  int prefill_target_items = 0;
+  int num_cus = 256;
+};
+
+struct Plan {
+  std::vector<PrefillItem> prefill;
+  std::vector<DecodeItem> decode;
+  std::vector<MergeGroup> merge;
+  int64_t partial_rows = 0;
+  int32_t decode_split_blocks = 0;
+  // workspace layout (byte offsets from the workspace base)
+  size_t off_prefill = 0, off_decode = 0, off_merge = 0, off_part_o = 0, off_part_lse = 0;
+  size_t plan_bytes = 0;   // bytes of the uploaded item lists
+  size_t ws_bytes = 0;     // total workspace
+};
+
+struct AppendPlan {
+  std::vector<AppendItem> items;
+  size_t ws_bytes = 0;
+};
+
+// Host validation shared by every entry point.  Returns CP_OK or a CP_ERR_*.
+int validate(const cp_attn_desc* d, const cp_row_meta* rows, int32_t n_rows);
+
+// Builds the attention plan; assumes validate() passed.
+void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, const Tuning& t,
+                Plan& p);
+
+void build_append_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows,
+                       AppendPlan& p);
+
+Tuning tuning_from_env(int num_cus);
+
+}  // namespace cpattn
