@@ -145,6 +145,16 @@ int cp_plan_summary(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n
 int64_t cp_plan_items(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows,
                       int32_t *items, int64_t cap);
 
+/* Diagnostics: per-kernel GPU time.  After cp_profile_begin(), every kernel
+ * the compute calls launch is bracketed by a pair of HIP events recorded on
+ * the call's stream.  cp_profile_end() waits for those events and writes,
+ * per kernel kind (0 append, 1 prefill, 2 decode, 3 merge), the summed
+ * milliseconds into ms[4] and the launch count into launches[4]; it then
+ * stops recording.  Costs one event record per launch edge; not reentrant
+ * across threads. */
+int cp_profile_begin(void);
+int cp_profile_end(double ms[4], int64_t launches[4]);
+
 #ifdef __cplusplus
 }
 #endif

@@ -72,13 +72,16 @@ def load():
     lib.cp_plan_summary.restype = ctypes.c_int
     lib.cp_plan_items.argtypes = [dp, vp, i32, vp, i64]
     lib.cp_plan_items.restype = i64
+    lib.cp_profile_begin.argtypes, lib.cp_profile_begin.restype = [], ctypes.c_int
+    lib.cp_profile_end.argtypes, lib.cp_profile_end.restype = [vp, vp], ctypes.c_int
     _lib = lib
     return lib
 
 
 def exported_symbols():
     return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch", "cp_kv_append",
-            "cp_attn_mixed", "cp_plan_summary", "cp_plan_items"]
+            "cp_attn_mixed", "cp_plan_summary", "cp_plan_items", "cp_profile_begin",
+            "cp_profile_end"]
 
 
 def strerror(code: int) -> str:
@@ -185,3 +188,22 @@ def plan_items(desc: Desc, rows) -> np.ndarray:
     n2 = lib.cp_plan_items(ctypes.byref(desc), r.ctypes.data, r.shape[0], out.ctypes.data, n)
     assert n2 == n
     return out[:n]
+
+
+KERNEL_KINDS = ("append", "prefill", "decode", "merge")
+
+
+def profile_begin() -> None:
+    rc = load().cp_profile_begin()
+    if rc != CP_OK:
+        raise CpError(rc, "cp_profile_begin")
+
+
+def profile_end() -> dict:
+    """{kind: (total_ms, launches)} of the kernels launched since profile_begin()."""
+    ms = np.zeros(4, dtype=np.float64)
+    n = np.zeros(4, dtype=np.int64)
+    rc = load().cp_profile_end(ms.ctypes.data, n.ctypes.data)
+    if rc != CP_OK:
+        raise CpError(rc, "cp_profile_end")
+    return {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KERNEL_KINDS)}

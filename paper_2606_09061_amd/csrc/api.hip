@@ -104,6 +104,36 @@ int64_t total_tokens(const cp_row_meta* rows, int32_t n) {
   return t;
 }
 
+// ---- per-kernel event timing (diagnostics)
+struct ProfPair {
+  hipEvent_t a = nullptr, b = nullptr;
+  int kind = 0;
+};
+struct Profiler {
+  bool on = false;
+  std::vector<ProfPair> pool;
+  size_t used = 0;
+};
+Profiler g_prof;
+
+// Records the opening event of a launch of `kind`; returns the pair index or -1.
+long prof_open(int kind, hipStream_t s) {
+  if (!g_prof.on) return -1;
+  if (g_prof.used == g_prof.pool.size()) {
+    ProfPair p;
+    if (hipEventCreate(&p.a) != hipSuccess || hipEventCreate(&p.b) != hipSuccess) return -1;
+    g_prof.pool.push_back(p);
+  }
+  ProfPair& p = g_prof.pool[g_prof.used];
+  p.kind = kind;
+  if (hipEventRecord(p.a, s) != hipSuccess) return -1;
+  return (long)g_prof.used++;
+}
+
+void prof_close(long idx, hipStream_t s) {
+  if (idx >= 0) (void)hipEventRecord(g_prof.pool[idx].b, s);
+}
+
 int finish(hipError_t e, hipStream_t s) {
   if (e != hipSuccess) return CP_ERR_HIP;
   if (debug_sync()) {
@@ -198,7 +228,7 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
       ++n;
     };
     for (const PrefillItem& it : p.prefill)
-      put(0, it.tok0, it.n_tok, it.pos0, it.req, it.kvh, it.kv_begin, it.kv_end);
+      if (it.n_tok > 0) put(0, it.tok0, it.n_tok, it.pos0, it.req, it.kvh, it.kv_begin, it.kv_end);
     for (const DecodeItem& it : p.decode) {
       // position of the decode query: its row's ctx_len - 1, recovered from the row
       int32_t pos = -1;
@@ -245,7 +275,10 @@ int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new,
     a.bt = block_tables;
     a.hkv = desc->num_kv_heads;
     a.mbr = desc->max_blocks_per_req;
-    return finish(launch_append(desc->head_dim, desc->block_size, a, s), s);
+    const long pi = prof_open(0, s);
+    const hipError_t e = launch_append(desc->head_dim, desc->block_size, a, s);
+    prof_close(pi, s);
+    return finish(e, s);
   } catch (...) {
     return CP_ERR_INVALID_ARG;
   }
@@ -293,21 +326,55 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
     const int D = desc->head_dim;
     const int G = desc->num_q_heads / desc->num_kv_heads;
     if (a.n_prefill > 0) {
-      rc = finish(launch_prefill(D, G, a, s), s);
+      const long pi = prof_open(1, s);
+      const hipError_t e = launch_prefill(D, G, a, s);
+      prof_close(pi, s);
+      rc = finish(e, s);
       if (rc != CP_OK) return rc;
     }
     if (a.n_decode > 0) {
-      rc = finish(launch_decode(D, desc->block_size, G, a, s), s);
+      const long pi = prof_open(2, s);
+      const hipError_t e = launch_decode(D, desc->block_size, G, a, s);
+      prof_close(pi, s);
+      rc = finish(e, s);
       if (rc != CP_OK) return rc;
     }
     if (a.n_merge > 0) {
-      rc = finish(launch_merge(D, G, a, s), s);
+      const long pi = prof_open(3, s);
+      const hipError_t e = launch_merge(D, G, a, s);
+      prof_close(pi, s);
+      rc = finish(e, s);
       if (rc != CP_OK) return rc;
     }
     return CP_OK;
   } catch (...) {
     return CP_ERR_INVALID_ARG;
   }
+}
+
+int cp_profile_begin(void) {
+  g_prof.used = 0;
+  g_prof.on = true;
+  return CP_OK;
+}
+
+int cp_profile_end(double ms[4], int64_t launches[4]) {
+  if (!ms || !launches) return CP_ERR_INVALID_ARG;
+  for (int k = 0; k < 4; ++k) {
+    ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  g_prof.on = false;
+  for (size_t i = 0; i < g_prof.used; ++i) {
+    ProfPair& p = g_prof.pool[i];
+    if (hipEventSynchronize(p.b) != hipSuccess) return CP_ERR_HIP;
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, p.a, p.b) != hipSuccess) return CP_ERR_HIP;
+    ms[p.kind] += t;
+    launches[p.kind] += 1;
+  }
+  g_prof.used = 0;
+  return CP_OK;
 }
 
 }  // extern "C"

@@ -20,6 +20,66 @@ bool is_pow2_in(int v, int lo, int hi) {
   return (v & (v - 1)) == 0;
 }
 
+// Merge items of at most one workgroup's worth of rows (256 threads, each
+// combining 4 features of one row).
+void add_merge(Plan& p, int32_t tok0, int32_t n_tok, int32_t kvh, int32_t ns, int32_t part0, int G,
+               int D) {
+  const int32_t rows = n_tok * G;
+  const int32_t per = 256 / (D / 4);
+  for (int32_t r0 = 0; r0 < rows; r0 += per) {
+    MergeGroup g{tok0, n_tok, kvh, ns, part0, r0, std::min(per, rows - r0), 0};
+    p.merge.push_back(g);
+  }
+}
+
+// Orders prefill items so that items sharing a K/V range run on one XCD
+// (workgroup i is dispatched to XCD i mod num_xcds) and each XCD runs its
+// items longest first.  Groups are dealt to the least-loaded XCD, largest
+// group first; missing slots of shorter XCD lists become empty items.
+template <class T>
+void order_for_xcds(std::vector<T>& pf, int num_xcds, std::vector<PrefillItem>& out) {
+  out.clear();
+  if (pf.empty()) return;
+  const int X = std::max(1, num_xcds);
+  std::stable_sort(pf.begin(), pf.end(), [](const T& a, const T& b) {
+    return a.group < b.group;
+  });
+  struct Grp {
+    size_t b, e;
+    int64_t cost;
+  };
+  std::vector<Grp> groups;
+  for (size_t i = 0; i < pf.size();) {
+    size_t j = i;
+    int64_t c = 0;
+    while (j < pf.size() && pf[j].group == pf[i].group) c += pf[j++].cost;
+    groups.push_back({i, j, c});
+    i = j;
+  }
+  std::stable_sort(groups.begin(), groups.end(),
+                   [](const Grp& a, const Grp& b) { return a.cost > b.cost; });
+  std::vector<int64_t> load(X, 0);
+  std::vector<std::vector<const T*>> lists(X);
+  for (const Grp& g : groups) {
+    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[x] += g.cost;
+    for (size_t i = g.b; i < g.e; ++i) lists[x].push_back(&pf[i]);
+  }
+  size_t longest = 0;
+  for (auto& l : lists) {
+    std::stable_sort(l.begin(), l.end(), [](const T* a, const T* b) { return a->cost > b->cost; });
+    longest = std::max(longest, l.size());
+  }
+  PrefillItem empty{};
+  empty.n_tok = 0;
+  empty.part = -1;
+  out.reserve(longest * X);
+  for (size_t k = 0; k < longest; ++k)
+    for (int x = 0; x < X; ++x) out.push_back(k < lists[x].size() ? lists[x][k]->it : empty);
+  // drop trailing empty items
+  while (!out.empty() && out.back().n_tok == 0) out.pop_back();
+}
+
 }  // namespace
 
 int validate(const cp_attn_desc* d, const cp_row_meta* rows, int32_t n_rows) {
@@ -59,6 +119,8 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_PREFILL_MIN_LEN")) t.prefill_min_len = std::max(2, atoi(s));
   if (const char* s = std::getenv("CP_DECODE_TARGET_ITEMS")) t.decode_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_TARGET_ITEMS")) t.prefill_target_items = atoi(s);
+  if (const char* s = std::getenv("CP_PREFILL_MIN_SPLIT")) t.prefill_min_split = std::max(1, atoi(s));
+  if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::max(1, atoi(s));
   return t;
 }
 
@@ -79,7 +141,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     int32_t tok0, n_tok, pos0, req, kv_end;
   };
   std::vector<Tile> tiles;
-  int64_t pf_cost = 0;  // in kPrefillKeys-key steps per tile per kv head
+  int64_t pf_cost = 0;  // in kPrefillKeys-key steps, summed over tiles and kv heads
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len < t.prefill_min_len) continue;
@@ -90,31 +152,27 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
       pf_cost += ceil_div(tl.kv_end, kPrefillKeys) * Hkv;
     }
   }
-  // Split long key ranges so the item count covers the chip a few times
-  // and no single item dominates the critical path.
+  // Key ranges longer than split_keys are cut on a grid of multiples of
+  // split_keys, the same grid for every tile, so the tiles of one chunk share
+  // their split ranges exactly.  No cut lies past a tile's first query
+  // position, so every query of a tile sees at least one key in every split.
   const int64_t pf_target =
-      t.prefill_target_items > 0 ? t.prefill_target_items : (int64_t)t.num_cus * 2 * 2;
-  int64_t pf_steps = 0;  // max steps per item
-  if (!tiles.empty()) {
-    pf_steps = std::max<int64_t>(16, ceil_div(pf_cost, pf_target));
-  }
+      t.prefill_target_items > 0 ? t.prefill_target_items : (int64_t)t.num_cus * 4;
+  const int64_t split_steps =
+      tiles.empty() ? 1 : std::max<int64_t>(t.prefill_min_split, ceil_div(pf_cost, pf_target));
+  const int64_t split_keys = split_steps * kPrefillKeys;
   struct PfTmp {
     PrefillItem it;
     int64_t cost;
+    int64_t group;  // items sharing (request, kv head, key range start)
   };
   std::vector<PfTmp> pf;
   std::vector<int32_t> bounds;
   for (const Tile& tl : tiles) {
-    const int64_t steps = ceil_div(tl.kv_end, kPrefillKeys);
-    const int64_t want = std::max<int64_t>(1, ceil_div(steps, pf_steps));
-    // Split [0, kv_end) at step boundaries, none past the tile's first query
-    // position, so every query of the tile sees at least one key in every split.
-    const int32_t last_cut = (tl.pos0 / kPrefillKeys) * kPrefillKeys;
+    const int64_t last_cut = (tl.pos0 / kPrefillKeys) * (int64_t)kPrefillKeys;
     bounds.assign(1, 0);
-    for (int64_t s = 1; s < want; ++s) {
-      const int32_t b = (int32_t)std::min<int64_t>(steps * s / want * kPrefillKeys, last_cut);
-      if (b > bounds.back()) bounds.push_back(b);
-    }
+    for (int64_t c = split_keys; c <= last_cut && c < tl.kv_end; c += split_keys)
+      bounds.push_back((int32_t)c);
     bounds.push_back(tl.kv_end);
     const int64_t ns = (int64_t)bounds.size() - 1;
     for (int kvh = 0; kvh < Hkv; ++kvh) {
@@ -122,8 +180,6 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
       if (ns > 1) {
         part0 = (int32_t)p.partial_rows;
         p.partial_rows += ns * (int64_t)tl.n_tok * G;
-        MergeGroup g{tl.tok0, tl.n_tok, kvh, (int32_t)ns, part0, 0, 0, 0};
-        p.merge.push_back(g);
       }
       for (int64_t s = 0; s < ns; ++s) {
         PrefillItem it;
@@ -135,14 +191,14 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
         it.kv_begin = bounds[s];
         it.kv_end = bounds[s + 1];
         it.part = ns > 1 ? part0 + (int32_t)(s * tl.n_tok * G) : -1;
-        pf.push_back({it, ceil_div(it.kv_end - it.kv_begin, kPrefillKeys)});
+        // group id: request, kv head and split start (split starts are grid points)
+        const int64_t gid = (((int64_t)tl.req * Hkv + kvh) << 20) + bounds[s] / split_keys;
+        pf.push_back({it, ceil_div(it.kv_end - it.kv_begin, kPrefillKeys), gid});
       }
+      if (ns > 1) add_merge(p, tl.tok0, tl.n_tok, kvh, (int32_t)ns, part0, G, d.head_dim);
     }
   }
-  std::stable_sort(pf.begin(), pf.end(),
-                   [](const PfTmp& a, const PfTmp& b) { return a.cost > b.cost; });
-  p.prefill.reserve(pf.size());
-  for (auto& x : pf) p.prefill.push_back(x.it);
+  order_for_xcds(pf, t.num_xcds, p.prefill);
 
   // ---- decode ranges --------------------------------------------------
   int64_t dec_blocks = 0;
@@ -175,8 +231,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
         if (ns > 1) {
           part0 = (int32_t)p.partial_rows;
           p.partial_rows += ns * (int64_t)G;
-          MergeGroup g{(int32_t)off[r], 1, kvh, (int32_t)ns, part0, 0, 0, 0};
-          p.merge.push_back(g);
+          add_merge(p, (int32_t)off[r], 1, kvh, (int32_t)ns, part0, G, d.head_dim);
         }
         for (int64_t s = 0; s < ns; ++s) {
           const int64_t b0 = nb * s / ns, b1 = nb * (s + 1) / ns;

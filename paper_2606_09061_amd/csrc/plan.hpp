@@ -47,13 +47,15 @@ struct DecodeItem {   // 32 bytes
   int32_t pad0, pad1;
 };
 
-struct MergeGroup {   // 32 bytes
+struct MergeGroup {   // 32 bytes: rows [row0, row0 + n_rows) of one split group
   int32_t tok0;       // first token of the group
-  int32_t n_tok;      // tokens (rows = n_tok * G)
+  int32_t n_tok;      // tokens of the group (its rows = n_tok * G)
   int32_t kvh;
   int32_t n_split;    // partials to combine per row
   int32_t part0;      // row r of split s lives at part0 + s * n_tok * G + r
-  int32_t pad0, pad1, pad2;
+  int32_t row0;       // first row this item merges
+  int32_t n_rows;     // rows this item merges
+  int32_t pad0;
 };
 
 struct AppendItem {   // 16 bytes: one request's new tokens inside one block
@@ -67,7 +69,9 @@ struct Tuning {
   int prefill_min_len = 2;      // rows with chunk_len >= this go to the MFMA kernel
   int decode_target_items = 0;  // 0: derived from the CU count
   int prefill_target_items = 0;
+  int prefill_min_split = 32;   // shortest prefill split, in kPrefillKeys steps
   int num_cus = 256;
+  int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
 };
 
 struct Plan {

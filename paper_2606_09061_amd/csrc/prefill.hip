@@ -34,8 +34,11 @@ __device__ __forceinline__ int sigma(int c) {
   return (c & ~12) | ((c & 4) << 1) | ((c & 8) >> 1);
 }
 
-// row of the 32x32 accumulator held in register r by lane half g
-__device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+// key (within a 32-key sub-tile) of accumulator register r of lane half g:
+// sigma of the accumulator row 8*(r/4) + 4*g + r%4
+__device__ __forceinline__ int acc_key(int r, int g) {
+  return 16 * ((r >> 3) & 1) + 8 * g + 4 * ((r >> 2) & 1) + (r & 3);
+}
 
 }  // namespace
 
@@ -49,19 +52,24 @@ struct PrefillSmem {
   static constexpr int TOTAL = 2 * BUF;
 };
 
-template <int D, int G>
+template <int D, int B, int G>
 __global__ __launch_bounds__(256, 2) void prefill_kernel(
     const PrefillItem* __restrict__ items, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
-    float* __restrict__ part_lse, int hq, int hkv, int B, int mbr, float scale_log2) {
+    float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
   using SM = PrefillSmem<D>;
   constexpr int NKS = D / 16;                   // k-steps of S^T
   constexpr int NDT = D / 32;                   // 32-feature tiles of O^T
   constexpr int CH = BN * D * 2 / (256 * 16);   // 16-byte chunks per thread per K (and V) step
+  constexpr int KCH = D / 8;                    // 16-byte chunks per K row
+  constexpr int VPB = D * B / 8;                // 16-byte chunks per V block (one kv head)
+  constexpr int LOG2B = B == 16 ? 4 : 5;
+  static_assert(B == 16 || B == 32, "block size");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const PrefillItem it = items[blockIdx.x];
+  if (it.n_tok == 0) return;  // padding slot of the XCD-interleaved order
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -73,56 +81,71 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
   const bool row_valid = tl < it.n_tok;
   const int qpos = it.pos0 + tl;
   const int32_t* bt_row = bt + (int64_t)it.req * mbr;
-  const int64_t kv_head_off = (int64_t)it.kvh * B * D;  // (head) offset inside a block
   const int64_t blk_elems = (int64_t)hkv * B * D;
+  const uint16_t* kbase = k_cache + (int64_t)it.kvh * B * D;
+  const uint16_t* vbase = v_cache + (int64_t)it.kvh * B * D;
 
   // Q^T operand: lane holds features [16 ks + 8 g, +8) of its query row
   uint4 qreg[NKS];
   {
-    const uint16_t* qp = q + ((int64_t)(it.tok0 + (row_valid ? tl : 0)) * hq + it.kvh * G + hh) * D + g * 8;
+    const uint16_t* qp =
+        q + ((int64_t)(it.tok0 + (row_valid ? tl : 0)) * hq + it.kvh * G + hh) * D + g * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
       qreg[ks] = row_valid ? ld_global16(qp + ks * 16) : make_uint4(0, 0, 0, 0);
   }
 
-  // ---- tile loader: global -> registers -> LDS
+  // ---- gather geometry of 16-byte chunk c of this thread (shifts and masks
+  // only: every divisor below is a compile-time power of two)
+  //   K chunk: key kkey(c) of the step, feature chunk x % KCH
+  //   V chunk: block x / VPB of the step, feature row d, 8 keys from slot s0
+  auto kkey = [&](int c) { return (c * 256 + tid) / KCH; };
+  auto kgoff = [&](int c) { return (kkey(c) & (B - 1)) * D + ((c * 256 + tid) % KCH) * 8; };
+  auto klds = [&](int c) { return kkey(c) * SM::KS + ((c * 256 + tid) % KCH) * 16; };
+  auto vblk = [&](int c) { return (c * 256 + tid) / VPB; };
+  auto vd = [&](int c) { return ((c * 256 + tid) % VPB) / (B / 8); };
+  auto vs0 = [&](int c) { return (((c * 256 + tid) % VPB) % (B / 8)) * 8; };
+  auto vkey = [&](int c) { return vblk(c) * B + vs0(c); };
+  auto vgoff = [&](int c) { return vd(c) * B + vs0(c); };
+  auto vlds = [&](int c) { return vd(c) * SM::VS + vkey(c) * 2; };
+
   uint4 kreg[CH], vreg[CH];
   auto gload = [&](int k0) {
+    const int b0 = k0 >> LOG2B;
+    if (k0 + BN <= it.kv_end) {
 #pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      const int x = c * 256 + tid;
-      // K: chunk x -> key x / (D/8), 16-byte feature chunk x % (D/8)
-      const int key = x / (D / 8);
-      const int dch = x % (D / 8);
-      const int kpos = k0 + key;
-      uint4 kv = make_uint4(0, 0, 0, 0);
-      if (kpos < it.kv_end) {
-        const int64_t blk = bt_row[kpos / B];
-        kv = ld_global16(k_cache + blk * blk_elems + kv_head_off + (int64_t)(kpos % B) * D + dch * 8);
+      for (int c = 0; c < CH; ++c) {
+        const int64_t kb = bt_row[b0 + (kkey(c) >> LOG2B)];
+        kreg[c] = ld_global16(kbase + kb * blk_elems + kgoff(c));
+        const int64_t vb = bt_row[b0 + vblk(c)];
+        vreg[c] = ld_global16(vbase + vb * blk_elems + vgoff(c));
       }
-      kreg[c] = kv;
-      // V: chunk x -> block bi of the step, feature row d, 8 keys from slot s0
-      const int per_blk = D * B / 8;
-      const int bi = x / per_blk;
-      const int within = x % per_blk;
-      const int d = within / (B / 8);
-      const int s0 = (within % (B / 8)) * 8;
-      const int vpos = k0 + bi * B + s0;
-      uint4 vv = make_uint4(0, 0, 0, 0);
-      if (vpos < it.kv_end) {
-        const int64_t blk = bt_row[(k0 + bi * B) / B];
-        vv = ld_global16(v_cache + blk * blk_elems + kv_head_off + (int64_t)d * B + s0);
-        if (vpos + 8 > it.kv_end) {
-          uint32_t* w = reinterpret_cast<uint32_t*>(&vv);
+    } else {  // last step of the range: keys at or past kv_end are zero
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint32_t lo = (vpos + 2 * e) < it.kv_end ? 0x0000ffffu : 0u;
-            const uint32_t hi = (vpos + 2 * e + 1) < it.kv_end ? 0xffff0000u : 0u;
-            w[e] &= (lo | hi);
+      for (int c = 0; c < CH; ++c) {
+        uint4 kv = make_uint4(0, 0, 0, 0);
+        if (k0 + kkey(c) < it.kv_end) {
+          const int64_t kb = bt_row[b0 + (kkey(c) >> LOG2B)];
+          kv = ld_global16(kbase + kb * blk_elems + kgoff(c));
+        }
+        kreg[c] = kv;
+        uint4 vv = make_uint4(0, 0, 0, 0);
+        const int vpos = k0 + vkey(c);
+        if (vpos < it.kv_end) {
+          const int64_t vb = bt_row[b0 + vblk(c)];
+          vv = ld_global16(vbase + vb * blk_elems + vgoff(c));
+          if (vpos + 8 > it.kv_end) {
+            uint32_t* w = reinterpret_cast<uint32_t*>(&vv);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const uint32_t lo = (vpos + 2 * e) < it.kv_end ? 0x0000ffffu : 0u;
+              const uint32_t hi = (vpos + 2 * e + 1) < it.kv_end ? 0xffff0000u : 0u;
+              w[e] &= (lo | hi);
+            }
           }
         }
+        vreg[c] = vv;
       }
-      vreg[c] = vv;
     }
   };
   auto sstore = [&](int buf) {
@@ -130,16 +153,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
     uint8_t* vb = kb + SM::K_BYTES;
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      const int x = c * 256 + tid;
-      const int key = x / (D / 8);
-      const int dch = x % (D / 8);
-      *reinterpret_cast<uint4*>(kb + key * SM::KS + dch * 16) = kreg[c];
-      const int per_blk = D * B / 8;
-      const int bi = x / per_blk;
-      const int within = x % per_blk;
-      const int d = within / (B / 8);
-      const int s0 = (within % (B / 8)) * 8;
-      *reinterpret_cast<uint4*>(vb + d * SM::VS + (bi * B + s0) * 2) = vreg[c];
+      *reinterpret_cast<uint4*>(kb + klds(c)) = kreg[c];
+      *reinterpret_cast<uint4*>(vb + vlds(c)) = vreg[c];
     }
   };
 
@@ -148,7 +163,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
   for (int i = 0; i < NDT; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
-  float m_run = -INFINITY;
+  float m_run = -INFINITY;  // running max of the scaled (base-2) scores
   float l_run = 0.f;
 
   const int n_step = (it.kv_end - it.kv_begin + BN - 1) / BN;
@@ -180,22 +195,22 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
       }
     }
 
-    // ---- online softmax down this lane's query column
-    const bool need_mask = (k0 + BN - 1 > it.pos0) || (k0 + BN > it.kv_end);
+    // ---- online softmax down this lane's query column (raw scores; the
+    // scale is folded into the exponent)
+    if ((k0 + BN - 1 > it.pos0) || (k0 + BN > it.kv_end)) {
+      const int lim = min(qpos + 1, it.kv_end) - k0;  // keys [k0, k0 + lim) are visible
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (kt * 32 + acc_key(r, g) >= lim) sacc[kt][r] = -INFINITY;
+    }
     float mt = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = sacc[kt][r] * scale_log2;
-        if (need_mask) {
-          const int key = k0 + kt * 32 + sigma(acc_row(r, g));
-          if (key > qpos || key >= it.kv_end) v = -INFINITY;
-        }
-        sacc[kt][r] = v;
-        mt = fmaxf(mt, v);
-      }
-    mt = fmaxf(mt, shfl_xor_f(mt, 32));
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[kt][r]);
+    mt = fmaxf(mt, shfl_xor_f(mt, 32)) * scale_log2;
     if (__builtin_amdgcn_ballot_w64(mt > m_run + kRescaleThreshold)) {
       const float mnew = fmaxf(m_run, mt);
       const float alpha = (m_run == -INFINITY) ? 0.f : exp2f(m_run - mnew);
@@ -206,7 +221,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
     }
-    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
     uint4 pk[2][2];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -215,7 +230,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
         float p[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(sacc[kt][8 * h2 + e] - m_use);
+          p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][8 * h2 + e], scale_log2, neg_m));
           l_run += p[e];
         }
         pk[kt][h2] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
@@ -269,38 +284,38 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
   }
 }
 
-template <int D, int G>
+template <int D, int B, int G>
 static hipError_t launch_prefill_t(const AttnArgs& a, hipStream_t s) {
   constexpr int smem = PrefillSmem<D>::TOTAL;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<D, G>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<D, B, G>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, smem);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((prefill_kernel<D, G>), dim3(a.n_prefill), dim3(256), smem, s, a.prefill,
+  hipLaunchKernelGGL((prefill_kernel<D, B, G>), dim3(a.n_prefill), dim3(256), smem, s, a.prefill,
                      a.q, a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv,
-                     a.block_size, a.mbr, a.scale_log2);
+                     a.mbr, a.scale_log2);
   return hipGetLastError();
 }
 
-hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s) {
-  if (D == 128) {
-    switch (G) {
-      case 1: return launch_prefill_t<128, 1>(a, s);
-      case 2: return launch_prefill_t<128, 2>(a, s);
-      case 4: return launch_prefill_t<128, 4>(a, s);
-      case 8: return launch_prefill_t<128, 8>(a, s);
-    }
-  } else if (D == 64) {
-    switch (G) {
-      case 1: return launch_prefill_t<64, 1>(a, s);
-      case 2: return launch_prefill_t<64, 2>(a, s);
-      case 4: return launch_prefill_t<64, 4>(a, s);
-      case 8: return launch_prefill_t<64, 8>(a, s);
-    }
+template <int D, int B>
+static hipError_t launch_prefill_g(int G, const AttnArgs& a, hipStream_t s) {
+  switch (G) {
+    case 1: return launch_prefill_t<D, B, 1>(a, s);
+    case 2: return launch_prefill_t<D, B, 2>(a, s);
+    case 4: return launch_prefill_t<D, B, 4>(a, s);
+    case 8: return launch_prefill_t<D, B, 8>(a, s);
   }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s) {
+  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16>(G, a, s);
+  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32>(G, a, s);
+  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16>(G, a, s);
+  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32>(G, a, s);
   return hipErrorInvalidValue;
 }
 

@@ -1,0 +1,188 @@
+"""Host-only checks of libcpattn: exported symbols, validation error codes and
+exact coverage of the planner's work items.  Nothing here launches a kernel."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_09061_amd as cp
+from paper_2606_09061_amd import binding
+from workloads import make_batch, make_config, replay_schedule
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "cp_attn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(cp_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = binding.load()
+    names = header_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in cp_attn.h but not exported"
+    assert sorted(binding.exported_symbols()) == names
+
+
+def test_version_and_strerror():
+    assert cp.version() == 10000
+    for code in (0, -1, -2, -3, -4, -5):
+        assert binding.strerror(code) != "unknown error"
+    assert binding.strerror(-99) == "unknown error"
+
+
+def _desc(**kw):
+    base = dict(num_q_heads=32, num_kv_heads=8, head_dim=128, block_size=16, num_blocks=100,
+                max_blocks_per_req=10, num_reqs_in_table=4, sm_scale=0.088)
+    base.update(kw)
+    return cp.make_desc(**base)
+
+
+GOOD_ROWS = np.array([[0, 10, 5, 15], [1, 0, 1, 1]], np.int32)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(num_q_heads=0), binding.CP_ERR_INVALID_ARG),
+    (dict(num_blocks=0), binding.CP_ERR_INVALID_ARG),
+    (dict(num_q_heads=12, num_kv_heads=8), binding.CP_ERR_BAD_META),
+    (dict(sm_scale=float("nan")), binding.CP_ERR_BAD_META),
+    (dict(sm_scale=-1.0), binding.CP_ERR_BAD_META),
+    (dict(head_dim=96), binding.CP_ERR_UNSUPPORTED),
+    (dict(block_size=8), binding.CP_ERR_UNSUPPORTED),
+    (dict(num_q_heads=48, num_kv_heads=3), binding.CP_ERR_UNSUPPORTED),
+    (dict(num_q_heads=32, num_kv_heads=2), binding.CP_ERR_UNSUPPORTED),
+])
+def test_desc_validation(kw, code):
+    assert cp.check_batch(_desc(**kw), GOOD_ROWS) == code
+
+
+@pytest.mark.parametrize("row,code", [
+    ([0, 10, -1, 9], binding.CP_ERR_BAD_META),     # negative chunk
+    ([0, -1, 2, 1], binding.CP_ERR_BAD_META),      # negative start
+    ([0, 10, 5, 16], binding.CP_ERR_BAD_META),     # ctx != start + len
+    ([0, 150, 20, 170], binding.CP_ERR_BAD_META),  # ctx beyond the table capacity (160)
+    ([7, 0, 1, 1], binding.CP_ERR_BAD_META),       # req out of range
+    ([-1, 0, 1, 1], binding.CP_ERR_BAD_META),
+    ([1, 3, 1, 4], binding.CP_ERR_BAD_META),       # duplicate req in one batch
+])
+def test_row_validation(row, code):
+    rows = np.array([[1, 0, 1, 1], row], np.int32)
+    assert cp.check_batch(_desc(), rows) == code
+
+
+def test_good_batch_and_empty_batch_validate():
+    assert cp.check_batch(_desc(), GOOD_ROWS) == 0
+    assert cp.check_batch(_desc(), np.zeros((0, 4), np.int32)) == 0
+
+
+def test_compute_calls_reject_before_touching_anything():
+    """Bad metadata, null pointers and short workspaces are refused on the host
+    (the pointers below are never dereferenced; no GPU is needed)."""
+    lib = binding.load()
+    d = _desc()
+    bad = np.array([[0, 10, 5, 16]], np.int32)
+    fake = 1 << 20  # never dereferenced
+    rc = lib.cp_attn_mixed(ctypes.byref(d), fake, fake, fake, fake, bad.ctypes.data, 1, fake,
+                           fake, 1 << 30, None)
+    assert rc == binding.CP_ERR_BAD_META
+    rc = lib.cp_kv_append(ctypes.byref(d), fake, fake, fake, fake, fake, bad.ctypes.data, 1,
+                          fake, 1 << 30, None)
+    assert rc == binding.CP_ERR_BAD_META
+    good = GOOD_ROWS
+    rc = lib.cp_attn_mixed(ctypes.byref(d), None, fake, fake, fake, good.ctypes.data, 2, fake,
+                           fake, 1 << 30, None)
+    assert rc == binding.CP_ERR_INVALID_ARG
+    rc = lib.cp_attn_mixed(ctypes.byref(d), fake + 2, fake, fake, fake, good.ctypes.data, 2,
+                           fake, fake, 1 << 30, None)
+    assert rc == binding.CP_ERR_INVALID_ARG  # misaligned q
+    need = cp.workspace_bytes(d, good)
+    rc = lib.cp_attn_mixed(ctypes.byref(d), fake, fake, fake, fake, good.ctypes.data, 2, fake,
+                           fake, need - 1, None)
+    assert rc == binding.CP_ERR_WORKSPACE
+    rc = lib.cp_kv_append(ctypes.byref(d), fake, fake, fake, fake, fake, good.ctypes.data, 2,
+                          fake, 0, None)
+    assert rc == binding.CP_ERR_WORKSPACE
+    # an empty batch succeeds without touching its (null) buffers
+    empty = np.zeros((0, 4), np.int32)
+    assert lib.cp_attn_mixed(ctypes.byref(d), None, None, None, None, empty.ctypes.data, 0, None,
+                             None, 0, None) == 0
+    assert lib.cp_kv_append(ctypes.byref(d), None, None, None, None, None, empty.ctypes.data, 0,
+                            None, 0, None) == 0
+
+
+def test_workspace_bytes_zero_for_invalid():
+    with pytest.raises(binding.CpError):
+        cp.workspace_bytes(_desc(head_dim=96), GOOD_ROWS)
+
+
+# ----------------------------------------------------------------- planner coverage
+
+def _check_coverage(batch):
+    d = cp.desc_for(batch)
+    items = cp.plan_items(d, batch.rows)
+    G = batch.group
+    Hkv = batch.num_kv_heads
+    off = batch.tok_offsets()
+    # token -> (row, position)
+    cover = {}
+    for kind, tok0, ntok, pos0, req, kvh, kb, ke in items.tolist():
+        assert 0 <= kvh < Hkv and ke > kb >= 0
+        for j in range(ntok):
+            cover.setdefault((tok0 + j, kvh), []).append((kind, kb, ke, pos0, ntok, req))
+    seen = set()
+    for r, (req, s, c, ctx) in enumerate(batch.rows.tolist()):
+        for j in range(c):
+            t = off[r] + j
+            p = s + j
+            for kvh in range(Hkv):
+                lst = cover.get((t, kvh))
+                assert lst, f"token {t} head {kvh} not covered"
+                seen.add((t, kvh))
+                kinds = {x[0] for x in lst}
+                assert kinds == ({0} if c >= 2 else {1})
+                assert all(x[5] == req for x in lst)
+                ranges = sorted((x[1], x[2]) for x in lst)
+                # the ranges partition [0, end) with p < end <= ctx
+                assert ranges[0][0] == 0
+                for a, b in zip(ranges, ranges[1:]):
+                    assert a[1] == b[0], f"gap/overlap {a} {b}"
+                end = ranges[-1][1]
+                assert p < end <= ctx
+                # every split holds a key the token may see
+                for kb, ke in ranges:
+                    assert kb <= p
+                if c == 1:
+                    assert end == ctx
+    assert seen == set(cover), "items cover tokens outside the batch"
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4])
+def test_plan_covers_every_query_exactly_once(n):
+    _check_coverage(make_config(n))
+
+
+def test_plan_coverage_replay_and_ragged():
+    batches, _ = replay_schedule()
+    for b in batches[::4]:
+        _check_coverage(b)
+    rng = np.random.default_rng(3)
+    for hq, hkv, d, bs in ((8, 8, 64, 16), (16, 2, 128, 32), (8, 1, 128, 16)):
+        rows = [(int(s), int(c)) for s, c in zip(rng.integers(0, 5000, 12),
+                                                  rng.integers(0, 700, 12))]
+        rows += [(0, 1), (31, 1), (4095, 1), (7, 0)]
+        _check_coverage(make_batch("ragged", hq, hkv, d, bs, rows, rng))
+
+
+def test_plan_summary_counts_consistent():
+    b = make_config(3)
+    s = cp.plan_summary(cp.desc_for(b), b.rows)
+    items = cp.plan_items(cp.desc_for(b), b.rows)
+    assert s["prefill_items"] + s["decode_items"] >= len(items)
+    assert s["workspace_bytes"] == cp.workspace_bytes(cp.desc_for(b), b.rows)
+    assert s["workspace_bytes"] >= s["partial_rows"] * (b.head_dim + 1) * 4

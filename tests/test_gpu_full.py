@@ -1,0 +1,124 @@
+"""Full-size GPU parity: the benchmark's mixes in the benchmark's launch
+configuration (same C ABI calls, same plans), checked against the fp64
+oracle.  Whole K/V pools are compared bit for bit after the append; outputs
+are compared on sampled (token, q head) pairs the oracle computes one by
+one: every decode row, the first/last token of every chunk and of every
+prefill tile, and a uniform random sample.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import assert_close, run_step, say, words
+from workloads import Batch, make_caches, make_config, make_step_tensors, make_tensors
+from workloads import replay_schedule
+
+pytestmark = pytest.mark.gpu
+
+
+def sample_pairs(batch, n_random=1500, seed=0):
+    Hq = batch.num_q_heads
+    tile = 128 // batch.group
+    off = batch.tok_offsets()
+    toks = set()
+    for r, (req, s, c, ctx) in enumerate(batch.rows.tolist()):
+        if c == 0:
+            continue
+        for j in (0, c - 1, tile - 1, tile, c // 2):
+            if 0 <= j < c:
+                toks.add(int(off[r] + j))
+    sel = {t * Hq + h for t in toks for h in range(Hq)}
+    rng = np.random.default_rng(seed)
+    total = batch.num_tokens * Hq
+    sel |= set(rng.choice(total, size=min(total, n_random), replace=False).tolist())
+    return np.array(sorted(sel), dtype=np.int64)
+
+
+def check_sampled(batch, out_gpu, q_host, kc_ref, vc_ref, what, seed=0):
+    sel = sample_pairs(batch, seed=seed)
+    ref = oracle.attn(batch, q_host, kc_ref, vc_ref, sel=sel)
+    got = out_gpu.reshape(-1, batch.head_dim)[torch.from_numpy(sel).to(out_gpu.device)]
+    return assert_close(got, ref, f"{what} ({len(sel)} sampled rows)")
+
+
+@pytest.mark.parametrize("n", [2, 3, 4])
+def test_full_size_mix(n):
+    batch = make_config(n)
+    say(f"[gpu] mix {n}: rows={batch.n_rows} T={batch.num_tokens} blocks={batch.num_blocks}")
+    dev = torch.device("cuda", 0)
+    t = make_tensors(batch, seed=7000 + n, device=dev)
+    host = {k: v.cpu() for k, v in t.items() if k in ("q", "k_new", "v_new")}
+    kc0, vc0 = words(t["k_cache"]), words(t["v_cache"])
+    out = run_step(batch, t)
+    torch.cuda.synchronize()
+    kc_ref, vc_ref = oracle.kv_append(batch, host["k_new"], host["v_new"], kc0, vc0)
+    del kc0, vc0
+    assert np.array_equal(words(t["k_cache"]).reshape(-1), kc_ref.reshape(-1)), "K pool differs"
+    assert np.array_equal(words(t["v_cache"]).reshape(-1), vc_ref.reshape(-1)), "V pool differs"
+    check_sampled(batch, out, host["q"], kc_ref, vc_ref, f"mix {n}")
+
+
+def test_replay_twenty_iterations_lockstep():
+    batches, info = replay_schedule()
+    dev = torch.device("cuda", 0)
+    kc, vc = make_caches(batches[0], device=dev, fill_prior=False)
+    kc_ref, vc_ref = words(kc), words(vc)
+    for i, b in enumerate(batches):
+        q, kn, vn, _ = make_step_tensors(b, 9000 + i, dev)
+        t = {"q": q, "k_new": kn, "v_new": vn, "k_cache": kc, "v_cache": vc,
+             "block_tables": torch.from_numpy(b.block_tables).to(dev)}
+        say(f"[gpu] replay iteration {i}: rows={b.n_rows} T={b.num_tokens}")
+        out = run_step(b, t)
+        torch.cuda.synchronize()
+        kc_ref, vc_ref = oracle.kv_append(b, kn.cpu(), vn.cpu(), kc_ref, vc_ref)
+        check_sampled(b, out, q.cpu(), kc_ref, vc_ref, f"replay it {i}", seed=i)
+        if i in (0, 9, 19):
+            assert np.array_equal(words(kc).reshape(-1), kc_ref.reshape(-1)), f"K pool it {i}"
+            assert np.array_equal(words(vc).reshape(-1), vc_ref.reshape(-1)), f"V pool it {i}"
+
+
+def test_block_ids_beyond_2g_elements():
+    """Blocks whose element offset exceeds 2^31 (pool > 4 GiB per cache)."""
+    hq, hkv, d, bsz = 32, 8, 128, 16
+    per_block = hkv * bsz * d
+    nb = (1 << 31) // per_block + 4096              # 135168 blocks, 4.4 GB per cache
+    rows = [(3000, 200), (5000, 1), (777, 1), (0, 40)]
+    rng = np.random.default_rng(21)
+    need = [-(-(s + c) // bsz) for s, c in rows]
+    ids = rng.permutation(np.arange(nb - 2048, nb - 1))[: sum(need)]  # beyond 2^31 elements
+    assert ids.min() * per_block > (1 << 31)
+    mbr = max(need)
+    bt = np.full((len(rows), mbr), nb - 1, np.int32)
+    k = 0
+    rr = np.zeros((len(rows), 4), np.int32)
+    for i, (s, c) in enumerate(rows):
+        bt[i, : need[i]] = ids[k: k + need[i]]
+        k += need[i]
+        rr[i] = (i, s, c, s + c)
+    big = Batch("bigpool", hq, hkv, d, bsz, rr, bt, nb, nb - 1)
+    # the oracle sees the same data through a compact pool (block ids remapped)
+    remap = {int(b): j for j, b in enumerate(ids)}
+    bt_small = np.vectorize(lambda x: remap.get(int(x), 0))(bt).astype(np.int32)
+    small = Batch("compact", hq, hkv, d, bsz, rr, bt_small, len(ids), 0)
+    ref_t = make_tensors(small, seed=555)           # compact pool holds every referenced block
+    dev = torch.device("cuda", 0)
+    say(f"[gpu] big pool: {nb} blocks, max element offset {int(ids.max()) * per_block:.3e}")
+    kc = torch.full((nb, hkv, bsz, d), float("nan"), dtype=torch.bfloat16, device=dev)
+    vc = torch.full((nb, hkv, d, bsz), float("nan"), dtype=torch.bfloat16, device=dev)
+    idx = torch.from_numpy(ids.astype(np.int64)).to(dev)
+    kc[idx] = ref_t["k_cache"].to(dev)
+    vc[idx] = ref_t["v_cache"].to(dev)
+    t = {"q": ref_t["q"].to(dev), "k_new": ref_t["k_new"].to(dev), "v_new": ref_t["v_new"].to(dev),
+         "k_cache": kc, "v_cache": vc, "block_tables": torch.from_numpy(bt).to(dev)}
+    out = run_step(big, t)
+    torch.cuda.synchronize()
+    kc_ref, vc_ref = oracle.kv_append(small, ref_t["k_new"], ref_t["v_new"], ref_t["k_cache"],
+                                      ref_t["v_cache"])
+    assert np.array_equal(words(kc[idx]).reshape(-1), kc_ref.reshape(-1))
+    assert np.array_equal(words(vc[idx]).reshape(-1), vc_ref.reshape(-1))
+    assert bool(torch.isnan(kc[nb - 1].float()).all()), "poison block written"
+    assert bool(torch.isnan(vc[nb - 1].float()).all()), "poison block written"
+    ref = oracle.attn(small, ref_t["q"], kc_ref, vc_ref)
+    assert_close(out, ref, "big pool")

@@ -15,4 +15,4 @@ from .configs import (  # noqa: F401
     replay_schedule,
     tiny_batch,
 )
-from .tensors import make_tensors, make_step_tensors  # noqa: F401
+from .tensors import make_caches, make_step_tensors, make_tensors  # noqa: F401

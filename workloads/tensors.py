@@ -61,7 +61,7 @@ def make_step_tensors(batch, seed, device="cpu"):
 def make_caches(batch, gen=None, device="cpu", fill_prior=True, poison=True, seed=None):
     """K and V pools: N(0,1) prior context (or all NaN if ``fill_prior`` is False),
     NaN in unreferenced blocks and in every slot at or past each row's chunk_start."""
-    if gen is None:
+    if gen is None and fill_prior:
         gen = torch.Generator(device=device)
         gen.manual_seed(int(seed))
     NB, Hkv, B, D = batch.num_blocks, batch.num_kv_heads, batch.block_size, batch.head_dim
