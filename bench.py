@@ -267,6 +267,19 @@ CONFIG_NAMES_SHORT = {1: "tiny", 2: "llama3-8b-budget512", 3: "llama3-8b-prefill
                       4: "llama3-8b-decode-dominated", 5: "llama-70b-replay"}
 
 
+def copy_calibration(mib, reps):
+    """Plain device-to-device copies of a known size, for scaling the HBM byte
+    counters (FETCH_SIZE / WRITE_SIZE) of a profiler run."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_per_launch": n, "launches": reps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -276,7 +289,12 @@ def main():
     ap.add_argument("--all", action="store_true", help="one JSON line per mix")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run plain copies of MIB MiB (counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, args.steps)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the attention step is "
               "measured on a single MI355X; a multi-GPU run would shard heads across GPUs with "

@@ -148,6 +148,9 @@ void serialize(const Plan& p, std::vector<uint8_t>& buf) {
   if (!p.prefill.empty())
     std::memcpy(buf.data() + p.off_prefill, p.prefill.data(),
                 p.prefill.size() * sizeof(PrefillItem));
+  if (!p.prefill_wide.empty())
+    std::memcpy(buf.data() + p.off_prefill_wide, p.prefill_wide.data(),
+                p.prefill_wide.size() * sizeof(PrefillItem));
   if (!p.decode.empty())
     std::memcpy(buf.data() + p.off_decode, p.decode.data(), p.decode.size() * sizeof(DecodeItem));
   if (!p.merge.empty())
@@ -197,7 +200,7 @@ int cp_plan_summary(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
   try {
     Plan p;
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
-    counts[0] = (int64_t)p.prefill.size();
+    counts[0] = (int64_t)(p.prefill.size() + p.prefill_wide.size());
     counts[1] = (int64_t)p.decode.size();
     counts[2] = (int64_t)p.merge.size();
     counts[3] = p.partial_rows;
@@ -227,8 +230,10 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
       }
       ++n;
     };
-    for (const PrefillItem& it : p.prefill)
-      if (it.n_tok > 0) put(0, it.tok0, it.n_tok, it.pos0, it.req, it.kvh, it.kv_begin, it.kv_end);
+    for (const auto* lst : {&p.prefill_wide, &p.prefill})
+      for (const PrefillItem& it : *lst)
+        if (it.n_tok > 0)
+          put(0, it.tok0, it.n_tok, it.pos0, it.req, it.kvh, it.kv_begin, it.kv_end);
     for (const DecodeItem& it : p.decode) {
       // position of the decode query: its row's ctx_len - 1, recovered from the row
       int32_t pos = -1;
@@ -307,6 +312,8 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
     AttnArgs a;
     a.prefill = reinterpret_cast<const PrefillItem*>(base + p.off_prefill);
     a.n_prefill = (int)p.prefill.size();
+    a.prefill_wide = reinterpret_cast<const PrefillItem*>(base + p.off_prefill_wide);
+    a.n_prefill_wide = (int)p.prefill_wide.size();
     a.decode = reinterpret_cast<const DecodeItem*>(base + p.off_decode);
     a.n_decode = (int)p.decode.size();
     a.merge = reinterpret_cast<const MergeGroup*>(base + p.off_merge);
@@ -325,7 +332,7 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
     a.scale_log2 = desc->sm_scale * 1.4426950408889634f;
     const int D = desc->head_dim;
     const int G = desc->num_q_heads / desc->num_kv_heads;
-    if (a.n_prefill > 0) {
+    if (a.n_prefill > 0 || a.n_prefill_wide > 0) {
       const long pi = prof_open(1, s);
       const hipError_t e = launch_prefill(D, G, a, s);
       prof_close(pi, s);

@@ -20,8 +20,10 @@ struct AppendArgs {
 };
 
 struct AttnArgs {
-  const PrefillItem* prefill;
+  const PrefillItem* prefill;       // 128-row tiles (4-wave kernel)
   int n_prefill;
+  const PrefillItem* prefill_wide;  // 256-row tiles (8-wave kernel)
+  int n_prefill_wide;
   const DecodeItem* decode;
   int n_decode;
   const MergeGroup* merge;

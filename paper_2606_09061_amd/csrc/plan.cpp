@@ -139,17 +139,20 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   // ---- prefill tiles --------------------------------------------------
   struct Tile {
     int32_t tok0, n_tok, pos0, req, kv_end;
+    bool wide;
   };
   std::vector<Tile> tiles;
   int64_t pf_cost = 0;  // in kPrefillKeys-key steps, summed over tiles and kv heads
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len < t.prefill_min_len) continue;
-    for (int32_t j = 0; j < m.chunk_len; j += tile_tok) {
-      const int32_t n = std::min<int32_t>(tile_tok, m.chunk_len - j);
-      Tile tl{(int32_t)(off[r] + j), n, m.chunk_start + j, m.req_id, m.chunk_start + j + n};
+    const bool wide = (int64_t)m.chunk_len * G > kPrefillRows;
+    const int32_t tt = wide ? kPrefillRowsWide / G : tile_tok;
+    for (int32_t j = 0; j < m.chunk_len; j += tt) {
+      const int32_t n = std::min<int32_t>(tt, m.chunk_len - j);
+      Tile tl{(int32_t)(off[r] + j), n, m.chunk_start + j, m.req_id, m.chunk_start + j + n, wide};
       tiles.push_back(tl);
-      pf_cost += ceil_div(tl.kv_end, kPrefillKeys) * Hkv;
+      pf_cost += ceil_div(tl.kv_end, kPrefillKeys) * Hkv * (wide ? 2 : 1);
     }
   }
   // Key ranges longer than split_keys are cut on a grid of multiples of
@@ -166,7 +169,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     int64_t cost;
     int64_t group;  // items sharing (request, kv head, key range start)
   };
-  std::vector<PfTmp> pf;
+  std::vector<PfTmp> pf, pfw;
   std::vector<int32_t> bounds;
   for (const Tile& tl : tiles) {
     const int64_t last_cut = (tl.pos0 / kPrefillKeys) * (int64_t)kPrefillKeys;
@@ -193,12 +196,13 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
         it.part = ns > 1 ? part0 + (int32_t)(s * tl.n_tok * G) : -1;
         // group id: request, kv head and split start (split starts are grid points)
         const int64_t gid = (((int64_t)tl.req * Hkv + kvh) << 20) + bounds[s] / split_keys;
-        pf.push_back({it, ceil_div(it.kv_end - it.kv_begin, kPrefillKeys), gid});
+        (tl.wide ? pfw : pf).push_back({it, ceil_div(it.kv_end - it.kv_begin, kPrefillKeys), gid});
       }
       if (ns > 1) add_merge(p, tl.tok0, tl.n_tok, kvh, (int32_t)ns, part0, G, d.head_dim);
     }
   }
   order_for_xcds(pf, t.num_xcds, p.prefill);
+  order_for_xcds(pfw, t.num_xcds, p.prefill_wide);
 
   // ---- decode ranges --------------------------------------------------
   int64_t dec_blocks = 0;
@@ -257,6 +261,8 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   size_t o = 0;
   p.off_prefill = o;
   o = align_up(o + p.prefill.size() * sizeof(PrefillItem), 256);
+  p.off_prefill_wide = o;
+  o = align_up(o + p.prefill_wide.size() * sizeof(PrefillItem), 256);
   p.off_decode = o;
   o = align_up(o + p.decode.size() * sizeof(DecodeItem), 256);
   p.off_merge = o;

@@ -17,10 +17,11 @@
 
 namespace cpattn {
 
-// Query rows per prefill workgroup: 4 waves x 32 rows.  A row is one
-// (query token, q head) pair of a single kv-head group, so a tile holds
-// kPrefillRows / G tokens of one chunk.
+// Query rows per prefill workgroup: 4 waves x 32 rows, or 8 waves x 32 rows
+// for chunks with more rows than that.  A row is one (query token, q head)
+// pair of a single kv-head group, so a tile holds rows / G tokens of a chunk.
 constexpr int kPrefillRows = 128;
+constexpr int kPrefillRowsWide = 256;
 // Keys per prefill main-loop iteration.
 constexpr int kPrefillKeys = 64;
 // Waves per decode workgroup (each wave walks every kDecodeWaves-th block).
@@ -75,13 +76,15 @@ struct Tuning {
 };
 
 struct Plan {
-  std::vector<PrefillItem> prefill;
+  std::vector<PrefillItem> prefill;       // 128-row tiles
+  std::vector<PrefillItem> prefill_wide;  // 256-row tiles
   std::vector<DecodeItem> decode;
   std::vector<MergeGroup> merge;
   int64_t partial_rows = 0;
   int32_t decode_split_blocks = 0;
   // workspace layout (byte offsets from the workspace base)
-  size_t off_prefill = 0, off_decode = 0, off_merge = 0, off_part_o = 0, off_part_lse = 0;
+  size_t off_prefill = 0, off_prefill_wide = 0, off_decode = 0, off_merge = 0, off_part_o = 0,
+         off_part_lse = 0;
   size_t plan_bytes = 0;   // bytes of the uploaded item lists
   size_t ws_bytes = 0;     // total workspace
 };

@@ -4,13 +4,12 @@
 // queries over s prior keys costs ~c*s + c^2/2 query-key pairs per head (the
 // prefill_interaction feature of Table 2 tracks exactly that product).
 //
-// Work item: a tile of up to 128 query rows of one chunk, where a row is a
+// Work item: a tile of up to 32*NW query rows of one chunk, where a row is a
 // (token, q head) pair of the G q heads that share one kv head, so K and V
-// are loaded once for all G heads (GQA sharing); plus a key range.  Four
-// waves own 32 rows each.  Per 64-key step the workgroup gathers the K rows
-// and the feature-major V blocks of the step through the block table into
-// a double-buffered LDS tile (the next step's global loads are in flight
-// while the current one is multiplied), then each wave computes
+// are gathered once for all G heads (GQA sharing); plus a key range.  Each
+// of the NW waves owns 32 rows.  Per 64-key step the workgroup gathers the K
+// rows and the feature-major V blocks of the step through the block table
+// into an LDS tile; each wave then computes
 //     S^T (64 keys x 32 queries) = K . Q^T      MFMA, fp32 accumulators
 //     online softmax down each query column     fp32, base 2
 //     O^T (D x 32 queries)     += V^T . P^T     MFMA, P rounded to bf16
@@ -20,6 +19,14 @@
 // makes the score registers of a lane exactly the B operand of the P.V step,
 // so probabilities never leave registers.  Only steps that cross the causal
 // diagonal or the end of the range apply a mask.
+//
+// Pipeline: two LDS tiles and two register sets.  The global loads of step
+// s+2 are issued at the start of step s and written to LDS at the end of
+// step s+1, so every gather has two steps of MFMA work to arrive.  Block ids
+// are wave-uniform for every load instruction (a wave's 64 lanes read one
+// block), so the block base is computed once per wave in scalar registers.
+// LDS rows are XOR-swizzled in 16-byte units instead of padded so that the
+// MFMA operand reads of 16 consecutive lanes hit distinct banks.
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -40,32 +47,54 @@ __device__ __forceinline__ int acc_key(int r, int g) {
   return 16 * ((r >> 3) & 1) + 8 * g + 4 * ((r >> 2) & 1) + (r & 3);
 }
 
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
 }  // namespace
 
-template <int D>
-struct PrefillSmem {
-  static constexpr int KS = D * 2 + 16;   // bytes per K row (padded)
-  static constexpr int VS = BN * 2 + 16;  // bytes per V^T feature row (padded)
-  static constexpr int K_BYTES = BN * KS;
-  static constexpr int V_BYTES = D * VS;
+template <int D, int B>
+struct PrefillLayout {
+  static constexpr int KCH = D / 8;          // 16-byte chunks per K row
+  static constexpr int K_BYTES = BN * D * 2;
+  static constexpr int V_BYTES = BN * D * 2;
   static constexpr int BUF = K_BYTES + V_BYTES;
-  static constexpr int TOTAL = 2 * BUF;
+  static constexpr int KV_TOTAL = 2 * BUF;
+  // query rows staged in LDS (wide tiles only): row r, chunk c -> byte offset
+  __device__ static int q_off(int r, int c) {
+    return KV_TOTAL + r * D * 2 + ((c ^ (r & (KCH - 1))) << 4);
+  }
+  static constexpr int VSLOTS = B / 8;       // 16-byte slots per V^T row
+  // K row `key`, chunk c -> byte offset
+  __device__ static int k_off(int key, int c) {
+    return key * D * 2 + ((c ^ (sigma(key & 15) & (KCH - 1))) << 4);
+  }
+  // V^T of step-block bi, feature row d, slot s (8 keys) -> byte offset
+  __device__ static int v_off(int bi, int d, int s) {
+    const int h = B == 16 ? (((d >> 2) ^ (d >> 3)) & 1) : ((d >> 2) & 3);
+    return K_BYTES + bi * D * B * 2 + d * B * 2 + ((s ^ h) << 4);
+  }
 };
 
-template <int D, int B, int G>
-__global__ __launch_bounds__(256, 2) void prefill_kernel(
+template <int D, int B, int G, int NW>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
     const PrefillItem* __restrict__ items, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
-  using SM = PrefillSmem<D>;
+  using L = PrefillLayout<D, B>;
+  // Wide (8-wave) tiles keep the query operand in LDS and double the
+  // register staging of the gather (two steps in flight); 4-wave tiles keep
+  // the query operand in registers with one step in flight.
+  constexpr bool kWide = NW == 8;
+  constexpr int NT = NW * 64;                   // threads
   constexpr int NKS = D / 16;                   // k-steps of S^T
   constexpr int NDT = D / 32;                   // 32-feature tiles of O^T
-  constexpr int CH = BN * D * 2 / (256 * 16);   // 16-byte chunks per thread per K (and V) step
-  constexpr int KCH = D / 8;                    // 16-byte chunks per K row
+  constexpr int KCH = L::KCH;
+  constexpr int CK = BN * KCH / NT;             // K chunks per thread per step
   constexpr int VPB = D * B / 8;                // 16-byte chunks per V block (one kv head)
+  constexpr int CV = BN * D / 8 / NT;           // V chunks per thread per step
   constexpr int LOG2B = B == 16 ? 4 : 5;
   static_assert(B == 16 || B == 32, "block size");
+  static_assert(CK >= 1 && CV >= 1, "tile geometry");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const PrefillItem it = items[blockIdx.x];
@@ -86,75 +115,92 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
   const uint16_t* vbase = v_cache + (int64_t)it.kvh * B * D;
 
   // Q^T operand: lane holds features [16 ks + 8 g, +8) of its query row
-  uint4 qreg[NKS];
-  {
+  uint4 qreg[kWide ? 1 : NKS];
+  if constexpr (kWide) {
+    // stage the tile's query rows in LDS: chunk x -> row x / KCH, chunk x % KCH
+#pragma unroll
+    for (int i = 0; i < NW * 32 * KCH / NT; ++i) {
+      const int x = i * NT + tid;
+      const int r = x / KCH;
+      const int t = r / G;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (t < it.n_tok)
+        v = ld_global16(q + ((int64_t)(it.tok0 + t) * hq + it.kvh * G + r % G) * D + (x % KCH) * 8);
+      *reinterpret_cast<uint4*>(smem + L::q_off(r, x % KCH)) = v;
+    }
+  } else {
     const uint16_t* qp =
         q + ((int64_t)(it.tok0 + (row_valid ? tl : 0)) * hq + it.kvh * G + hh) * D + g * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
       qreg[ks] = row_valid ? ld_global16(qp + ks * 16) : make_uint4(0, 0, 0, 0);
   }
+  auto qop = [&](int ks) -> uint4 {
+    if constexpr (kWide)
+      return *reinterpret_cast<const uint4*>(smem + L::q_off(row, 2 * ks + g));
+    else
+      return qreg[ks];
+  };
 
-  // ---- gather geometry of 16-byte chunk c of this thread (shifts and masks
-  // only: every divisor below is a compile-time power of two)
-  //   K chunk: key kkey(c) of the step, feature chunk x % KCH
-  //   V chunk: block x / VPB of the step, feature row d, 8 keys from slot s0
-  auto kkey = [&](int c) { return (c * 256 + tid) / KCH; };
-  auto kgoff = [&](int c) { return (kkey(c) & (B - 1)) * D + ((c * 256 + tid) % KCH) * 8; };
-  auto klds = [&](int c) { return kkey(c) * SM::KS + ((c * 256 + tid) % KCH) * 16; };
-  auto vblk = [&](int c) { return (c * 256 + tid) / VPB; };
-  auto vd = [&](int c) { return ((c * 256 + tid) % VPB) / (B / 8); };
-  auto vs0 = [&](int c) { return (((c * 256 + tid) % VPB) % (B / 8)) * 8; };
-  auto vkey = [&](int c) { return vblk(c) * B + vs0(c); };
-  auto vgoff = [&](int c) { return vd(c) * B + vs0(c); };
-  auto vlds = [&](int c) { return vd(c) * SM::VS + vkey(c) * 2; };
-
-  uint4 kreg[CH], vreg[CH];
-  auto gload = [&](int k0) {
+  // ---- gather geometry: K chunk i of this thread is x = i*NT + tid
+  // (key x / KCH, chunk x % KCH); V chunk i is x = i*NT + tid (step-block
+  // x / VPB, feature row, 8-key slot).  All of a wave's lanes read one block.
+  struct Regs {
+    uint4 k[CK], v[CV];
+  };
+  auto gload = [&](Regs& r, int k0) {
     const int b0 = k0 >> LOG2B;
-    if (k0 + BN <= it.kv_end) {
+    const bool full = k0 + BN <= it.kv_end;
 #pragma unroll
-      for (int c = 0; c < CH; ++c) {
-        const int64_t kb = bt_row[b0 + (kkey(c) >> LOG2B)];
-        kreg[c] = ld_global16(kbase + kb * blk_elems + kgoff(c));
-        const int64_t vb = bt_row[b0 + vblk(c)];
-        vreg[c] = ld_global16(vbase + vb * blk_elems + vgoff(c));
+    for (int i = 0; i < CK; ++i) {
+      const int x = i * NT + tid;
+      const int key = x / KCH;
+      const int kb = uniform(key) >> LOG2B;       // block of this wave's keys
+      const bool live = full || (k0 + uniform(key) < it.kv_end);
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (live) {
+        const int64_t blk = bt_row[b0 + kb];
+        val = ld_global16(kbase + blk * blk_elems + (key & (B - 1)) * D + (x % KCH) * 8);
       }
-    } else {  // last step of the range: keys at or past kv_end are zero
+      r.k[i] = val;
+    }
 #pragma unroll
-      for (int c = 0; c < CH; ++c) {
-        uint4 kv = make_uint4(0, 0, 0, 0);
-        if (k0 + kkey(c) < it.kv_end) {
-          const int64_t kb = bt_row[b0 + (kkey(c) >> LOG2B)];
-          kv = ld_global16(kbase + kb * blk_elems + kgoff(c));
-        }
-        kreg[c] = kv;
-        uint4 vv = make_uint4(0, 0, 0, 0);
-        const int vpos = k0 + vkey(c);
-        if (vpos < it.kv_end) {
-          const int64_t vb = bt_row[b0 + vblk(c)];
-          vv = ld_global16(vbase + vb * blk_elems + vgoff(c));
-          if (vpos + 8 > it.kv_end) {
-            uint32_t* w = reinterpret_cast<uint32_t*>(&vv);
+    for (int i = 0; i < CV; ++i) {
+      const int x = i * NT + tid;
+      const int bi = uniform(x / VPB);
+      const int w = x % VPB;
+      const int d = w / L::VSLOTS;
+      const int s = w % L::VSLOTS;
+      const int vpos = k0 + bi * B + s * 8;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (full || k0 + bi * B < it.kv_end) {
+        const int64_t blk = bt_row[b0 + bi];
+        val = ld_global16(vbase + blk * blk_elems + d * B + s * 8);
+        if (!full && vpos + 8 > it.kv_end) {  // zero values of keys past the range
+          uint32_t* wv = reinterpret_cast<uint32_t*>(&val);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const uint32_t lo = (vpos + 2 * e) < it.kv_end ? 0x0000ffffu : 0u;
-              const uint32_t hi = (vpos + 2 * e + 1) < it.kv_end ? 0xffff0000u : 0u;
-              w[e] &= (lo | hi);
-            }
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t lo = (vpos + 2 * e) < it.kv_end ? 0x0000ffffu : 0u;
+            const uint32_t hi = (vpos + 2 * e + 1) < it.kv_end ? 0xffff0000u : 0u;
+            wv[e] &= (lo | hi);
           }
         }
-        vreg[c] = vv;
       }
+      r.v[i] = val;
     }
   };
-  auto sstore = [&](int buf) {
-    uint8_t* kb = smem + buf * SM::BUF;
-    uint8_t* vb = kb + SM::K_BYTES;
+  auto sstore = [&](const Regs& r, int buf) {
+    uint8_t* base = smem + buf * L::BUF;
 #pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      *reinterpret_cast<uint4*>(kb + klds(c)) = kreg[c];
-      *reinterpret_cast<uint4*>(vb + vlds(c)) = vreg[c];
+    for (int i = 0; i < CK; ++i) {
+      const int x = i * NT + tid;
+      *reinterpret_cast<uint4*>(base + L::k_off(x / KCH, x % KCH)) = r.k[i];
+    }
+#pragma unroll
+    for (int i = 0; i < CV; ++i) {
+      const int x = i * NT + tid;
+      const int w = x % VPB;
+      *reinterpret_cast<uint4*>(base + L::v_off(x / VPB, w / L::VSLOTS, w % L::VSLOTS)) = r.v[i];
     }
   };
 
@@ -165,51 +211,53 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
   float m_run = -INFINITY;  // running max of the scaled (base-2) scores
   float l_run = 0.f;
-
-  const int n_step = (it.kv_end - it.kv_begin + BN - 1) / BN;
-  gload(it.kv_begin);
-  sstore(0);
-  __syncthreads();
-
   const int krow0 = sigma(col);
-  for (int st = 0; st < n_step; ++st) {
-    const int cur = st & 1;
-    const int k0 = it.kv_begin + st * BN;
-    const bool has_next = st + 1 < n_step;
-    if (has_next) gload(k0 + BN);
 
-    const uint8_t* kb = smem + cur * SM::BUF;
-    const uint8_t* vb = kb + SM::K_BYTES;
-
-    // ---- S^T = K . Q^T for two 32-key sub-tiles
+  // MFMA loops: operand reads run kRing MFMAs ahead through a register ring;
+  // scheduling fences keep that order (left alone, the scheduler trades the
+  // ring for registers and waits on every read).
+  constexpr int kRing = 4;
+  auto compute = [&](int buf, int k0) {
+    const uint8_t* base = smem + buf * L::BUF;
+    // ---- S^T = K . Q^T: MFMA i uses k-step i / 2 and 32-key sub-tile i % 2
+    constexpr int NQK = 2 * NKS;
+    auto kop = [&](int i) {
+      return *reinterpret_cast<const uint4*>(base + L::k_off((i & 1) * 32 + krow0, 2 * (i >> 1) + g));
+    };
     f32x16_t sacc[2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
+    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[kt][r] = 0.f;
-      const uint8_t* ka = kb + (kt * 32 + krow0) * SM::KS + g * 16;
+    {
+      uint4 ring[kRing];
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const uint4 a = *reinterpret_cast<const uint4*>(ka + ks * 32);
-        sacc[kt] = mfma32x32x16(a, qreg[ks], sacc[kt]);
+      for (int i = 0; i < kRing; ++i) ring[i] = kop(i);
+#pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        const uint4 a = ring[i % kRing];
+        if (i + kRing < NQK) ring[i % kRing] = kop(i + kRing);
+        sacc[i & 1] = mfma32x32x16(a, qop(i >> 1), sacc[i & 1]);
+        __builtin_amdgcn_sched_barrier(0);  // keep reads kRing MFMAs ahead
       }
     }
-
-    // ---- online softmax down this lane's query column (raw scores; the
-    // scale is folded into the exponent)
-    if ((k0 + BN - 1 > it.pos0) || (k0 + BN > it.kv_end)) {
-      const int lim = min(qpos + 1, it.kv_end) - k0;  // keys [k0, k0 + lim) are visible
+    // ---- online softmax on raw scores (the scale is folded into exp2)
+    const bool edge = (k0 + BN - 1 > it.pos0) || (k0 + BN > it.kv_end);
+    if (edge) {
+      // keys [k0, k0 + lim) are visible; register r of half g holds key
+      // kt*32 + acc_key(r, 0) + 8*g, so compare against lim - 8*g
+      const int limg = min(qpos + 1, it.kv_end) - k0 - 8 * g;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (kt * 32 + acc_key(r, g) >= lim) sacc[kt][r] = -INFINITY;
+          if (kt * 32 + acc_key(r, 0) >= limg) sacc[kt][r] = -INFINITY;
     }
     float mt = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[kt][r]);
+      for (int r = 0; r < 16; r += 2) mt = fmaxf(fmaxf(mt, sacc[kt][r]), sacc[kt][r + 1]);
     mt = fmaxf(mt, shfl_xor_f(mt, 32)) * scale_log2;
     if (__builtin_amdgcn_ballot_w64(mt > m_run + kRescaleThreshold)) {
       const float mnew = fmaxf(m_run, mt);
@@ -223,33 +271,80 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
     }
     const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
     uint4 pk[2][2];
+    const uint32_t ones = 0x3f803f80u;  // bf16 pair (1, 1)
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
-        float p[8];
+        uint32_t w[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][8 * h2 + e], scale_log2, neg_m));
-          l_run += p[e];
+        for (int e = 0; e < 4; ++e) {
+          const float p0 =
+              __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][8 * h2 + 2 * e], scale_log2, neg_m));
+          const float p1 = __builtin_amdgcn_exp2f(
+              __builtin_fmaf(sacc[kt][8 * h2 + 2 * e + 1], scale_log2, neg_m));
+          w[e] = pack_bf16x2(p0, p1);
+          l_run = dot2_bf16(w[e], ones, l_run);  // sum of the rounded weights
         }
-        pk[kt][h2] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                                pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+        pk[kt][h2] = make_uint4(w[0], w[1], w[2], w[3]);
       }
-
-    // ---- O^T += V^T . P^T
+    // values of keys past the range were zeroed by the gather
+    // ---- O^T += V^T . P^T: MFMA i uses key step i / NDT and feature tile i % NDT
+    constexpr int NPV = 4 * NDT;
+    auto vop = [&](int i) {
+      const int ks2 = i / NDT, dt = i % NDT;
+      return *reinterpret_cast<const uint4*>(
+          base + L::v_off((ks2 * 16) / B, dt * 32 + col, ((ks2 * 16) % B) / 8 + g));
+    };
+    {
+      uint4 ring[kRing];
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-      const uint8_t* va = vb + (dt * 32 + col) * SM::VS + g * 16;
+      for (int i = 0; i < kRing; ++i) ring[i] = vop(i);
 #pragma unroll
-      for (int ks2 = 0; ks2 < 4; ++ks2) {
-        const uint4 a = *reinterpret_cast<const uint4*>(va + ks2 * 32);
-        oacc[dt] = mfma32x32x16(a, pk[ks2 >> 1][ks2 & 1], oacc[dt]);
+      for (int i = 0; i < NPV; ++i) {
+        const uint4 a = ring[i % kRing];
+        if (i + kRing < NPV) ring[i % kRing] = vop(i + kRing);
+        const int ks2 = i / NDT;
+        oacc[i % NDT] = mfma32x32x16(a, pk[ks2 >> 1][ks2 & 1], oacc[i % NDT]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
+  };
 
-    if (has_next) sstore(cur ^ 1);
+  const int n_step = (it.kv_end - it.kv_begin + BN - 1) / BN;
+  if constexpr (kWide) {
+    Regs ra, rb;
+    gload(ra, it.kv_begin);
+    sstore(ra, 0);
+    if (n_step > 1) gload(rb, it.kv_begin + BN);
     __syncthreads();
+    for (int st = 0; st < n_step; st += 2) {
+      const int k0 = it.kv_begin + st * BN;
+      // even step: LDS 0 holds step st, rb carries step st+1
+      if (st + 2 < n_step) gload(ra, k0 + 2 * BN);
+      compute(0, k0);
+      if (st + 1 < n_step) sstore(rb, 1);
+      __syncthreads();
+      if (st + 1 >= n_step) break;
+      // odd step: LDS 1 holds step st+1, ra carries step st+2
+      if (st + 3 < n_step) gload(rb, k0 + 3 * BN);
+      compute(1, k0 + BN);
+      if (st + 2 < n_step) sstore(ra, 0);
+      __syncthreads();
+    }
+  } else {
+    Regs ra;
+    gload(ra, it.kv_begin);
+    sstore(ra, 0);
+    __syncthreads();
+    for (int st = 0; st < n_step; ++st) {
+      const int k0 = it.kv_begin + st * BN;
+      const bool has_next = st + 1 < n_step;
+      if (has_next) gload(ra, k0 + BN);
+      compute(st & 1, k0);
+      if (has_next) sstore(ra, (st & 1) ^ 1);
+      __syncthreads();
+    }
   }
 
   // ---- finish: the two lane halves hold disjoint keys of the same query
@@ -284,39 +379,52 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(
   }
 }
 
-template <int D, int B, int G>
-static hipError_t launch_prefill_t(const AttnArgs& a, hipStream_t s) {
-  constexpr int smem = PrefillSmem<D>::TOTAL;
+template <int D, int B, int G, int NW>
+static hipError_t launch_prefill_t(const PrefillItem* items, int n, const AttnArgs& a,
+                                   hipStream_t s) {
+  constexpr int smem = PrefillLayout<D, B>::KV_TOTAL + (NW == 8 ? NW * 32 * D * 2 : 0);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<D, B, G>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+    hipError_t e =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<D, B, G, NW>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, smem);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((prefill_kernel<D, B, G>), dim3(a.n_prefill), dim3(256), smem, s, a.prefill,
-                     a.q, a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv,
-                     a.mbr, a.scale_log2);
+  hipLaunchKernelGGL((prefill_kernel<D, B, G, NW>), dim3(n), dim3(NW * 64), smem, s, items, a.q,
+                     a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv, a.mbr,
+                     a.scale_log2);
   return hipGetLastError();
 }
 
-template <int D, int B>
-static hipError_t launch_prefill_g(int G, const AttnArgs& a, hipStream_t s) {
+template <int D, int B, int NW>
+static hipError_t launch_prefill_g(int G, const PrefillItem* items, int n, const AttnArgs& a,
+                                   hipStream_t s) {
   switch (G) {
-    case 1: return launch_prefill_t<D, B, 1>(a, s);
-    case 2: return launch_prefill_t<D, B, 2>(a, s);
-    case 4: return launch_prefill_t<D, B, 4>(a, s);
-    case 8: return launch_prefill_t<D, B, 8>(a, s);
+    case 1: return launch_prefill_t<D, B, 1, NW>(items, n, a, s);
+    case 2: return launch_prefill_t<D, B, 2, NW>(items, n, a, s);
+    case 4: return launch_prefill_t<D, B, 4, NW>(items, n, a, s);
+    case 8: return launch_prefill_t<D, B, 8, NW>(items, n, a, s);
   }
+  return hipErrorInvalidValue;
+}
+
+template <int NW>
+static hipError_t launch_prefill_w(int D, int G, const PrefillItem* items, int n,
+                                   const AttnArgs& a, hipStream_t s) {
+  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, items, n, a, s);
+  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, items, n, a, s);
+  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, items, n, a, s);
+  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, items, n, a, s);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s) {
-  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16>(G, a, s);
-  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32>(G, a, s);
-  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16>(G, a, s);
-  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32>(G, a, s);
-  return hipErrorInvalidValue;
+  hipError_t e = hipSuccess;
+  if (a.n_prefill_wide > 0)
+    e = launch_prefill_w<8>(D, G, a.prefill_wide, a.n_prefill_wide, a, s);
+  if (e == hipSuccess && a.n_prefill > 0) e = launch_prefill_w<4>(D, G, a.prefill, a.n_prefill, a, s);
+  return e;
 }
 
 }  // namespace cpattn
