@@ -179,19 +179,31 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0):
         step(i)
     torch.cuda.synchronize()
     log(f"[bench] warmup done ({warmup} steps); timing {steps_n} steps")
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps_n + 1)]
-    binding.profile_begin()
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    evs[0].record(stream)
-    for i in range(steps_n):
-        step(i)
-        evs[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    prof = binding.profile_end()
-    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps_n)])
-    total_ms = float(evs[0].elapsed_time(evs[-1]))
+    def timed(n, detail):
+        """n steps between two events on the step stream; with ``detail`` also
+        an event after every step and the library's per-kernel event pairs."""
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1 if detail else 2)]
+        if detail:
+            binding.profile_begin()
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        evs[0].record(stream)
+        for i in range(n):
+            step(i)
+            if detail:
+                evs[i + 1].record(stream)
+        if not detail:
+            evs[1].record(stream)
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - w0
+        prof_ = binding.profile_end() if detail else None
+        per = (np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(n)]) if detail else None)
+        return float(evs[0].elapsed_time(evs[-1])), wall_s, per, prof_
+
+    # headline region: only the two bracketing events
+    total_ms, wall, _, _ = timed(steps_n, False)
+    # second region, same steps: per-step latencies and per-kernel durations
+    _, _, per_step, prof = timed(steps_n, True)
     tokens = sum(batches[i % len(batches)].num_tokens for i in range(steps_n))
     log(f"[bench] timed region {total_ms:.3f} ms (wall {wall * 1e3:.3f} ms)")
 

@@ -27,6 +27,7 @@ struct Stage {
   bool pending = false;
 };
 
+// Per-device state: the staging ring.
 struct DeviceCtx {
   Stage ring[kRingSlots];
   int next = 0;
@@ -143,18 +144,30 @@ int finish(hipError_t e, hipStream_t s) {
   return CP_OK;
 }
 
+template <class T>
+void put(std::vector<uint8_t>& buf, size_t off, const std::vector<T>& v) {
+  if (!v.empty()) std::memcpy(buf.data() + off, v.data(), v.size() * sizeof(T));
+}
+
 void serialize(const Plan& p, std::vector<uint8_t>& buf) {
-  buf.assign(p.plan_bytes, 0);
-  if (!p.prefill.empty())
-    std::memcpy(buf.data() + p.off_prefill, p.prefill.data(),
-                p.prefill.size() * sizeof(PrefillItem));
-  if (!p.prefill_wide.empty())
-    std::memcpy(buf.data() + p.off_prefill_wide, p.prefill_wide.data(),
-                p.prefill_wide.size() * sizeof(PrefillItem));
-  if (!p.decode.empty())
-    std::memcpy(buf.data() + p.off_decode, p.decode.data(), p.decode.size() * sizeof(DecodeItem));
-  if (!p.merge.empty())
-    std::memcpy(buf.data() + p.off_merge, p.merge.data(), p.merge.size() * sizeof(MergeGroup));
+  buf.resize(p.plan_bytes);
+  put(buf, p.off_prefill, p.prefill);
+  put(buf, p.off_prefill_slots, p.prefill_slots);
+  put(buf, p.off_prefill_wide, p.prefill_wide);
+  put(buf, p.off_prefill_wide_slots, p.prefill_wide_slots);
+  put(buf, p.off_decode, p.decode);
+  put(buf, p.off_merge, p.merge);
+}
+
+// One plan per thread, reused across calls (its vectors keep their capacity).
+Plan& thread_plan() {
+  thread_local Plan p;
+  return p;
+}
+
+AppendPlan& thread_append_plan() {
+  thread_local AppendPlan p;
+  return p;
 }
 
 }  // namespace
@@ -182,9 +195,9 @@ int cp_check_batch(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_
 size_t cp_workspace_bytes(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows) {
   if (validate(desc, rows, n_rows) != CP_OK) return 0;
   try {
-    Plan p;
+    Plan& p = thread_plan();
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
-    AppendPlan a;
+    AppendPlan& a = thread_append_plan();
     build_append_plan(*desc, rows, n_rows, a);
     return p.ws_bytes > a.ws_bytes ? p.ws_bytes : a.ws_bytes;
   } catch (...) {
@@ -198,14 +211,15 @@ int cp_plan_summary(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
   if (v != CP_OK) return v;
   if (!counts) return CP_ERR_INVALID_ARG;
   try {
-    Plan p;
+    Plan& p = thread_plan();
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
-    counts[0] = (int64_t)(p.prefill.size() + p.prefill_wide.size());
-    counts[1] = (int64_t)p.decode.size();
-    counts[2] = (int64_t)p.merge.size();
+    const int64_t hkv = desc->num_kv_heads;
+    counts[0] = (int64_t)(p.prefill.size() + p.prefill_wide.size()) * hkv;
+    counts[1] = (int64_t)p.decode.size() * hkv;
+    counts[2] = (int64_t)p.merge.size() * hkv;
     counts[3] = p.partial_rows;
-    counts[4] = (int64_t)cp_workspace_bytes(desc, rows, n_rows);
     counts[5] = p.decode_split_blocks;
+    counts[4] = (int64_t)cp_workspace_bytes(desc, rows, n_rows);  // rebuilds the plan
   } catch (...) {
     return CP_ERR_INVALID_ARG;
   }
@@ -218,11 +232,12 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
   if (v != CP_OK) return v;
   if (cap > 0 && !items) return CP_ERR_INVALID_ARG;
   try {
-    Plan p;
+    Plan& p = thread_plan();
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    const int32_t hkv = desc->num_kv_heads;
     int64_t n = 0;
-    auto put = [&](int32_t kind, int32_t tok, int32_t ntok, int32_t pos, int32_t req, int32_t kvh,
-                   int32_t kb, int32_t ke) {
+    auto put_item = [&](int32_t kind, int32_t tok, int32_t ntok, int32_t pos, int32_t req,
+                        int32_t kvh, int32_t kb, int32_t ke) {
       if (n < cap) {
         int32_t* o = items + 8 * n;
         o[0] = kind, o[1] = tok, o[2] = ntok, o[3] = pos, o[4] = req, o[5] = kvh, o[6] = kb,
@@ -230,23 +245,30 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
       }
       ++n;
     };
-    for (const auto* lst : {&p.prefill_wide, &p.prefill})
-      for (const PrefillItem& it : *lst)
-        if (it.n_tok > 0)
-          put(0, it.tok0, it.n_tok, it.pos0, it.req, it.kvh, it.kv_begin, it.kv_end);
-    for (const DecodeItem& it : p.decode) {
-      // position of the decode query: its row's ctx_len - 1, recovered from the row
-      int32_t pos = -1;
+    // prefill work in slot order (the order the kernels' workgroups take it)
+    for (int w = 1; w >= 0; --w) {
+      const auto& list = w ? p.prefill_wide : p.prefill;
+      for (int32_t slot : (w ? p.prefill_wide_slots : p.prefill_slots)) {
+        if (slot < 0) continue;
+        const PrefillItem& it = list[slot / hkv];
+        put_item(0, it.tok0, it.n_tok, it.pos0, it.req, slot % hkv, it.kv_begin, it.kv_end);
+      }
+    }
+    // position of a decode query: its row's chunk_start
+    std::vector<int32_t> pos_of_tok;
+    {
       int64_t t = 0;
+      for (int32_t r = 0; r < n_rows; ++r) t += rows[r].chunk_len;
+      pos_of_tok.assign((size_t)t, -1);
+      t = 0;
       for (int32_t r = 0; r < n_rows; ++r) {
-        if (t == it.tok && rows[r].chunk_len > 0) {
-          pos = rows[r].chunk_start;
-          break;
-        }
+        if (rows[r].chunk_len > 0) pos_of_tok[(size_t)t] = rows[r].chunk_start;
         t += rows[r].chunk_len;
       }
-      put(1, it.tok, 1, pos, it.req, it.kvh, it.kv_begin, it.kv_end);
     }
+    for (int32_t h = 0; h < hkv; ++h)
+      for (const DecodeItem& it : p.decode)
+        put_item(1, it.tok, 1, pos_of_tok[(size_t)it.tok], it.req, h, it.kv_begin, it.kv_end);
     return n;
   } catch (...) {
     return CP_ERR_INVALID_ARG;
@@ -264,12 +286,10 @@ int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new,
       !aligned(v_cache, 16) || !aligned(ws, 256) || !aligned(block_tables, 4))
     return CP_ERR_INVALID_ARG;
   try {
-    AppendPlan p;
+    AppendPlan& p = thread_append_plan();
     build_append_plan(*desc, rows, n_rows, p);
     if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    int rc = upload(ws, p.items.data(), p.items.size() * sizeof(AppendItem), s);
-    if (rc != CP_OK) return rc;
     AppendArgs a;
     a.items = reinterpret_cast<const AppendItem*>(ws);
     a.n_items = (int)p.items.size();
@@ -280,8 +300,17 @@ int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new,
     a.bt = block_tables;
     a.hkv = desc->num_kv_heads;
     a.mbr = desc->max_blocks_per_req;
+    const AppendInline* inl = nullptr;
+    if (a.n_items <= kAppendInlineItems) {
+      thread_local AppendInline buf;
+      std::memcpy(buf.items, p.items.data(), p.items.size() * sizeof(AppendItem));
+      inl = &buf;
+    } else {
+      const int rc = upload(ws, p.items.data(), p.items.size() * sizeof(AppendItem), s);
+      if (rc != CP_OK) return rc;
+    }
     const long pi = prof_open(0, s);
-    const hipError_t e = launch_append(desc->head_dim, desc->block_size, a, s);
+    const hipError_t e = launch_append(desc->head_dim, desc->block_size, a, inl, s);
     prof_close(pi, s);
     return finish(e, s);
   } catch (...) {
@@ -300,7 +329,7 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
       !aligned(ws, 256) || !aligned(block_tables, 4))
     return CP_ERR_INVALID_ARG;
   try {
-    Plan p;
+    Plan& p = thread_plan();
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
     if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
     thread_local std::vector<uint8_t> buf;
@@ -311,9 +340,11 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
     uint8_t* base = static_cast<uint8_t*>(ws);
     AttnArgs a;
     a.prefill = reinterpret_cast<const PrefillItem*>(base + p.off_prefill);
-    a.n_prefill = (int)p.prefill.size();
+    a.prefill_slots = reinterpret_cast<const int32_t*>(base + p.off_prefill_slots);
+    a.n_prefill_slots = (int)p.prefill_slots.size();
     a.prefill_wide = reinterpret_cast<const PrefillItem*>(base + p.off_prefill_wide);
-    a.n_prefill_wide = (int)p.prefill_wide.size();
+    a.prefill_wide_slots = reinterpret_cast<const int32_t*>(base + p.off_prefill_wide_slots);
+    a.n_prefill_wide_slots = (int)p.prefill_wide_slots.size();
     a.decode = reinterpret_cast<const DecodeItem*>(base + p.off_decode);
     a.n_decode = (int)p.decode.size();
     a.merge = reinterpret_cast<const MergeGroup*>(base + p.off_merge);
@@ -332,7 +363,8 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
     a.scale_log2 = desc->sm_scale * 1.4426950408889634f;
     const int D = desc->head_dim;
     const int G = desc->num_q_heads / desc->num_kv_heads;
-    if (a.n_prefill > 0 || a.n_prefill_wide > 0) {
+    const bool has_pf = a.n_prefill_slots > 0 || a.n_prefill_wide_slots > 0;
+    if (has_pf) {
       const long pi = prof_open(1, s);
       const hipError_t e = launch_prefill(D, G, a, s);
       prof_close(pi, s);

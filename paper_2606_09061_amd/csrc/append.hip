@@ -1,25 +1,25 @@
 // Paged KV append: scatters the batch's new K/V rows into their cache slots.
 //
-// One workgroup per (request, logical block) span of new tokens and kv head.
+// One workgroup per (request, logical block) span of new tokens and kv head;
+// the span list comes from device memory or, when short, from the kernel
+// arguments.
 // K rows are token-major inside a block, so each 16-byte chunk of a new K row
-// is one aligned vector copy.  V is feature-major inside a block ([D][B]):
-// thread d gathers the span's values of feature d and writes them as one run
-// of its feature row (one 16-byte store per 8 slots when the span fills the
-// block).  Every load is issued before the first store.
+// is one aligned vector copy.  V is feature-major inside a block ([D][B]): a
+// thread transposes an 8-slot x 8-feature tile in registers, reading token
+// rows and writing feature runs with 16-byte accesses.  Every load is issued
+// before the first store.
 #include "device.hpp"
 #include "kernels.hpp"
 
 namespace cpattn {
 
 template <int D, int B>
-__global__ __launch_bounds__(256) void kv_append_kernel(const AppendItem* __restrict__ items,
-                                                        const uint16_t* __restrict__ k_new,
-                                                        const uint16_t* __restrict__ v_new,
-                                                        uint16_t* __restrict__ k_cache,
-                                                        uint16_t* __restrict__ v_cache,
-                                                        const int32_t* __restrict__ bt, int hkv,
-                                                        int mbr) {
-  const AppendItem it = items[blockIdx.x];
+__device__ __forceinline__ void append_span(const AppendItem& it,
+                                            const uint16_t* __restrict__ k_new,
+                                            const uint16_t* __restrict__ v_new,
+                                            uint16_t* __restrict__ k_cache,
+                                            uint16_t* __restrict__ v_cache,
+                                            const int32_t* __restrict__ bt, int hkv, int mbr) {
   const int h = blockIdx.y;
   const int req = it.req_slot0 >> 8;
   const int slot0 = it.req_slot0 & 0xff;
@@ -37,14 +37,28 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendItem* __rest
       kv[i] = *reinterpret_cast<const uint4*>(k_new + ((int64_t)(it.tok0 + j) * hkv + h) * D +
                                               (x % kChunks) * 8);
   }
-  // V: thread d gathers the span's values of feature d (coalesced over d)
-  uint16_t vv[B];
-  const bool vthread = tid < D;
-  if (vthread) {
-    const uint16_t* src = v_new + ((int64_t)it.tok0 * hkv + h) * D + tid;
+  // V: thread (slot tile ts, feature group fg) loads the 16-byte pieces of
+  // features [8 fg, 8 fg + 8) of the tokens in slots [8 ts, 8 ts + 8), turns
+  // the 8x8 tile around in registers and writes one 8-slot run per feature:
+  // a 16-byte store when the span covers the whole tile.
+  constexpr int NTS = B / 8, NFG = D / 8;
+  static_assert(NTS * NFG <= 256, "one V tile per thread");
+  const int ts = tid / NFG;
+  const int fg = tid % NFG;
+  const int s_lo = max(8 * ts, slot0);
+  const int s_hi = min(8 * ts + 8, slot0 + it.n_tok);
+  const bool vwork = tid < NTS * NFG && s_lo < s_hi;
+  uint32_t w[8][4];  // w[e]: token in slot 8 ts + e, features 8 fg .. 8 fg + 7
+  if (vwork) {
 #pragma unroll
-    for (int j = 0; j < B; ++j)
-      if (j < it.n_tok) vv[j] = src[(int64_t)j * hkv * D];
+    for (int e = 0; e < 8; ++e) {
+      const int slot = 8 * ts + e;
+      uint4 r = make_uint4(0, 0, 0, 0);
+      if (slot >= s_lo && slot < s_hi)
+        r = *reinterpret_cast<const uint4*>(
+            v_new + ((int64_t)(it.tok0 + slot - slot0) * hkv + h) * D + fg * 8);
+      w[e][0] = r.x, w[e][1] = r.y, w[e][2] = r.z, w[e][3] = r.w;
+    }
   }
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
@@ -54,39 +68,72 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendItem* __rest
       *reinterpret_cast<uint4*>(k_cache + ((blk * hkv + h) * B + slot0 + j) * D +
                                 (x % kChunks) * 8) = kv[i];
   }
-  if (vthread) {
-    uint16_t* dst = v_cache + ((blk * hkv + h) * D + tid) * B;
-    if (it.n_tok == B) {
+  if (vwork) {
+    uint16_t* dst = v_cache + ((blk * hkv + h) * D + fg * 8) * B + 8 * ts;
+    const bool whole = s_lo == 8 * ts && s_hi == 8 * ts + 8;
 #pragma unroll
-      for (int j = 0; j < B / 8; ++j) {
-        uint4 w;
-        w.x = (uint32_t)vv[8 * j + 0] | ((uint32_t)vv[8 * j + 1] << 16);
-        w.y = (uint32_t)vv[8 * j + 2] | ((uint32_t)vv[8 * j + 3] << 16);
-        w.z = (uint32_t)vv[8 * j + 4] | ((uint32_t)vv[8 * j + 5] << 16);
-        w.w = (uint32_t)vv[8 * j + 6] | ((uint32_t)vv[8 * j + 7] << 16);
-        reinterpret_cast<uint4*>(dst)[j] = w;
+    for (int f = 0; f < 8; ++f) {
+      // feature 8 fg + f of the 8 slots
+      uint32_t v16[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v16[e] = (w[e][f / 2] >> (16 * (f % 2))) & 0xffffu;
+      if (whole) {
+        uint4 o;
+        o.x = v16[0] | (v16[1] << 16);
+        o.y = v16[2] | (v16[3] << 16);
+        o.z = v16[4] | (v16[5] << 16);
+        o.w = v16[6] | (v16[7] << 16);
+        *reinterpret_cast<uint4*>(dst + f * B) = o;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (8 * ts + e >= s_lo && 8 * ts + e < s_hi) dst[f * B + e] = (uint16_t)v16[e];
       }
-    } else {
-#pragma unroll
-      for (int j = 0; j < B; ++j)
-        if (j < it.n_tok) dst[slot0 + j] = vv[j];
     }
   }
 }
 
 template <int D, int B>
-static hipError_t launch_append_t(const AppendArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((kv_append_kernel<D, B>), dim3(a.n_items, a.hkv), dim3(256), 0, s, a.items,
-                     a.k_new,
-                     a.v_new, a.k_cache, a.v_cache, a.bt, a.hkv, a.mbr);
+__global__ __launch_bounds__(256) void kv_append_kernel(const AppendItem* __restrict__ items,
+                                                        const uint16_t* __restrict__ k_new,
+                                                        const uint16_t* __restrict__ v_new,
+                                                        uint16_t* __restrict__ k_cache,
+                                                        uint16_t* __restrict__ v_cache,
+                                                        const int32_t* __restrict__ bt, int hkv,
+                                                        int mbr) {
+  append_span<D, B>(items[blockIdx.x], k_new, v_new, k_cache, v_cache, bt, hkv, mbr);
+}
+
+template <int D, int B>
+__global__ __launch_bounds__(256) void kv_append_inline_kernel(const AppendInline inl,
+                                                               const uint16_t* __restrict__ k_new,
+                                                               const uint16_t* __restrict__ v_new,
+                                                               uint16_t* __restrict__ k_cache,
+                                                               uint16_t* __restrict__ v_cache,
+                                                               const int32_t* __restrict__ bt,
+                                                               int hkv, int mbr) {
+  append_span<D, B>(inl.items[blockIdx.x], k_new, v_new, k_cache, v_cache, bt, hkv, mbr);
+}
+
+template <int D, int B>
+static hipError_t launch_append_t(const AppendArgs& a, const AppendInline* inl, hipStream_t s) {
+  if (inl) {
+    if (a.n_items > kAppendInlineItems) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((kv_append_inline_kernel<D, B>), dim3(a.n_items, a.hkv), dim3(256), 0, s,
+                       *inl, a.k_new, a.v_new, a.k_cache, a.v_cache, a.bt, a.hkv, a.mbr);
+  } else {
+    hipLaunchKernelGGL((kv_append_kernel<D, B>), dim3(a.n_items, a.hkv), dim3(256), 0, s, a.items,
+                       a.k_new, a.v_new, a.k_cache, a.v_cache, a.bt, a.hkv, a.mbr);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_append(int D, int B, const AppendArgs& a, hipStream_t s) {
-  if (D == 128 && B == 16) return launch_append_t<128, 16>(a, s);
-  if (D == 128 && B == 32) return launch_append_t<128, 32>(a, s);
-  if (D == 64 && B == 16) return launch_append_t<64, 16>(a, s);
-  if (D == 64 && B == 32) return launch_append_t<64, 32>(a, s);
+hipError_t launch_append(int D, int B, const AppendArgs& a, const AppendInline* inl,
+                         hipStream_t s) {
+  if (D == 128 && B == 16) return launch_append_t<128, 16>(a, inl, s);
+  if (D == 128 && B == 32) return launch_append_t<128, 32>(a, inl, s);
+  if (D == 64 && B == 16) return launch_append_t<64, 16>(a, inl, s);
+  if (D == 64 && B == 32) return launch_append_t<64, 32>(a, inl, s);
   return hipErrorInvalidValue;
 }
 

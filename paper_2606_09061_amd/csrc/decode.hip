@@ -5,19 +5,20 @@
 // heads, so the kernel is organised around streaming the paged blocks at
 // full HBM rate and keeping the VALU work per byte small.
 //
-// Work item: (row, kv head, range of whole blocks).  A workgroup of 4 waves
-// takes one item; wave w walks blocks w, w+4, ... of the range, one block per
-// step, with the next block's loads issued before the current one is used.
+// Work item: (row, range of whole blocks), for the kv head blockIdx.y.  A
+// workgroup of 4 waves takes one item; the range is walked in tiles of 16
+// keys (a block holds B / 16), wave w taking tiles w, w+4, ..., with the next
+// tile's loads issued before the current one is used.
 //
-// Per block (one "tile" of B keys) every lane issues NL 16-byte loads of K
-// and NL of V; instruction i of the wave reads bytes [1024 i, 1024 i + 1024)
-// of the block, so each load instruction is one contiguous 1 KiB segment.
-//   K tile [B][D]: lane holds 8 features (chunk lane % (D/8)) of NL keys.
+// Per tile every lane issues NL 16-byte loads of K and NL of V.
+//   K tile [16][D] (contiguous inside the block): instruction i of the wave
+//     reads bytes [1024 i, 1024 i + 1024) of it; lane holds 8 features
+//     (chunk lane % (D/8)) of NL keys.
 //     Scores: bf16 dot2 against the lane's 8 features of each of the G q
 //     heads, then a butterfly reduce-scatter over the D/8 lanes of a key row
 //     (DPP inside rows of 16) leaves each lane with whole scores.
-//   V tile [D][B]: lane holds 8 consecutive keys (chunk lane % (B/8)) of NL
-//     feature rows.  Weights of those 8 keys come from a per-wave LDS slot,
+//   V tile: the tile's 16 slots of each feature row of the [D][B] block; a
+//     lane holds 8 consecutive keys (chunk lane % 2) of NL feature rows.  Weights of those 8 keys come from a per-wave LDS slot,
 //     and the weighted sum is again bf16 dot2 with fp32 accumulation.
 // Online softmax runs in base 2 with a lazily updated running max per head.
 // The 4 waves' (max, sum, output) states are combined through LDS; an item
@@ -57,42 +58,59 @@ __device__ __forceinline__ void reduce_scatter(float* v, int lane) {
 }  // namespace
 
 template <int D, int B, int G>
-__global__ __launch_bounds__(256) void decode_kernel(
+__global__ __launch_bounds__(256, G * D >= 512 ? 3 : 4) void decode_kernel(
     const DecodeItem* __restrict__ items, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
-  constexpr int NL = B * D * 2 / 1024;  // 16-byte loads per lane per tile, K and V each
+  constexpr int TK = 16;                // keys per tile (a block holds B / TK tiles)
+  constexpr int NL = TK * D * 2 / 1024; // 16-byte loads per lane per tile, K and V each
   constexpr int LPR = D / 8;            // lanes sharing one K row
   constexpr int TPI = 64 / LPR;         // K rows per load instruction
-  constexpr int LPD = B / 8;            // lanes sharing one V feature row
+  constexpr int LPD = TK / 8;           // lanes sharing one V feature row
   constexpr int DPI = 64 / LPD;         // V feature rows per load instruction
   constexpr int NV = NL * G;            // partial scores per lane
   constexpr int NVL = NV >= LPR ? NV / LPR : 1;
   constexpr int DUP = NV >= LPR ? 1 : LPR / NV;  // lanes holding the same score
   constexpr int kWaves = kDecodeWaves;
-  static_assert(NL * TPI == B && NL * DPI == D, "tile geometry");
+  static_assert(NL * TPI == TK && NL * DPI == D && B % TK == 0 && LPD == 2, "tile geometry");
 
-  __shared__ __attribute__((aligned(16))) uint16_t p_lds[kWaves][G][B];
+  __shared__ __attribute__((aligned(16))) uint16_t p_lds[kWaves][G][TK];
   __shared__ float red_o[kWaves][G][D];
   __shared__ float red_m[kWaves][G];
   __shared__ float red_l[kWaves][G];
 
   const DecodeItem it = items[blockIdx.x];
+  const int kvh = blockIdx.y;
+  const int part = it.part < 0 ? -1 : it.part + kvh * it.part_kvh_stride;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // wave-uniform in a scalar register, so that the tile loop, its branches
+  // and the block-table reads are scalar and leave the vector memory counter
+  // to the K/V loads (the prefetched tile stays in flight during a tile)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int sub = lane % LPR;
   const int krow = lane / LPR;
   const int tc = lane % LPD;
   const int vrow = lane / LPD;
 
-  uint4 qv[G];
-  {
-    const uint16_t* qb = q + ((int64_t)it.tok * hq + it.kvh * G) * D + sub * 8;
+  // Large head groups keep the query in LDS (read again every tile) so that
+  // the kernel stays at three waves per SIMD; small ones keep it in registers.
+  constexpr bool kQLds = G * D >= 1024;
+  __shared__ __attribute__((aligned(16))) uint16_t q_lds[kQLds ? G : 1][kQLds ? D : 8];
+  uint4 qv[kQLds ? 1 : G];
+  if constexpr (kQLds) {
+    const uint16_t* qb = q + ((int64_t)it.tok * hq + kvh * G) * D;
+    for (int x = tid; x < G * D / 8; x += 256)
+      *reinterpret_cast<uint4*>(&q_lds[x / (D / 8)][(x % (D / 8)) * 8]) = ld_global16(qb + x * 8);
+    __syncthreads();
+  } else {
+    const uint16_t* qb = q + ((int64_t)it.tok * hq + kvh * G) * D + sub * 8;
 #pragma unroll
     for (int h = 0; h < G; ++h) qv[h] = ld_global16(qb + h * D);
+    __builtin_amdgcn_sched_barrier(0);  // query loads stay older than the tile loads
   }
+  auto qop = [&](int h) -> uint4 { return *reinterpret_cast<const uint4*>(&q_lds[h][sub * 8]); };
 
   // reduced-score slot k of this lane -> (head, key within tile)
   int s_head[NVL], s_key[NVL];
@@ -118,45 +136,48 @@ __global__ __launch_bounds__(256) void decode_kernel(
   }
 
   const int64_t head_elems = (int64_t)B * D;
-  const int kb0 = it.kv_begin / B;
-  const int kb1 = (it.kv_end + B - 1) / B;
+  const int kt0 = it.kv_begin / TK;
+  const int kt1 = (it.kv_end + TK - 1) / TK;
   const int32_t* bt_row = bt + (int64_t)it.req * mbr;
+  // tile t: K rows [t*TK % B, +TK) of its block (contiguous), and the same
+  // slots of every V feature row of the block
+  auto load_tile = [&](int t, uint4* kr, uint4* vr) {
+    const int64_t blk = ((int64_t)bt_row[(t * TK) / B] * hkv + kvh) * head_elems;
+    const int toff = (t * TK) % B;
+    const uint16_t* kp = k_cache + blk + toff * D + lane * 8;
+    const uint16_t* vp = v_cache + blk + vrow * B + toff + tc * 8;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) kr[i] = ld_global16(kp + i * 512);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) vr[i] = ld_global16(vp + i * DPI * B);
+  };
 
-  uint4 kr[NL], vr[NL];
-  int kb = kb0 + wave;
-  if (kb < kb1) {
-    const int64_t base = ((int64_t)bt_row[kb] * hkv + it.kvh) * head_elems + lane * 8;
-#pragma unroll
-    for (int i = 0; i < NL; ++i) kr[i] = ld_global16(k_cache + base + i * 512);
-#pragma unroll
-    for (int i = 0; i < NL; ++i) vr[i] = ld_global16(v_cache + base + i * 512);
-  }
-
-  for (; kb < kb1; kb += kWaves) {
-    const int nkb = kb + kWaves;
-    uint4 kn[NL], vn[NL];
-    if (nkb < kb1) {
-      const int64_t base = ((int64_t)bt_row[nkb] * hkv + it.kvh) * head_elems + lane * 8;
-#pragma unroll
-      for (int i = 0; i < NL; ++i) kn[i] = ld_global16(k_cache + base + i * 512);
-#pragma unroll
-      for (int i = 0; i < NL; ++i) vn[i] = ld_global16(v_cache + base + i * 512);
-    }
-    const int valid = min(B, it.kv_end - kb * B);
+  // one tile: scores, online softmax, weighted values
+  auto step = [&](const uint4* kr, uint4* vr, int kt) {
+    const int valid = min(TK, it.kv_end - kt * TK);
 
     // ---- scores
     float sv[NV];
-#pragma unroll
-    for (int i = 0; i < NL; ++i) {
+    auto score = [&](int i, int h, const uint4& qh) {
+      float acc = 0.f;
+      acc = dot2_bf16(kr[i].x, qh.x, acc);
+      acc = dot2_bf16(kr[i].y, qh.y, acc);
+      acc = dot2_bf16(kr[i].z, qh.z, acc);
+      acc = dot2_bf16(kr[i].w, qh.w, acc);
+      sv[i * G + h] = acc;
+    };
+    if constexpr (kQLds) {  // one LDS read of each head's query piece
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        float acc = 0.f;
-        acc = dot2_bf16(kr[i].x, qv[h].x, acc);
-        acc = dot2_bf16(kr[i].y, qv[h].y, acc);
-        acc = dot2_bf16(kr[i].z, qv[h].z, acc);
-        acc = dot2_bf16(kr[i].w, qv[h].w, acc);
-        sv[i * G + h] = acc;
+        const uint4 qh = qop(h);
+#pragma unroll
+        for (int i = 0; i < NL; ++i) score(i, h, qh);
       }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NL; ++i)
+#pragma unroll
+        for (int h = 0; h < G; ++h) score(i, h, qv[h]);
     }
     reduce_scatter<NV, LPR / 2>(sv, lane);
     float s[NVL];
@@ -200,12 +221,8 @@ __global__ __launch_bounds__(256) void decode_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    uint4 pv[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) pv[h] = *reinterpret_cast<const uint4*>(&p_lds[wave][h][tc * 8]);
-
     // ---- zero values of keys past the end of the range (may hold NaN)
-    if (valid < B) {
+    if (valid < TK) {
       const int t0 = tc * 8;
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
@@ -218,25 +235,37 @@ __global__ __launch_bounds__(256) void decode_kernel(
         }
       }
     }
-    // ---- weighted values
+    // ---- weighted values (each head's 8 weights read just before use)
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
+    for (int h = 0; h < G; ++h) {
+      const uint4 pv = *reinterpret_cast<const uint4*>(&p_lds[wave][h][tc * 8]);
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
+      for (int i = 0; i < NL; ++i) {
         float acc = o[h][i];
-        acc = dot2_bf16(vr[i].x, pv[h].x, acc);
-        acc = dot2_bf16(vr[i].y, pv[h].y, acc);
-        acc = dot2_bf16(vr[i].z, pv[h].z, acc);
-        acc = dot2_bf16(vr[i].w, pv[h].w, acc);
+        acc = dot2_bf16(vr[i].x, pv.x, acc);
+        acc = dot2_bf16(vr[i].y, pv.y, acc);
+        acc = dot2_bf16(vr[i].z, pv.z, acc);
+        acc = dot2_bf16(vr[i].w, pv.w, acc);
         o[h][i] = acc;
       }
     }
     __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      kr[i] = kn[i];
-      vr[i] = vn[i];
-    }
+  };
+
+  // Two register sets in turn: the loads of a wave's next tile are in flight
+  // while it works on the current one.  The prefetch is unconditional (past
+  // the range it re-reads the range's last tile, which is unused) so that
+  // the compiler's wait counts stay exact and never drain the prefetch.
+  uint4 ka[NL], va[NL], kb[NL], vb[NL];
+  const int last = kt1 - 1;  // items are never empty
+  int kt = kt0 + wave;
+  load_tile(min(kt, last), ka, va);
+  for (; kt < kt1; kt += 2 * kWaves) {
+    load_tile(min(kt + kWaves, last), kb, vb);
+    step(ka, va, kt);
+    if (kt + kWaves >= kt1) break;
+    load_tile(min(kt + 2 * kWaves, last), ka, va);
+    step(kb, vb, kt + kWaves);
   }
 
   // ---- combine inside the wave: feature rows are split over LPD lanes
@@ -245,8 +274,7 @@ __global__ __launch_bounds__(256) void decode_kernel(
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       float x = o[h][i];
-      x += dpp<kXor1>(x);
-      if constexpr (LPD == 4) x += dpp<kXor2>(x);
+      x += dpp<kXor1>(x);  // the two lanes of a V feature row
       o[h][i] = x;
     }
   float lsum[G];
@@ -289,18 +317,18 @@ __global__ __launch_bounds__(256) void decode_kernel(
       O += f * red_o[w][h][d];
     }
     const float val = L > 0.f ? O / L : 0.f;
-    if (it.part < 0) {
-      out[((int64_t)it.tok * hq + it.kvh * G + h) * D + d] = to_bf16(val);
+    if (part < 0) {
+      out[((int64_t)it.tok * hq + kvh * G + h) * D + d] = to_bf16(val);
     } else {
-      part_o[(int64_t)(it.part + h) * D + d] = val;
-      if (d == 0) part_lse[it.part + h] = L > 0.f ? M + __log2f(L) : -INFINITY;
+      part_o[(int64_t)(part + h) * D + d] = val;
+      if (d == 0) part_lse[part + h] = L > 0.f ? M + __log2f(L) : -INFINITY;
     }
   }
 }
 
 template <int D, int B, int G>
 static hipError_t launch_decode_t(const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((decode_kernel<D, B, G>), dim3(a.n_decode), dim3(256), 0, s, a.decode, a.q,
+  hipLaunchKernelGGL((decode_kernel<D, B, G>), dim3(a.n_decode, a.hkv), dim3(256), 0, s, a.decode, a.q,
                      a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv, a.mbr,
                      a.scale_log2);
   return hipGetLastError();

@@ -8,6 +8,13 @@
 
 namespace cpattn {
 
+// Append plans of up to kAppendInlineItems items travel inside the kernel
+// arguments (3.2 KB), so a small append needs no plan upload.
+constexpr int kAppendInlineItems = 200;
+struct AppendInline {
+  AppendItem items[kAppendInlineItems];
+};
+
 struct AppendArgs {
   const AppendItem* items;
   int n_items;
@@ -21,12 +28,14 @@ struct AppendArgs {
 
 struct AttnArgs {
   const PrefillItem* prefill;       // 128-row tiles (4-wave kernel)
-  int n_prefill;
+  const int32_t* prefill_slots;     // item * hkv + kv head, or -1
+  int n_prefill_slots;
   const PrefillItem* prefill_wide;  // 256-row tiles (8-wave kernel)
-  int n_prefill_wide;
-  const DecodeItem* decode;
+  const int32_t* prefill_wide_slots;
+  int n_prefill_wide_slots;
+  const DecodeItem* decode;         // grid (n_decode, hkv)
   int n_decode;
-  const MergeGroup* merge;
+  const MergeGroup* merge;          // grid (n_merge, hkv)
   int n_merge;
   const uint16_t* q;
   const uint16_t* k_cache;
@@ -39,7 +48,10 @@ struct AttnArgs {
   float scale_log2;  // sm_scale * log2(e)
 };
 
-hipError_t launch_append(int D, int B, const AppendArgs& a, hipStream_t s);
+// `inl` non-null: the items are taken from it (a.n_items <= kAppendInlineItems)
+// and a.items is ignored.
+hipError_t launch_append(int D, int B, const AppendArgs& a, const AppendInline* inl,
+                         hipStream_t s);
 hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s);
 hipError_t launch_decode(int D, int B, int G, const AttnArgs& a, hipStream_t s);
 hipError_t launch_merge(int D, int G, const AttnArgs& a, hipStream_t s);

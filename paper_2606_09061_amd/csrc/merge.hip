@@ -19,8 +19,9 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeGroup* __restrict
   if (rl >= mg.n_rows) return;
   const int dq = threadIdx.x % DQ;
   const int rows = mg.n_tok * G;
+  const int kvh = blockIdx.y;
   const int r = mg.row0 + rl;
-  const int base = mg.part0 + r;
+  const int base = mg.part0 + kvh * mg.n_split * rows + r;
   float M = -INFINITY;
 #pragma unroll 4
   for (int s = 0; s < mg.n_split; ++s) M = fmaxf(M, part_lse[base + s * rows]);
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeGroup* __restrict
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   const int tok = mg.tok0 + r / G;
-  const int h = mg.kvh * G + r % G;
+  const int h = kvh * G + r % G;
   uint2 w2;
   w2.x = pack_bf16x2(acc.x * inv, acc.y * inv);
   w2.y = pack_bf16x2(acc.z * inv, acc.w * inv);
@@ -49,10 +50,10 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeGroup* __restrict
 
 hipError_t launch_merge(int D, int G, const AttnArgs& a, hipStream_t s) {
   if (D == 128)
-    hipLaunchKernelGGL(merge_kernel<128>, dim3(a.n_merge), dim3(256), 0, s, a.merge, a.part_o,
+    hipLaunchKernelGGL(merge_kernel<128>, dim3(a.n_merge, a.hkv), dim3(256), 0, s, a.merge, a.part_o,
                        a.part_lse, a.out, a.hq, G);
   else if (D == 64)
-    hipLaunchKernelGGL(merge_kernel<64>, dim3(a.n_merge), dim3(256), 0, s, a.merge, a.part_o,
+    hipLaunchKernelGGL(merge_kernel<64>, dim3(a.n_merge, a.hkv), dim3(256), 0, s, a.merge, a.part_o,
                        a.part_lse, a.out, a.hq, G);
   else
     return hipErrorInvalidValue;

@@ -5,7 +5,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <numeric>
-#include <unordered_set>
+#include <stdexcept>
 
 namespace cpattn {
 
@@ -21,63 +21,67 @@ bool is_pow2_in(int v, int lo, int hi) {
 }
 
 // Merge items of at most one workgroup's worth of rows (256 threads, each
-// combining 4 features of one row).
-void add_merge(Plan& p, int32_t tok0, int32_t n_tok, int32_t kvh, int32_t ns, int32_t part0, int G,
-               int D) {
+// combining 4 features of one row); the kernel's grid covers the kv heads.
+void add_merge(Plan& p, int32_t tok0, int32_t n_tok, int32_t ns, int32_t part0, int G, int D) {
   const int32_t rows = n_tok * G;
   const int32_t per = 256 / (D / 4);
   for (int32_t r0 = 0; r0 < rows; r0 += per) {
-    MergeGroup g{tok0, n_tok, kvh, ns, part0, r0, std::min(per, rows - r0), 0};
+    MergeGroup g{tok0, n_tok, ns, part0, r0, std::min(per, rows - r0), 0, 0};
     p.merge.push_back(g);
   }
 }
 
-// Orders prefill items so that items sharing a K/V range run on one XCD
-// (workgroup i is dispatched to XCD i mod num_xcds) and each XCD runs its
-// items longest first.  Groups are dealt to the least-loaded XCD, largest
-// group first; missing slots of shorter XCD lists become empty items.
-template <class T>
-void order_for_xcds(std::vector<T>& pf, int num_xcds, std::vector<PrefillItem>& out) {
-  out.clear();
-  if (pf.empty()) return;
-  const int X = std::max(1, num_xcds);
-  std::stable_sort(pf.begin(), pf.end(), [](const T& a, const T& b) {
-    return a.group < b.group;
-  });
-  struct Grp {
-    size_t b, e;
-    int64_t cost;
-  };
-  std::vector<Grp> groups;
-  for (size_t i = 0; i < pf.size();) {
-    size_t j = i;
-    int64_t c = 0;
-    while (j < pf.size() && pf[j].group == pf[i].group) c += pf[j++].cost;
-    groups.push_back({i, j, c});
-    i = j;
+// Orders the prefill slots of one item list (narrow or wide tiles) so that
+// slots sharing a K/V range -- the tiles of one chunk in one split, for one
+// kv head -- run on one XCD (workgroup i is dispatched to XCD i mod
+// num_xcds), and each XCD runs its slots longest first.  Groups are dealt to
+// the least-loaded XCD, largest group first; shorter XCD lists are padded
+// with idle slots (-1).
+void order_for_xcds(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_xcds,
+                    PlanScratch& sc, std::vector<int32_t>& slots) {
+  using detail::Slot;
+  slots.clear();
+  auto& groups = sc.groups;
+  groups.clear();
+  for (int32_t c = 0; c < (int32_t)sc.chunks.size(); ++c) {
+    const detail::Chunk& ch = sc.chunks[c];
+    if (ch.wide != wide) continue;
+    for (int32_t s = 0; s < ch.max_ns; ++s) {
+      int64_t gc = 0;
+      for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i)
+        if (sc.tiles[i].ns > s) gc += cost[sc.tiles[i].item0 + s];
+      for (int32_t h = 0; h < Hkv; ++h) groups.push_back({c, h, s, gc});
+    }
   }
+  if (groups.empty()) return;
+  const int X = std::max(1, num_xcds);
   std::stable_sort(groups.begin(), groups.end(),
-                   [](const Grp& a, const Grp& b) { return a.cost > b.cost; });
-  std::vector<int64_t> load(X, 0);
-  std::vector<std::vector<const T*>> lists(X);
-  for (const Grp& g : groups) {
-    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-    load[x] += g.cost;
-    for (size_t i = g.b; i < g.e; ++i) lists[x].push_back(&pf[i]);
+                   [](const detail::Group& a, const detail::Group& b) { return a.cost > b.cost; });
+  sc.load.assign(X, 0);
+  if ((int)sc.lists.size() < X) sc.lists.resize(X);
+  for (int x = 0; x < X; ++x) sc.lists[x].clear();
+  for (const detail::Group& g : groups) {
+    const int x = (int)(std::min_element(sc.load.begin(), sc.load.end()) - sc.load.begin());
+    sc.load[x] += g.cost;
+    const detail::Chunk& ch = sc.chunks[g.chunk];
+    for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i) {
+      const detail::Tile& tl = sc.tiles[i];
+      if (tl.ns <= g.split) continue;
+      const int32_t item = tl.item0 + g.split;
+      sc.lists[x].push_back({item * Hkv + g.kvh, cost[item]});
+    }
   }
   size_t longest = 0;
-  for (auto& l : lists) {
-    std::stable_sort(l.begin(), l.end(), [](const T* a, const T* b) { return a->cost > b->cost; });
+  for (int x = 0; x < X; ++x) {
+    auto& l = sc.lists[x];
+    std::stable_sort(l.begin(), l.end(), [](const Slot& a, const Slot& b) { return a.cost > b.cost; });
     longest = std::max(longest, l.size());
   }
-  PrefillItem empty{};
-  empty.n_tok = 0;
-  empty.part = -1;
-  out.reserve(longest * X);
+  slots.reserve(longest * X);
   for (size_t k = 0; k < longest; ++k)
-    for (int x = 0; x < X; ++x) out.push_back(k < lists[x].size() ? lists[x][k]->it : empty);
-  // drop trailing empty items
-  while (!out.empty() && out.back().n_tok == 0) out.pop_back();
+    for (int x = 0; x < X; ++x) slots.push_back(k < sc.lists[x].size() ? sc.lists[x][k].slot : -1);
+  // trailing idle slots change no XCD assignment
+  while (!slots.empty() && slots.back() < 0) slots.pop_back();
 }
 
 }  // namespace
@@ -97,17 +101,33 @@ int validate(const cp_attn_desc* d, const cp_row_meta* rows, int32_t n_rows) {
   const int64_t cap = (int64_t)d->max_blocks_per_req * d->block_size;
   if (cap > (int64_t)INT32_MAX) return CP_ERR_UNSUPPORTED;
   int64_t total = 0;
-  std::unordered_set<int32_t> seen;
-  seen.reserve((size_t)n_rows * 2);
-  for (int32_t r = 0; r < n_rows; ++r) {
+  int32_t r = 0;
+  for (; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
-    if (m.chunk_len < 0 || m.chunk_start < 0) return CP_ERR_BAD_META;
-    if ((int64_t)m.chunk_start + m.chunk_len != (int64_t)m.ctx_len) return CP_ERR_BAD_META;
-    if ((int64_t)m.ctx_len > cap) return CP_ERR_BAD_META;
-    if (m.req_id < 0 || m.req_id >= d->num_reqs_in_table) return CP_ERR_BAD_META;
-    if (!seen.insert(m.req_id).second) return CP_ERR_BAD_META;
+    if (m.chunk_len < 0 || m.chunk_start < 0) break;
+    if ((int64_t)m.chunk_start + m.chunk_len != (int64_t)m.ctx_len) break;
+    if ((int64_t)m.ctx_len > cap) break;
+    if (m.req_id < 0 || m.req_id >= d->num_reqs_in_table) break;
     total += m.chunk_len;
   }
+  if (r < n_rows) return CP_ERR_BAD_META;
+  // duplicate request ids: one bit per block-table row, cleared again after
+  thread_local std::vector<uint64_t> seen;
+  const size_t words = ((size_t)d->num_reqs_in_table + 63) / 64;
+  if (seen.size() < words) seen.resize(words, 0);
+  bool dup = false;
+  int32_t marked = 0;
+  for (; marked < n_rows; ++marked) {
+    const uint32_t id = (uint32_t)rows[marked].req_id;
+    const uint64_t bit = 1ull << (id & 63);
+    if (seen[id >> 6] & bit) {
+      dup = true;
+      break;
+    }
+    seen[id >> 6] |= bit;
+  }
+  for (int32_t i = 0; i < marked; ++i) seen[(uint32_t)rows[i].req_id >> 6] = 0;
+  if (dup) return CP_ERR_BAD_META;
   // token indices and q/out element offsets must fit the kernels' index types
   if (total > (int64_t)INT32_MAX / 2) return CP_ERR_UNSUPPORTED;
   return CP_OK;
@@ -126,143 +146,171 @@ Tuning tuning_from_env(int num_cus) {
 
 void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, const Tuning& t,
                 Plan& p) {
-  p = Plan();
+  PlanScratch& sc = p.scratch;
+  p.prefill.clear();
+  p.prefill_slots.clear();
+  p.prefill_wide.clear();
+  p.prefill_wide_slots.clear();
+  p.decode.clear();
+  p.merge.clear();
+  p.partial_rows = 0;
+  p.decode_split_blocks = 0;
   const int G = d.num_q_heads / d.num_kv_heads;
   const int Hkv = d.num_kv_heads;
   const int B = d.block_size;
   const int tile_tok = kPrefillRows / G;
 
   // token offsets in row order
-  std::vector<int64_t> off((size_t)n_rows + 1, 0);
+  auto& off = sc.off;
+  off.assign((size_t)n_rows + 1, 0);
   for (int32_t r = 0; r < n_rows; ++r) off[r + 1] = off[r] + rows[r].chunk_len;
 
   // ---- prefill tiles --------------------------------------------------
-  struct Tile {
-    int32_t tok0, n_tok, pos0, req, kv_end;
-    bool wide;
-  };
-  std::vector<Tile> tiles;
+  auto& tiles = sc.tiles;
+  auto& chunks = sc.chunks;
+  tiles.clear();
+  chunks.clear();
   int64_t pf_cost = 0;  // in kPrefillKeys-key steps, summed over tiles and kv heads
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len < t.prefill_min_len) continue;
     const bool wide = (int64_t)m.chunk_len * G > kPrefillRows;
     const int32_t tt = wide ? kPrefillRowsWide / G : tile_tok;
+    detail::Chunk ch{(int32_t)tiles.size(), 0, 0, wide};
     for (int32_t j = 0; j < m.chunk_len; j += tt) {
       const int32_t n = std::min<int32_t>(tt, m.chunk_len - j);
-      Tile tl{(int32_t)(off[r] + j), n, m.chunk_start + j, m.req_id, m.chunk_start + j + n, wide};
+      detail::Tile tl{(int32_t)(off[r] + j), n, m.chunk_start + j, m.req_id,
+                      m.chunk_start + j + n, wide, 0, 0};
       tiles.push_back(tl);
+      ++ch.n_tiles;
       pf_cost += ceil_div(tl.kv_end, kPrefillKeys) * Hkv * (wide ? 2 : 1);
     }
+    chunks.push_back(ch);
   }
   // Key ranges longer than split_keys are cut on a grid of multiples of
   // split_keys, the same grid for every tile, so the tiles of one chunk share
   // their split ranges exactly.  No cut lies past a tile's first query
   // position, so every query of a tile sees at least one key in every split.
+  // The split length is the work of one 128-row tile slot when the total is
+  // spread over pf_target slots (two per CU), so that chunks over long
+  // prefixes fill the GPU, but never under prefill_min_split steps: shorter
+  // splits cost more in partial rows and merging than they gain.
   const int64_t pf_target =
-      t.prefill_target_items > 0 ? t.prefill_target_items : (int64_t)t.num_cus * 4;
+      t.prefill_target_items > 0 ? t.prefill_target_items : (int64_t)t.num_cus * 2;
   const int64_t split_steps =
       tiles.empty() ? 1 : std::max<int64_t>(t.prefill_min_split, ceil_div(pf_cost, pf_target));
   const int64_t split_keys = split_steps * kPrefillKeys;
-  struct PfTmp {
-    PrefillItem it;
-    int64_t cost;
-    int64_t group;  // items sharing (request, kv head, key range start)
-  };
-  std::vector<PfTmp> pf, pfw;
-  std::vector<int32_t> bounds;
-  for (const Tile& tl : tiles) {
-    const int64_t last_cut = (tl.pos0 / kPrefillKeys) * (int64_t)kPrefillKeys;
-    bounds.assign(1, 0);
-    for (int64_t c = split_keys; c <= last_cut && c < tl.kv_end; c += split_keys)
-      bounds.push_back((int32_t)c);
-    bounds.push_back(tl.kv_end);
-    const int64_t ns = (int64_t)bounds.size() - 1;
-    for (int kvh = 0; kvh < Hkv; ++kvh) {
+  auto& bounds = sc.bounds;
+  sc.item_cost[0].clear();
+  sc.item_cost[1].clear();
+  for (detail::Chunk& ch : chunks) {
+    auto& items = ch.wide ? p.prefill_wide : p.prefill;
+    auto& cost = sc.item_cost[ch.wide ? 1 : 0];
+    for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i) {
+      detail::Tile& tl = tiles[i];
+      const int64_t last_cut = (tl.pos0 / kPrefillKeys) * (int64_t)kPrefillKeys;
+      bounds.assign(1, 0);
+      for (int64_t c = split_keys; c <= last_cut && c < tl.kv_end; c += split_keys)
+        bounds.push_back((int32_t)c);
+      bounds.push_back(tl.kv_end);
+      const int32_t ns = (int32_t)bounds.size() - 1;
+      const int32_t stride = ns * tl.n_tok * G;  // partial rows per kv head
       int32_t part0 = -1;
       if (ns > 1) {
         part0 = (int32_t)p.partial_rows;
-        p.partial_rows += ns * (int64_t)tl.n_tok * G;
+        p.partial_rows += (int64_t)Hkv * stride;
+        add_merge(p, tl.tok0, tl.n_tok, ns, part0, G, d.head_dim);
       }
-      for (int64_t s = 0; s < ns; ++s) {
+      tl.item0 = (int32_t)items.size();
+      tl.ns = ns;
+      ch.max_ns = std::max(ch.max_ns, ns);
+      for (int32_t s = 0; s < ns; ++s) {
         PrefillItem it;
         it.tok0 = tl.tok0;
         it.n_tok = tl.n_tok;
         it.pos0 = tl.pos0;
         it.req = tl.req;
-        it.kvh = kvh;
         it.kv_begin = bounds[s];
         it.kv_end = bounds[s + 1];
-        it.part = ns > 1 ? part0 + (int32_t)(s * tl.n_tok * G) : -1;
-        // group id: request, kv head and split start (split starts are grid points)
-        const int64_t gid = (((int64_t)tl.req * Hkv + kvh) << 20) + bounds[s] / split_keys;
-        (tl.wide ? pfw : pf).push_back({it, ceil_div(it.kv_end - it.kv_begin, kPrefillKeys), gid});
+        it.part = ns > 1 ? part0 + s * tl.n_tok * G : -1;
+        it.part_kvh_stride = ns > 1 ? stride : 0;
+        items.push_back(it);
+        cost.push_back(ceil_div(it.kv_end - it.kv_begin, kPrefillKeys));
       }
-      if (ns > 1) add_merge(p, tl.tok0, tl.n_tok, kvh, (int32_t)ns, part0, G, d.head_dim);
     }
   }
-  order_for_xcds(pf, t.num_xcds, p.prefill);
-  order_for_xcds(pfw, t.num_xcds, p.prefill_wide);
+  if ((int64_t)std::max(p.prefill.size(), p.prefill_wide.size()) * Hkv > INT32_MAX)
+    throw std::length_error("prefill slot index overflows int32");
+  order_for_xcds(false, sc.item_cost[0], Hkv, t.num_xcds, sc, p.prefill_slots);
+  order_for_xcds(true, sc.item_cost[1], Hkv, t.num_xcds, sc, p.prefill_wide_slots);
 
   // ---- decode ranges --------------------------------------------------
   int64_t dec_blocks = 0;
-  int64_t dec_pairs = 0;
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
     dec_blocks += ceil_div(m.ctx_len, B) * Hkv;
-    dec_pairs += Hkv;
   }
-  if (dec_pairs > 0) {
+  if (dec_blocks > 0) {
     const int64_t target =
         t.decode_target_items > 0 ? t.decode_target_items : (int64_t)t.num_cus * 8;
     int64_t sb = ceil_div(dec_blocks, target);
     sb = std::max<int64_t>(sb, 8);
     sb = ceil_div(sb, kDecodeWaves) * kDecodeWaves;
     p.decode_split_blocks = (int32_t)sb;
-    struct DcTmp {
-      DecodeItem it;
-      int64_t cost;
-    };
-    std::vector<DcTmp> dc;
+    // Items are placed longest first (a stable counting sort on their block
+    // count, which is at most sb): first count, then place.
+    auto& count = sc.count;
+    count.assign((size_t)sb + 2, 0);
     for (int32_t r = 0; r < n_rows; ++r) {
       const cp_row_meta& m = rows[r];
       if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
       const int64_t nb = ceil_div(m.ctx_len, B);
       const int64_t ns = std::max<int64_t>(1, ceil_div(nb, sb));
-      for (int kvh = 0; kvh < Hkv; ++kvh) {
-        int32_t part0 = -1;
-        if (ns > 1) {
-          part0 = (int32_t)p.partial_rows;
-          p.partial_rows += ns * (int64_t)G;
-          add_merge(p, (int32_t)off[r], 1, kvh, (int32_t)ns, part0, G, d.head_dim);
-        }
-        for (int64_t s = 0; s < ns; ++s) {
-          const int64_t b0 = nb * s / ns, b1 = nb * (s + 1) / ns;
-          DecodeItem it;
-          it.tok = (int32_t)off[r];
-          it.req = m.req_id;
-          it.kvh = kvh;
-          it.kv_begin = (int32_t)(b0 * B);
-          it.kv_end = (int32_t)std::min<int64_t>(b1 * B, m.ctx_len);
-          it.part = ns > 1 ? part0 + (int32_t)(s * G) : -1;
-          it.pad0 = it.pad1 = 0;
-          dc.push_back({it, b1 - b0});
-        }
+      for (int64_t s = 0; s < ns; ++s) ++count[nb * (s + 1) / ns - nb * s / ns];
+    }
+    int64_t n_items = 0;
+    for (int64_t c = sb + 1; c >= 0; --c) {  // count[c] becomes the first slot of cost c
+      const int64_t k = count[c];
+      count[c] = n_items;
+      n_items += k;
+    }
+    p.decode.resize((size_t)n_items);
+    for (int32_t r = 0; r < n_rows; ++r) {
+      const cp_row_meta& m = rows[r];
+      if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
+      const int64_t nb = ceil_div(m.ctx_len, B);
+      const int64_t ns = std::max<int64_t>(1, ceil_div(nb, sb));
+      int32_t part0 = -1;
+      if (ns > 1) {
+        part0 = (int32_t)p.partial_rows;
+        p.partial_rows += (int64_t)Hkv * ns * G;
+        add_merge(p, (int32_t)off[r], 1, (int32_t)ns, part0, G, d.head_dim);
+      }
+      for (int64_t s = 0; s < ns; ++s) {
+        const int64_t b0 = nb * s / ns, b1 = nb * (s + 1) / ns;
+        DecodeItem& it = p.decode[(size_t)count[b1 - b0]++];
+        it.tok = (int32_t)off[r];
+        it.req = m.req_id;
+        it.kv_begin = (int32_t)(b0 * B);
+        it.kv_end = (int32_t)std::min<int64_t>(b1 * B, m.ctx_len);
+        it.part = ns > 1 ? part0 + (int32_t)(s * G) : -1;
+        it.part_kvh_stride = ns > 1 ? (int32_t)(ns * G) : 0;
+        it.pad0 = it.pad1 = 0;
       }
     }
-    std::stable_sort(dc.begin(), dc.end(),
-                     [](const DcTmp& a, const DcTmp& b) { return a.cost > b.cost; });
-    p.decode.reserve(dc.size());
-    for (auto& x : dc) p.decode.push_back(x.it);
   }
 
   // ---- workspace layout ------------------------------------------------
   size_t o = 0;
   p.off_prefill = o;
   o = align_up(o + p.prefill.size() * sizeof(PrefillItem), 256);
+  p.off_prefill_slots = o;
+  o = align_up(o + p.prefill_slots.size() * sizeof(int32_t), 256);
   p.off_prefill_wide = o;
   o = align_up(o + p.prefill_wide.size() * sizeof(PrefillItem), 256);
+  p.off_prefill_wide_slots = o;
+  o = align_up(o + p.prefill_wide_slots.size() * sizeof(int32_t), 256);
   p.off_decode = o;
   o = align_up(o + p.decode.size() * sizeof(DecodeItem), 256);
   p.off_merge = o;
@@ -277,7 +325,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
 
 void build_append_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows,
                        AppendPlan& p) {
-  p = AppendPlan();
+  p.items.clear();
   const int B = d.block_size;
   int64_t tok = 0;
   for (int32_t r = 0; r < n_rows; ++r) {

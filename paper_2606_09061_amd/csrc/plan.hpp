@@ -27,36 +27,41 @@ constexpr int kPrefillKeys = 64;
 // Waves per decode workgroup (each wave walks every kDecodeWaves-th block).
 constexpr int kDecodeWaves = 4;
 
+// One item describes the work of every kv head.  Decode and merge kernels run
+// on a grid of (items, num_kv_heads).  Prefill workgroups take a slot each:
+// slot = item * num_kv_heads + kv head, in an order the planner chooses for
+// the XCDs, or -1 for an idle padding slot.  A split item's partial rows for
+// kv head h start at part + h * part_kvh_stride.
+
 struct PrefillItem {  // 32 bytes
   int32_t tok0;       // first query token (index into q / out)
-  int32_t n_tok;      // tokens in the tile, 1 .. kPrefillRows / G
+  int32_t n_tok;      // tokens in the tile, 1 .. kPrefillRows / G (or kPrefillRowsWide / G)
   int32_t pos0;       // absolute position of tok0 inside its request
   int32_t req;        // block-table row
-  int32_t kvh;        // kv head
   int32_t kv_begin;   // keys [kv_begin, kv_end) of the request
   int32_t kv_end;
-  int32_t part;       // -1: final output; else first partial row of this split
+  int32_t part;       // -1: final output; else first partial row of this split (kv head 0)
+  int32_t part_kvh_stride;
 };
 
 struct DecodeItem {   // 32 bytes
   int32_t tok;        // query token
   int32_t req;
-  int32_t kvh;
   int32_t kv_begin;
   int32_t kv_end;
-  int32_t part;       // -1: final output; else first partial row (G rows)
+  int32_t part;       // -1: final output; else first partial row (G rows, kv head 0)
+  int32_t part_kvh_stride;
   int32_t pad0, pad1;
 };
 
 struct MergeGroup {   // 32 bytes: rows [row0, row0 + n_rows) of one split group
   int32_t tok0;       // first token of the group
-  int32_t n_tok;      // tokens of the group (its rows = n_tok * G)
-  int32_t kvh;
+  int32_t n_tok;      // tokens of the group (its rows = n_tok * G per kv head)
   int32_t n_split;    // partials to combine per row
-  int32_t part0;      // row r of split s lives at part0 + s * n_tok * G + r
+  int32_t part0;      // kv head h, split s, row r: part0 + (h * n_split + s) * n_tok * G + r
   int32_t row0;       // first row this item merges
   int32_t n_rows;     // rows this item merges
-  int32_t pad0;
+  int32_t pad0, pad1;
 };
 
 struct AppendItem {   // 16 bytes: one request's new tokens inside one block
@@ -69,24 +74,61 @@ struct AppendItem {   // 16 bytes: one request's new tokens inside one block
 struct Tuning {
   int prefill_min_len = 2;      // rows with chunk_len >= this go to the MFMA kernel
   int decode_target_items = 0;  // 0: derived from the CU count
-  int prefill_target_items = 0;
-  int prefill_min_split = 32;   // shortest prefill split, in kPrefillKeys steps
+  int prefill_target_items = 0; // 0: two 128-row tiles' worth of work per CU
+  int prefill_min_split = 8;    // shortest prefill split, in kPrefillKeys steps
   int num_cus = 256;
   int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
 };
 
+namespace detail {
+struct Tile {
+  int32_t tok0, n_tok, pos0, req, kv_end;
+  bool wide;
+  int32_t item0, ns;  // its items: item0 .. item0 + ns - 1, one per split
+};
+struct Chunk {        // the tiles of one chunk, cut on one split grid
+  int32_t tile0, n_tiles, max_ns;
+  bool wide;
+};
+struct Group {        // items sharing one kv head's K/V range: (chunk, kv head, split)
+  int32_t chunk, kvh, split;
+  int64_t cost;
+};
+struct Slot {
+  int32_t slot;
+  int64_t cost;
+};
+}  // namespace detail
+
+// Temporaries of build_plan, kept between calls so that a steady stream of
+// batches plans without touching the allocator.
+struct PlanScratch {
+  std::vector<int64_t> off;
+  std::vector<detail::Tile> tiles;
+  std::vector<detail::Chunk> chunks;
+  std::vector<int32_t> bounds;
+  std::vector<int64_t> item_cost[2];
+  std::vector<detail::Group> groups;
+  std::vector<int64_t> load;
+  std::vector<std::vector<detail::Slot>> lists;
+  std::vector<int64_t> count;
+};
+
 struct Plan {
   std::vector<PrefillItem> prefill;       // 128-row tiles
+  std::vector<int32_t> prefill_slots;
   std::vector<PrefillItem> prefill_wide;  // 256-row tiles
+  std::vector<int32_t> prefill_wide_slots;
   std::vector<DecodeItem> decode;
   std::vector<MergeGroup> merge;
   int64_t partial_rows = 0;
   int32_t decode_split_blocks = 0;
   // workspace layout (byte offsets from the workspace base)
-  size_t off_prefill = 0, off_prefill_wide = 0, off_decode = 0, off_merge = 0, off_part_o = 0,
-         off_part_lse = 0;
+  size_t off_prefill = 0, off_prefill_slots = 0, off_prefill_wide = 0, off_prefill_wide_slots = 0,
+         off_decode = 0, off_merge = 0, off_part_o = 0, off_part_lse = 0;
   size_t plan_bytes = 0;   // bytes of the uploaded item lists
   size_t ws_bytes = 0;     // total workspace
+  PlanScratch scratch;
 };
 
 struct AppendPlan {
@@ -95,15 +137,18 @@ struct AppendPlan {
 };
 
 // Host validation shared by every entry point.  Returns CP_OK or a CP_ERR_*.
+// Thread-safe; duplicate request ids are found with a per-thread bitmap.
 int validate(const cp_attn_desc* d, const cp_row_meta* rows, int32_t n_rows);
 
-// Builds the attention plan; assumes validate() passed.
+// Builds the attention plan; assumes validate() passed.  Reuses the capacity
+// of every vector in `p`, so callers keep one Plan per thread.
 void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, const Tuning& t,
                 Plan& p);
 
 void build_append_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows,
                        AppendPlan& p);
 
+// Tuning from the CP_* environment variables, read on every call.
 Tuning tuning_from_env(int num_cus);
 
 }  // namespace cpattn

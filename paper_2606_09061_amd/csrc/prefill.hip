@@ -29,54 +29,14 @@
 // MFMA operand reads of 16 consecutive lanes hit distinct banks.
 #include "device.hpp"
 #include "kernels.hpp"
+#include "prefill_common.hpp"
 
 namespace cpattn {
 
-namespace {
-
-constexpr int BN = kPrefillKeys;  // keys per step
-
-// key row loaded into MFMA row c of a 32-key sub-tile: swaps bits 2 and 3
-__device__ __forceinline__ int sigma(int c) {
-  return (c & ~12) | ((c & 4) << 1) | ((c & 8) >> 1);
-}
-
-// key (within a 32-key sub-tile) of accumulator register r of lane half g:
-// sigma of the accumulator row 8*(r/4) + 4*g + r%4
-__device__ __forceinline__ int acc_key(int r, int g) {
-  return 16 * ((r >> 3) & 1) + 8 * g + 4 * ((r >> 2) & 1) + (r & 3);
-}
-
-__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
-
-}  // namespace
-
-template <int D, int B>
-struct PrefillLayout {
-  static constexpr int KCH = D / 8;          // 16-byte chunks per K row
-  static constexpr int K_BYTES = BN * D * 2;
-  static constexpr int V_BYTES = BN * D * 2;
-  static constexpr int BUF = K_BYTES + V_BYTES;
-  static constexpr int KV_TOTAL = 2 * BUF;
-  // query rows staged in LDS (wide tiles only): row r, chunk c -> byte offset
-  __device__ static int q_off(int r, int c) {
-    return KV_TOTAL + r * D * 2 + ((c ^ (r & (KCH - 1))) << 4);
-  }
-  static constexpr int VSLOTS = B / 8;       // 16-byte slots per V^T row
-  // K row `key`, chunk c -> byte offset
-  __device__ static int k_off(int key, int c) {
-    return key * D * 2 + ((c ^ (sigma(key & 15) & (KCH - 1))) << 4);
-  }
-  // V^T of step-block bi, feature row d, slot s (8 keys) -> byte offset
-  __device__ static int v_off(int bi, int d, int s) {
-    const int h = B == 16 ? (((d >> 2) ^ (d >> 3)) & 1) : ((d >> 2) & 3);
-    return K_BYTES + bi * D * B * 2 + d * B * 2 + ((s ^ h) << 4);
-  }
-};
-
 template <int D, int B, int G, int NW>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
-    const PrefillItem* __restrict__ items, const uint16_t* __restrict__ q,
+    const PrefillItem* __restrict__ items, const int32_t* __restrict__ slots,
+    const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
@@ -97,8 +57,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
   static_assert(CK >= 1 && CV >= 1, "tile geometry");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
-  const PrefillItem it = items[blockIdx.x];
-  if (it.n_tok == 0) return;  // padding slot of the XCD-interleaved order
+  const int slot = slots[blockIdx.x];
+  if (slot < 0) return;  // idle slot of the XCD-interleaved order
+  const int item = slot / hkv;
+  const int kvh = slot - item * hkv;
+  const PrefillItem it = items[item];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -111,8 +74,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
   const int qpos = it.pos0 + tl;
   const int32_t* bt_row = bt + (int64_t)it.req * mbr;
   const int64_t blk_elems = (int64_t)hkv * B * D;
-  const uint16_t* kbase = k_cache + (int64_t)it.kvh * B * D;
-  const uint16_t* vbase = v_cache + (int64_t)it.kvh * B * D;
+  const uint16_t* kbase = k_cache + (int64_t)kvh * B * D;
+  const uint16_t* vbase = v_cache + (int64_t)kvh * B * D;
 
   // Q^T operand: lane holds features [16 ks + 8 g, +8) of its query row
   uint4 qreg[kWide ? 1 : NKS];
@@ -125,12 +88,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
       const int t = r / G;
       uint4 v = make_uint4(0, 0, 0, 0);
       if (t < it.n_tok)
-        v = ld_global16(q + ((int64_t)(it.tok0 + t) * hq + it.kvh * G + r % G) * D + (x % KCH) * 8);
+        v = ld_global16(q + ((int64_t)(it.tok0 + t) * hq + kvh * G + r % G) * D + (x % KCH) * 8);
       *reinterpret_cast<uint4*>(smem + L::q_off(r, x % KCH)) = v;
     }
   } else {
     const uint16_t* qp =
-        q + ((int64_t)(it.tok0 + (row_valid ? tl : 0)) * hq + it.kvh * G + hh) * D + g * 8;
+        q + ((int64_t)(it.tok0 + (row_valid ? tl : 0)) * hq + kvh * G + hh) * D + g * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
       qreg[ks] = row_valid ? ld_global16(qp + ks * 16) : make_uint4(0, 0, 0, 0);
@@ -352,7 +315,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
   if (!row_valid) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (it.part < 0) {
-    uint16_t* op = out + ((int64_t)(it.tok0 + tl) * hq + it.kvh * G + hh) * D + 4 * g;
+    uint16_t* op = out + ((int64_t)(it.tok0 + tl) * hq + kvh * G + hh) * D + 4 * g;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -364,7 +327,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
         *reinterpret_cast<uint2*>(op + d0) = w;
       }
   } else {
-    const int prow = it.part + row;
+    const int prow = it.part + kvh * it.part_kvh_stride + row;
     float* pp = part_o + (int64_t)prow * D + 4 * g;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -380,50 +343,49 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
 }
 
 template <int D, int B, int G, int NW>
-static hipError_t launch_prefill_t(const PrefillItem* items, int n, const AttnArgs& a,
-                                   hipStream_t s) {
+static hipError_t launch_prefill_t(const PrefillItem* items, const int32_t* slots, int n,
+                                   const AttnArgs& a, hipStream_t s) {
   constexpr int smem = PrefillLayout<D, B>::KV_TOTAL + (NW == 8 ? NW * 32 * D * 2 : 0);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e =
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<D, B, G, NW>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((prefill_kernel<D, B, G, NW>), dim3(n), dim3(NW * 64), smem, s, items, a.q,
+  static const hipError_t attr =
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<D, B, G, NW>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((prefill_kernel<D, B, G, NW>), dim3(n), dim3(NW * 64), smem, s, items, slots,
+                     a.q,
                      a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv, a.mbr,
                      a.scale_log2);
   return hipGetLastError();
 }
 
 template <int D, int B, int NW>
-static hipError_t launch_prefill_g(int G, const PrefillItem* items, int n, const AttnArgs& a,
-                                   hipStream_t s) {
+static hipError_t launch_prefill_g(int G, const PrefillItem* items, const int32_t* slots, int n,
+                                   const AttnArgs& a, hipStream_t s) {
   switch (G) {
-    case 1: return launch_prefill_t<D, B, 1, NW>(items, n, a, s);
-    case 2: return launch_prefill_t<D, B, 2, NW>(items, n, a, s);
-    case 4: return launch_prefill_t<D, B, 4, NW>(items, n, a, s);
-    case 8: return launch_prefill_t<D, B, 8, NW>(items, n, a, s);
+    case 1: return launch_prefill_t<D, B, 1, NW>(items, slots, n, a, s);
+    case 2: return launch_prefill_t<D, B, 2, NW>(items, slots, n, a, s);
+    case 4: return launch_prefill_t<D, B, 4, NW>(items, slots, n, a, s);
+    case 8: return launch_prefill_t<D, B, 8, NW>(items, slots, n, a, s);
   }
   return hipErrorInvalidValue;
 }
 
 template <int NW>
-static hipError_t launch_prefill_w(int D, int G, const PrefillItem* items, int n,
-                                   const AttnArgs& a, hipStream_t s) {
-  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, items, n, a, s);
-  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, items, n, a, s);
-  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, items, n, a, s);
-  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, items, n, a, s);
+static hipError_t launch_prefill_w(int D, int G, const PrefillItem* items, const int32_t* slots,
+                                   int n, const AttnArgs& a, hipStream_t s) {
+  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, items, slots, n, a, s);
+  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, items, slots, n, a, s);
+  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, items, slots, n, a, s);
+  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, items, slots, n, a, s);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s) {
   hipError_t e = hipSuccess;
-  if (a.n_prefill_wide > 0)
-    e = launch_prefill_w<8>(D, G, a.prefill_wide, a.n_prefill_wide, a, s);
-  if (e == hipSuccess && a.n_prefill > 0) e = launch_prefill_w<4>(D, G, a.prefill, a.n_prefill, a, s);
+  if (a.n_prefill_wide_slots > 0)
+    e = launch_prefill_w<8>(D, G, a.prefill_wide, a.prefill_wide_slots, a.n_prefill_wide_slots, a,
+                            s);
+  if (e == hipSuccess && a.n_prefill_slots > 0)
+    e = launch_prefill_w<4>(D, G, a.prefill, a.prefill_slots, a.n_prefill_slots, a, s);
   return e;
 }
 

@@ -183,6 +183,6 @@ def test_plan_summary_counts_consistent():
     b = make_config(3)
     s = cp.plan_summary(cp.desc_for(b), b.rows)
     items = cp.plan_items(cp.desc_for(b), b.rows)
-    assert s["prefill_items"] + s["decode_items"] >= len(items)
+    assert s["prefill_items"] + s["decode_items"] == len(items)
     assert s["workspace_bytes"] == cp.workspace_bytes(cp.desc_for(b), b.rows)
     assert s["workspace_bytes"] >= s["partial_rows"] * (b.head_dim + 1) * 4
