@@ -20,11 +20,11 @@
 // so probabilities never leave registers.  Only steps that cross the causal
 // diagonal or the end of the range apply a mask.
 //
-// Pipeline: two LDS tiles and two register sets.  The global loads of step
-// s+2 are issued at the start of step s and written to LDS at the end of
-// step s+1, so every gather has two steps of MFMA work to arrive.  Block ids
-// are wave-uniform for every load instruction (a wave's 64 lanes read one
-// block), so the block base is computed once per wave in scalar registers.
+// The query operand Q^T stays in registers for the whole item.  Pipeline:
+// one register set stages the gather into one of two LDS tiles while the
+// other is computed.
+// Each load instruction reads 1 KiB of one block, so its block id is
+// wave-uniform and the block base lives in scalar registers.
 // LDS rows are XOR-swizzled in 16-byte units instead of padded so that the
 // MFMA operand reads of 16 consecutive lanes hit distinct banks.
 #include "device.hpp"
@@ -41,20 +41,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
   using L = PrefillLayout<D, B>;
-  // Wide (8-wave) tiles keep the query operand in LDS and double the
-  // register staging of the gather (two steps in flight); 4-wave tiles keep
-  // the query operand in registers with one step in flight.
-  constexpr bool kWide = NW == 8;
-  constexpr int NT = NW * 64;                   // threads
   constexpr int NKS = D / 16;                   // k-steps of S^T
   constexpr int NDT = D / 32;                   // 32-feature tiles of O^T
   constexpr int KCH = L::KCH;
-  constexpr int CK = BN * KCH / NT;             // K chunks per thread per step
   constexpr int VPB = D * B / 8;                // 16-byte chunks per V block (one kv head)
-  constexpr int CV = BN * D / 8 / NT;           // V chunks per thread per step
   constexpr int LOG2B = B == 16 ? 4 : 5;
   static_assert(B == 16 || B == 32, "block size");
-  static_assert(CK >= 1 && CV >= 1, "tile geometry");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const int slot = slots[blockIdx.x];
@@ -64,7 +56,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
   const PrefillItem it = items[item];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = uniform(tid >> 6);
   const int col = lane & 31;
   const int g = lane >> 5;
   const int row = wave * 32 + col;  // query row of the tile
@@ -78,93 +70,66 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
   const uint16_t* vbase = v_cache + (int64_t)kvh * B * D;
 
   // Q^T operand: lane holds features [16 ks + 8 g, +8) of its query row
-  uint4 qreg[kWide ? 1 : NKS];
-  if constexpr (kWide) {
-    // stage the tile's query rows in LDS: chunk x -> row x / KCH, chunk x % KCH
-#pragma unroll
-    for (int i = 0; i < NW * 32 * KCH / NT; ++i) {
-      const int x = i * NT + tid;
-      const int r = x / KCH;
-      const int t = r / G;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (t < it.n_tok)
-        v = ld_global16(q + ((int64_t)(it.tok0 + t) * hq + kvh * G + r % G) * D + (x % KCH) * 8);
-      *reinterpret_cast<uint4*>(smem + L::q_off(r, x % KCH)) = v;
-    }
-  } else {
+  uint4 qreg[NKS];
+  {
     const uint16_t* qp =
         q + ((int64_t)(it.tok0 + (row_valid ? tl : 0)) * hq + kvh * G + hh) * D + g * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
       qreg[ks] = row_valid ? ld_global16(qp + ks * 16) : make_uint4(0, 0, 0, 0);
   }
-  auto qop = [&](int ks) -> uint4 {
-    if constexpr (kWide)
-      return *reinterpret_cast<const uint4*>(smem + L::q_off(row, 2 * ks + g));
-    else
-      return qreg[ks];
-  };
 
-  // ---- gather geometry: K chunk i of this thread is x = i*NT + tid
-  // (key x / KCH, chunk x % KCH); V chunk i is x = i*NT + tid (step-block
-  // x / VPB, feature row, 8-key slot).  All of a wave's lanes read one block.
+  // ---- gather: a step is BN keys of K (token-major rows) and BN / B V
+  // blocks (feature-major).  The first half of the waves load the K rows,
+  // the second half the V blocks, each wave a contiguous run of 1 KiB pieces
+  // (64 lanes x 16 bytes).  K and V address alike: chunk x of the step lies
+  // in block x / VPB at element (x % VPB) * 8.  No piece straddles a block,
+  // so every load instruction needs one wave-uniform block-table entry.
+  // Every load is issued: a piece past the range re-reads the step's first
+  // block (a valid entry, since k0 < kv_end).  Scores of keys past the range
+  // are masked, so such K rows may hold anything; V past the range is zeroed.
+  constexpr int HALF = NW / 2;                  // waves loading K
+  constexpr int CPL = BN * KCH / (HALF * 64);   // 16-byte chunks per lane per step
+  static_assert(CPL >= 1 && VPB % 64 == 0 && VPB == B * KCH, "gather geometry");
   struct Regs {
-    uint4 k[CK], v[CV];
+    uint4 c[CPL];
   };
+  const bool vwave = wave >= HALF;
+  const int wbase = (vwave ? wave - HALF : wave) * CPL * 64;  // first chunk of this wave
+  const uint16_t* gbase = vwave ? vbase : kbase;
   auto gload = [&](Regs& r, int k0) {
     const int b0 = k0 >> LOG2B;
     const bool full = k0 + BN <= it.kv_end;
 #pragma unroll
-    for (int i = 0; i < CK; ++i) {
-      const int x = i * NT + tid;
-      const int key = x / KCH;
-      const int kb = uniform(key) >> LOG2B;       // block of this wave's keys
-      const bool live = full || (k0 + uniform(key) < it.kv_end);
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (live) {
-        const int64_t blk = bt_row[b0 + kb];
-        val = ld_global16(kbase + blk * blk_elems + (key & (B - 1)) * D + (x % KCH) * 8);
-      }
-      r.k[i] = val;
-    }
+    for (int i = 0; i < CPL; ++i) {
+      const int p = wbase + i * 64;  // first chunk of the piece
+      const int bi = p / VPB;
+      const bool live = full || (k0 + (vwave ? bi * B : p / KCH) < it.kv_end);
+      const uint16_t* bp = gbase + (int64_t)bt_row[b0 + (live ? bi : 0)] * blk_elems;
+      uint4 val = ld_global16(bp + ((p + lane) % VPB) * 8);
+      if (vwave && !full) {  // zero values of keys past the range
+        const int vpos = k0 + bi * B + (((p + lane) % VPB) % L::VSLOTS) * 8;
+        uint32_t* wv = reinterpret_cast<uint32_t*>(&val);
 #pragma unroll
-    for (int i = 0; i < CV; ++i) {
-      const int x = i * NT + tid;
-      const int bi = uniform(x / VPB);
-      const int w = x % VPB;
-      const int d = w / L::VSLOTS;
-      const int s = w % L::VSLOTS;
-      const int vpos = k0 + bi * B + s * 8;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (full || k0 + bi * B < it.kv_end) {
-        const int64_t blk = bt_row[b0 + bi];
-        val = ld_global16(vbase + blk * blk_elems + d * B + s * 8);
-        if (!full && vpos + 8 > it.kv_end) {  // zero values of keys past the range
-          uint32_t* wv = reinterpret_cast<uint32_t*>(&val);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint32_t lo = (vpos + 2 * e) < it.kv_end ? 0x0000ffffu : 0u;
-            const uint32_t hi = (vpos + 2 * e + 1) < it.kv_end ? 0xffff0000u : 0u;
-            wv[e] &= (lo | hi);
-          }
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = (vpos + 2 * e) < it.kv_end ? 0x0000ffffu : 0u;
+          const uint32_t hi = (vpos + 2 * e + 1) < it.kv_end ? 0xffff0000u : 0u;
+          wv[e] &= (lo | hi);
         }
       }
-      r.v[i] = val;
+      r.c[i] = val;
     }
+  };
+  // LDS destination of chunk i of this lane (fixed for the whole item)
+  auto soff = [&](int i) {
+    const int x = wbase + i * 64 + lane;
+    const int w = x % VPB;
+    return vwave ? L::v_off(x / VPB, w / L::VSLOTS, w % L::VSLOTS) : L::k_off(x / KCH, x % KCH);
   };
   auto sstore = [&](const Regs& r, int buf) {
     uint8_t* base = smem + buf * L::BUF;
 #pragma unroll
-    for (int i = 0; i < CK; ++i) {
-      const int x = i * NT + tid;
-      *reinterpret_cast<uint4*>(base + L::k_off(x / KCH, x % KCH)) = r.k[i];
-    }
-#pragma unroll
-    for (int i = 0; i < CV; ++i) {
-      const int x = i * NT + tid;
-      const int w = x % VPB;
-      *reinterpret_cast<uint4*>(base + L::v_off(x / VPB, w / L::VSLOTS, w % L::VSLOTS)) = r.v[i];
-    }
+    for (int i = 0; i < CPL; ++i) *reinterpret_cast<uint4*>(base + soff(i)) = r.c[i];
   };
 
   f32x16_t oacc[NDT];
@@ -180,31 +145,32 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
   // scheduling fences keep that order (left alone, the scheduler trades the
   // ring for registers and waits on every read).
   constexpr int kRing = 4;
-  auto compute = [&](int buf, int k0) {
+  // ---- S^T = K . Q^T of the step in buffer `buf`: MFMA i uses k-step i / 2
+  // and 32-key sub-tile i % 2
+  auto qk = [&](int buf, f32x16_t* sacc) {
     const uint8_t* base = smem + buf * L::BUF;
-    // ---- S^T = K . Q^T: MFMA i uses k-step i / 2 and 32-key sub-tile i % 2
     constexpr int NQK = 2 * NKS;
     auto kop = [&](int i) {
       return *reinterpret_cast<const uint4*>(base + L::k_off((i & 1) * 32 + krow0, 2 * (i >> 1) + g));
     };
-    f32x16_t sacc[2];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[kt][r] = 0.f;
-    {
-      uint4 ring[kRing];
+    uint4 ring[kRing];
 #pragma unroll
-      for (int i = 0; i < kRing; ++i) ring[i] = kop(i);
+    for (int i = 0; i < kRing; ++i) ring[i] = kop(i);
 #pragma unroll
-      for (int i = 0; i < NQK; ++i) {
-        const uint4 a = ring[i % kRing];
-        if (i + kRing < NQK) ring[i % kRing] = kop(i + kRing);
-        sacc[i & 1] = mfma32x32x16(a, qop(i >> 1), sacc[i & 1]);
-        __builtin_amdgcn_sched_barrier(0);  // keep reads kRing MFMAs ahead
-      }
+    for (int i = 0; i < NQK; ++i) {
+      const uint4 a = ring[i % kRing];
+      if (i + kRing < NQK) ring[i % kRing] = kop(i + kRing);
+      sacc[i & 1] = mfma32x32x16(a, qreg[i >> 1], sacc[i & 1]);
+      __builtin_amdgcn_sched_barrier(0);  // keep reads kRing MFMAs ahead
     }
-    // ---- online softmax on raw scores (the scale is folded into exp2)
+  };
+  // ---- online softmax on raw scores (the scale is folded into exp2); the
+  // bf16 weights come out as the P^T operand of the next product
+  auto softmax = [&](f32x16_t* sacc, int k0, uint4 (&pk)[2][2]) {
     const bool edge = (k0 + BN - 1 > it.pos0) || (k0 + BN > it.kv_end);
     if (edge) {
       // keys [k0, k0 + lim) are visible; register r of half g holds key
@@ -233,7 +199,6 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
         for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
     }
     const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
-    uint4 pk[2][2];
     const uint32_t ones = 0x3f803f80u;  // bf16 pair (1, 1)
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -251,63 +216,53 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
         }
         pk[kt][h2] = make_uint4(w[0], w[1], w[2], w[3]);
       }
-    // values of keys past the range were zeroed by the gather
-    // ---- O^T += V^T . P^T: MFMA i uses key step i / NDT and feature tile i % NDT
+  };
+  // ---- O^T += V^T . P^T with the step in buffer `buf` (values of keys past
+  // the range were zeroed by the gather): MFMA i uses key step i / NDT and
+  // feature tile i % NDT
+  auto pv = [&](int buf, const uint4 (&pk)[2][2]) {
+    const uint8_t* base = smem + buf * L::BUF;
     constexpr int NPV = 4 * NDT;
     auto vop = [&](int i) {
       const int ks2 = i / NDT, dt = i % NDT;
       return *reinterpret_cast<const uint4*>(
           base + L::v_off((ks2 * 16) / B, dt * 32 + col, ((ks2 * 16) % B) / 8 + g));
     };
-    {
-      uint4 ring[kRing];
+    uint4 ring[kRing];
 #pragma unroll
-      for (int i = 0; i < kRing; ++i) ring[i] = vop(i);
+    for (int i = 0; i < kRing; ++i) ring[i] = vop(i);
 #pragma unroll
-      for (int i = 0; i < NPV; ++i) {
-        const uint4 a = ring[i % kRing];
-        if (i + kRing < NPV) ring[i % kRing] = vop(i + kRing);
-        const int ks2 = i / NDT;
-        oacc[i % NDT] = mfma32x32x16(a, pk[ks2 >> 1][ks2 & 1], oacc[i % NDT]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+    for (int i = 0; i < NPV; ++i) {
+      const uint4 a = ring[i % kRing];
+      if (i + kRing < NPV) ring[i % kRing] = vop(i + kRing);
+      const int ks2 = i / NDT;
+      oacc[i % NDT] = mfma32x32x16(a, pk[ks2 >> 1][ks2 & 1], oacc[i % NDT]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
   const int n_step = (it.kv_end - it.kv_begin + BN - 1) / BN;
-  if constexpr (kWide) {
-    Regs ra, rb;
-    gload(ra, it.kv_begin);
-    sstore(ra, 0);
-    if (n_step > 1) gload(rb, it.kv_begin + BN);
+  auto step = [&](int buf, int k0) {
+    f32x16_t sacc[2];
+    uint4 pk[2][2];
+    qk(buf, sacc);
+    softmax(sacc, k0, pk);
+    pv(buf, pk);
+  };
+  // Two LDS buffers, step s in buffer s % 2: the loads of step s+1 are
+  // issued before step s is computed and written to the other buffer after
+  // it, so every gather has one step of MFMA work to arrive.
+  Regs ra;
+  gload(ra, it.kv_begin);
+  sstore(ra, 0);
+  __syncthreads();
+  for (int st = 0; st < n_step; ++st) {
+    const int k0 = it.kv_begin + st * BN;
+    const bool has_next = st + 1 < n_step;
+    if (has_next) gload(ra, k0 + BN);
+    step(st & 1, k0);
+    if (has_next) sstore(ra, (st & 1) ^ 1);
     __syncthreads();
-    for (int st = 0; st < n_step; st += 2) {
-      const int k0 = it.kv_begin + st * BN;
-      // even step: LDS 0 holds step st, rb carries step st+1
-      if (st + 2 < n_step) gload(ra, k0 + 2 * BN);
-      compute(0, k0);
-      if (st + 1 < n_step) sstore(rb, 1);
-      __syncthreads();
-      if (st + 1 >= n_step) break;
-      // odd step: LDS 1 holds step st+1, ra carries step st+2
-      if (st + 3 < n_step) gload(rb, k0 + 3 * BN);
-      compute(1, k0 + BN);
-      if (st + 2 < n_step) sstore(ra, 0);
-      __syncthreads();
-    }
-  } else {
-    Regs ra;
-    gload(ra, it.kv_begin);
-    sstore(ra, 0);
-    __syncthreads();
-    for (int st = 0; st < n_step; ++st) {
-      const int k0 = it.kv_begin + st * BN;
-      const bool has_next = st + 1 < n_step;
-      if (has_next) gload(ra, k0 + BN);
-      compute(st & 1, k0);
-      if (has_next) sstore(ra, (st & 1) ^ 1);
-      __syncthreads();
-    }
   }
 
   // ---- finish: the two lane halves hold disjoint keys of the same query
@@ -345,7 +300,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void prefill_kernel(
 template <int D, int B, int G, int NW>
 static hipError_t launch_prefill_t(const PrefillItem* items, const int32_t* slots, int n,
                                    const AttnArgs& a, hipStream_t s) {
-  constexpr int smem = PrefillLayout<D, B>::KV_TOTAL + (NW == 8 ? NW * 32 * D * 2 : 0);
+  constexpr int smem = 2 * PrefillLayout<D, B>::BUF;
   static const hipError_t attr =
       hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_kernel<D, B, G, NW>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, smem);

@@ -34,12 +34,7 @@ struct PrefillLayout {
   static constexpr int KCH = D / 8;          // 16-byte chunks per K row
   static constexpr int K_BYTES = BN * D * 2;
   static constexpr int V_BYTES = BN * D * 2;
-  static constexpr int BUF = K_BYTES + V_BYTES;
-  static constexpr int KV_TOTAL = 2 * BUF;
-  // query rows staged in LDS (wide tiles only): row r, chunk c -> byte offset
-  __device__ static int q_off(int r, int c) {
-    return KV_TOTAL + r * D * 2 + ((c ^ (r & (KCH - 1))) << 4);
-  }
+  static constexpr int BUF = K_BYTES + V_BYTES;  // one step's K and V^T
   static constexpr int VSLOTS = B / 8;       // 16-byte slots per V^T row
   // K row `key`, chunk c -> byte offset
   __device__ static int k_off(int key, int c) {
