@@ -84,6 +84,42 @@ void order_for_xcds(bool wide, const std::vector<int64_t>& cost, int Hkv, int nu
   while (!slots.empty() && slots.back() < 0) slots.pop_back();
 }
 
+// Makespan, in steps, of longest-first list scheduling of `groups` (cost,
+// count) on `slots` identical slots.  Slot loads are kept as a histogram
+// (load, slots) sorted by load, so equal items are placed in bulk.
+int64_t lpt_makespan(std::vector<std::pair<int64_t, int64_t>>& groups, int64_t slots,
+                     std::vector<std::pair<int64_t, int64_t>>& load) {
+  if (groups.empty()) return 0;
+  std::sort(groups.begin(), groups.end(),
+            [](const std::pair<int64_t, int64_t>& a, const std::pair<int64_t, int64_t>& b) {
+              return a.first > b.first;
+            });
+  load.assign(1, {0, slots});
+  size_t head = 0;  // load[head] is the least-loaded bucket; earlier ones are empty
+  for (const auto& g : groups) {
+    int64_t k = g.second;
+    if (head + 1 == load.size() && k >= slots) {  // all slots level: whole rounds at once
+      load[head].first += (k / slots) * g.first;
+      k %= slots;
+    }
+    while (k > 0) {
+      const int64_t l = load[head].first, take = std::min(k, load[head].second);
+      if ((load[head].second -= take) == 0) ++head;
+      // insert `take` slots at load l + g.first, keeping the order
+      const int64_t nl = l + g.first;
+      auto pos = std::lower_bound(
+          load.begin() + head, load.end(), nl,
+          [](const std::pair<int64_t, int64_t>& a, int64_t v) { return a.first < v; });
+      if (pos != load.end() && pos->first == nl)
+        pos->second += take;
+      else
+        load.insert(pos, {nl, take});
+      k -= take;
+    }
+  }
+  return load.back().first;
+}
+
 }  // namespace
 
 int validate(const cp_attn_desc* d, const cp_row_meta* rows, int32_t n_rows) {
@@ -144,6 +180,83 @@ Tuning tuning_from_env(int num_cus) {
   return t;
 }
 
+// Split length, in steps, for the prefill tiles.  Candidates are a 2^(1/8)
+// grid from prefill_min_split up to the longest tile, plus the lengths that
+// cut the longest tile into k equal parts; each is scored by the estimated
+// run time of the two prefill launches -- wide tiles one workgroup per CU,
+// 128-row tiles two -- under longest-first placement, plus the merge traffic
+// its partial rows cause, and the best wins.  A tile's splits are all
+// split_steps long except its last, so a candidate reduces to a few
+// (cost, count) groups.  prefill_target_items > 0 instead fixes the split at
+// the work of one slot when the total is spread over that many slots.
+static int64_t choose_split_steps(const cp_attn_desc& d, const Tuning& t,
+                                  const std::vector<detail::Tile>& tiles, PlanScratch& sc) {
+  const int Hkv = d.num_kv_heads;
+  const int G = d.num_q_heads / d.num_kv_heads;
+  int64_t max_steps = 1;
+  bool has[2] = {false, false};  // narrow, wide tiles present
+  for (const detail::Tile& tl : tiles) {
+    max_steps = std::max<int64_t>(max_steps, ceil_div(tl.kv_end, kPrefillKeys));
+    has[tl.wide ? 1 : 0] = true;
+  }
+  const int64_t min_split = std::max(1, t.prefill_min_split);
+  if (t.prefill_target_items > 0) {
+    int64_t cost = 0;
+    for (const detail::Tile& tl : tiles)
+      cost += ceil_div(tl.kv_end, kPrefillKeys) * Hkv * (tl.wide ? 2 : 1);
+    return std::max(min_split, ceil_div(cost, t.prefill_target_items));
+  }
+  auto& cand = sc.candidates;
+  cand.clear();
+  for (double sf = (double)min_split; sf < (double)max_steps; sf *= 1.09050773)
+    cand.push_back((int64_t)sf);
+  for (int64_t k = 1; k <= 32; ++k) {
+    const int64_t c = ceil_div(max_steps, k);
+    if (c < min_split) break;
+    cand.push_back(c);
+  }
+  cand.push_back(max_steps);
+  std::sort(cand.begin(), cand.end());
+  cand.erase(std::unique(cand.begin(), cand.end()), cand.end());
+  constexpr int64_t kItemOverhead = 2;  // steps: query load, first gather, output
+  // merge: one step of a wide tile is ~2 us at the kernel's rate, in which
+  // HBM moves ~10 MB; a partial row is written and read once, (D + 1) fp32
+  const double merge_bytes_per_step = 10.0e6 * d.head_dim / 128.0;
+  int64_t best_s = max_steps;
+  double best = -1.0;
+  for (const int64_t S : cand) {
+    const int64_t split_keys = S * kPrefillKeys;
+    double est = 0.0;
+    int64_t partial_rows = 0;
+    for (int wide = 0; wide < 2; ++wide) {
+      if (!has[wide]) continue;
+      auto& groups = sc.groups2;
+      groups.clear();
+      int64_t full = 0;  // splits of exactly S steps
+      for (const detail::Tile& tl : tiles) {
+        if ((int)tl.wide != wide) continue;
+        // cuts are the multiples of split_keys in (0, min(last_cut, kv_end - 1)]
+        const int64_t last_cut = (tl.pos0 / kPrefillKeys) * (int64_t)kPrefillKeys;
+        const int64_t cuts = std::min<int64_t>(last_cut, tl.kv_end - 1) / split_keys;
+        const int64_t ns = 1 + cuts;
+        const int64_t start = cuts * split_keys;
+        full += cuts;
+        groups.push_back({ceil_div(tl.kv_end - start, kPrefillKeys) + kItemOverhead, Hkv});
+        if (ns > 1) partial_rows += Hkv * ns * tl.n_tok * G;
+      }
+      if (full > 0) groups.push_back({S + kItemOverhead, full * Hkv});
+      const int64_t slots = (int64_t)t.num_cus * (wide ? 1 : 2);
+      est += (double)lpt_makespan(groups, slots, sc.load_hist);
+    }
+    est += (double)partial_rows * (d.head_dim + 1) * 8 / merge_bytes_per_step;
+    if (best < 0 || est < best) {
+      best = est;
+      best_s = S;
+    }
+  }
+  return best_s;
+}
+
 void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, const Tuning& t,
                 Plan& p) {
   PlanScratch& sc = p.scratch;
@@ -170,7 +283,6 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   auto& chunks = sc.chunks;
   tiles.clear();
   chunks.clear();
-  int64_t pf_cost = 0;  // in kPrefillKeys-key steps, summed over tiles and kv heads
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len < t.prefill_min_len) continue;
@@ -183,7 +295,6 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
                       m.chunk_start + j + n, wide, 0, 0};
       tiles.push_back(tl);
       ++ch.n_tiles;
-      pf_cost += ceil_div(tl.kv_end, kPrefillKeys) * Hkv * (wide ? 2 : 1);
     }
     chunks.push_back(ch);
   }
@@ -191,14 +302,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   // split_keys, the same grid for every tile, so the tiles of one chunk share
   // their split ranges exactly.  No cut lies past a tile's first query
   // position, so every query of a tile sees at least one key in every split.
-  // The split length is the work of one 128-row tile slot when the total is
-  // spread over pf_target slots (two per CU), so that chunks over long
-  // prefixes fill the GPU, but never under prefill_min_split steps: shorter
-  // splits cost more in partial rows and merging than they gain.
-  const int64_t pf_target =
-      t.prefill_target_items > 0 ? t.prefill_target_items : (int64_t)t.num_cus * 2;
-  const int64_t split_steps =
-      tiles.empty() ? 1 : std::max<int64_t>(t.prefill_min_split, ceil_div(pf_cost, pf_target));
+  const int64_t split_steps = tiles.empty() ? 1 : choose_split_steps(d, t, tiles, sc);
   const int64_t split_keys = split_steps * kPrefillKeys;
   auto& bounds = sc.bounds;
   sc.item_cost[0].clear();

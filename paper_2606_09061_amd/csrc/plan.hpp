@@ -11,6 +11,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <utility>
 #include <vector>
 
 #include "cp_attn.h"
@@ -74,7 +75,7 @@ struct AppendItem {   // 16 bytes: one request's new tokens inside one block
 struct Tuning {
   int prefill_min_len = 2;      // rows with chunk_len >= this go to the MFMA kernel
   int decode_target_items = 0;  // 0: derived from the CU count
-  int prefill_target_items = 0; // 0: two 128-row tiles' worth of work per CU
+  int prefill_target_items = 0; // 0: split length chosen by the run-time estimate
   int prefill_min_split = 8;    // shortest prefill split, in kPrefillKeys steps
   int num_cus = 256;
   int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
@@ -112,6 +113,9 @@ struct PlanScratch {
   std::vector<int64_t> load;
   std::vector<std::vector<detail::Slot>> lists;
   std::vector<int64_t> count;
+  std::vector<int64_t> candidates;                    // split lengths to score
+  std::vector<std::pair<int64_t, int64_t>> groups2;  // (cost, count) of one split candidate
+  std::vector<std::pair<int64_t, int64_t>> load_hist; // (slot load, slots), by load
 };
 
 struct Plan {
