@@ -27,14 +27,15 @@ __device__ __forceinline__ void append_span(const AppendItem& it,
   const int tid = threadIdx.x;
   constexpr int kChunks = D / 8;           // 16-byte chunks per K row
   constexpr int kPer = (B * kChunks + 255) / 256;
-  // K: span rows of this head, 16-byte chunks; all loads before any store
-  uint4 kv[kPer];
+  // K: span rows of this head, 16-byte chunks; all loads before any store.
+  // Loads are unconditional (rows past the span re-read its last row and are
+  // not stored), which keeps the staging array in registers.
+  u32x4_t kv[kPer];
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
     const int x = i * 256 + tid;
-    const int j = x / kChunks;
-    if (j < it.n_tok)
-      kv[i] = *reinterpret_cast<const uint4*>(k_new + ((int64_t)(it.tok0 + j) * hkv + h) * D +
+    const int j = min(x / kChunks, it.n_tok - 1);
+    kv[i] = *reinterpret_cast<const u32x4_t*>(k_new + ((int64_t)(it.tok0 + j) * hkv + h) * D +
                                               (x % kChunks) * 8);
   }
   // V: thread (slot tile ts, feature group fg) loads the 16-byte pieces of
@@ -48,16 +49,13 @@ __device__ __forceinline__ void append_span(const AppendItem& it,
   const int s_lo = max(8 * ts, slot0);
   const int s_hi = min(8 * ts + 8, slot0 + it.n_tok);
   const bool vwork = tid < NTS * NFG && s_lo < s_hi;
-  uint32_t w[8][4];  // w[e]: token in slot 8 ts + e, features 8 fg .. 8 fg + 7
+  u32x4_t w[8];  // w[e]: token in slot 8 ts + e, features 8 fg .. 8 fg + 7
   if (vwork) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int slot = 8 * ts + e;
-      uint4 r = make_uint4(0, 0, 0, 0);
-      if (slot >= s_lo && slot < s_hi)
-        r = *reinterpret_cast<const uint4*>(
-            v_new + ((int64_t)(it.tok0 + slot - slot0) * hkv + h) * D + fg * 8);
-      w[e][0] = r.x, w[e][1] = r.y, w[e][2] = r.z, w[e][3] = r.w;
+    for (int e = 0; e < 8; ++e) {  // slots outside the span re-read one inside it
+      const int slot = min(max(8 * ts + e, s_lo), s_hi - 1);
+      w[e] = *reinterpret_cast<const u32x4_t*>(
+          v_new + ((int64_t)(it.tok0 + slot - slot0) * hkv + h) * D + fg * 8);
     }
   }
 #pragma unroll
@@ -65,8 +63,8 @@ __device__ __forceinline__ void append_span(const AppendItem& it,
     const int x = i * 256 + tid;
     const int j = x / kChunks;
     if (j < it.n_tok)
-      *reinterpret_cast<uint4*>(k_cache + ((blk * hkv + h) * B + slot0 + j) * D +
-                                (x % kChunks) * 8) = kv[i];
+      *reinterpret_cast<u32x4_t*>(k_cache + ((blk * hkv + h) * B + slot0 + j) * D +
+                                  (x % kChunks) * 8) = kv[i];
   }
   if (vwork) {
     uint16_t* dst = v_cache + ((blk * hkv + h) * D + fg * 8) * B + 8 * ts;
@@ -78,12 +76,12 @@ __device__ __forceinline__ void append_span(const AppendItem& it,
 #pragma unroll
       for (int e = 0; e < 8; ++e) v16[e] = (w[e][f / 2] >> (16 * (f % 2))) & 0xffffu;
       if (whole) {
-        uint4 o;
-        o.x = v16[0] | (v16[1] << 16);
-        o.y = v16[2] | (v16[3] << 16);
-        o.z = v16[4] | (v16[5] << 16);
-        o.w = v16[6] | (v16[7] << 16);
-        *reinterpret_cast<uint4*>(dst + f * B) = o;
+        u32x4_t o;
+        o[0] = v16[0] | (v16[1] << 16);
+        o[1] = v16[2] | (v16[3] << 16);
+        o[2] = v16[4] | (v16[5] << 16);
+        o[3] = v16[6] | (v16[7] << 16);
+        *reinterpret_cast<u32x4_t*>(dst + f * B) = o;
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
