@@ -8,9 +8,14 @@ kv heads, head_dim 128, block 16; 2 prefill chunks of 192 tokens + 128
 decode rows) on one GPU and prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--config N] [--all]
+                  [--sub prefill|decode] [--cold N] [--no-cpu]
+  python bench.py --peaks
+  python bench.py --latency-table out.csv
 
 ``--config 5`` replays the 20-iteration 70B-shaped schedule (a step is one
-iteration, iterations cycle).  ``--all`` prints one line per mix.
+iteration, iterations cycle).  ``--all`` prints one line per mix.  ``--sub``
+times only the prefill rows or only the decode rows of the mix (same pools);
+``--cold`` adds steps timed after flushing the caches.
 """
 
 from __future__ import annotations
@@ -122,24 +127,41 @@ def cpu_baseline(batches, host_caches, tensors_host, budget_s=10.0, seed=0):
 
 # --------------------------------------------------------------------------- gpu run
 
-def build_inputs(cfg, device):
+SUB_MASKS = {"prefill": lambda rows: rows[:, 2] >= 2, "decode": lambda rows: rows[:, 2] == 1}
+
+
+def build_inputs(cfg, device, sub=None):
+    """Batches, per-batch step tensors, the shared pools, and for the replay
+    the full batches that fill its pools (``prime``).  ``sub`` keeps only the
+    prefill rows or only the decode rows of every batch (same pools)."""
     import workloads as wl
     if cfg == 5:
-        batches, _ = wl.replay_schedule()
-        kc, vc = wl.make_caches(batches[0], device=device, fill_prior=False, seed=5000)
-        steps = []
-        for i, b in enumerate(batches):
+        full, _ = wl.replay_schedule()
+        kc, vc = wl.make_caches(full[0], device=device, fill_prior=False, seed=5000)
+        prime = []
+        for i, b in enumerate(full):
             q, kn, vn, _ = wl.make_step_tensors(b, 5100 + i, device)
+            prime.append((b, {"q": q, "k_new": kn, "v_new": vn}))
+        if sub is None:
+            return full, [t for _, t in prime], {"k_cache": kc, "v_cache": vc}, prime
+        batches, steps = [], []
+        for i, b in enumerate(full):
+            sb = wl.subset(b, SUB_MASKS[sub](b.rows), sub)
+            q, kn, vn, _ = wl.make_step_tensors(sb, 5300 + i, device)
+            batches.append(sb)
             steps.append({"q": q, "k_new": kn, "v_new": vn})
-        shared = {"k_cache": kc, "v_cache": vc}
-        return batches, steps, shared
+        return batches, steps, {"k_cache": kc, "v_cache": vc}, prime
     b = wl.make_config(cfg)
     t = wl.make_tensors(b, seed=1000 + cfg, device=device)
-    steps = [{"q": t["q"], "k_new": t["k_new"], "v_new": t["v_new"]}]
-    return [b], steps, {"k_cache": t["k_cache"], "v_cache": t["v_cache"]}
+    shared = {"k_cache": t["k_cache"], "v_cache": t["v_cache"]}
+    if sub is None:
+        return [b], [{"q": t["q"], "k_new": t["k_new"], "v_new": t["v_new"]}], shared, []
+    sb = wl.subset(b, SUB_MASKS[sub](b.rows), sub)
+    q, kn, vn, _ = wl.make_step_tensors(sb, 1050 + cfg, device)
+    return [sb], [{"q": q, "k_new": kn, "v_new": vn}], shared, []
 
 
-def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0):
+def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, cold=0):
     import numpy as np
     import torch
     import paper_2606_09061_amd as cp
@@ -147,16 +169,12 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0):
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    log(f"[bench] building inputs for mix {cfg}")
-    batches, steps, shared = build_inputs(cfg, dev)
-    host = None
-    if with_cpu:
-        host = ((shared["k_cache"].cpu().view(torch.int16).numpy().view(np.uint16),
-                 shared["v_cache"].cpu().view(torch.int16).numpy().view(np.uint16)),
-                {k: v.cpu() for k, v in steps[0].items()})
+    log(f"[bench] building inputs for mix {cfg}" + (f" ({sub} rows only)" if sub else ""))
+    batches, steps, shared, prime = build_inputs(cfg, dev, sub)
     descs = [cp.desc_for(b) for b in batches]
     tables = [torch.from_numpy(b.block_tables).to(dev) for b in batches]
-    ws_bytes = max(cp.workspace_bytes(d, b.rows) for d, b in zip(descs, batches))
+    ws_bytes = max([cp.workspace_bytes(d, b.rows) for d, b in zip(descs, batches)] +
+                   [cp.workspace_bytes(cp.desc_for(b), b.rows) for b, _ in prime])
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     outs = [torch.empty(b.num_tokens, b.num_q_heads, b.head_dim, dtype=torch.bfloat16, device=dev)
             for b in batches]
@@ -170,47 +188,66 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0):
         cp.attn_mixed(d, t["q"], shared["k_cache"], shared["v_cache"], tables[j], b.rows, outs[j],
                       ws, stream=stream)
 
-    if cfg == 5:
-        # the replay's caches are built by its own appends: run the iterations
-        # once in order before timing so every later step reads real context
-        for i in range(len(batches)):
-            step(i)
+    if prime:
+        # the replay's caches are built by its own appends: run the full
+        # iterations once in order before timing so every step reads real context
+        for b, t in prime:
+            d = cp.desc_for(b)
+            bt = torch.from_numpy(b.block_tables).to(dev)
+            cp.kv_append(d, t["k_new"], t["v_new"], shared["k_cache"], shared["v_cache"], bt,
+                         b.rows, ws, stream=stream)
+            cp.attn_mixed(d, t["q"], shared["k_cache"], shared["v_cache"], bt, b.rows,
+                          torch.empty(b.num_tokens, b.num_q_heads, b.head_dim,
+                                      dtype=torch.bfloat16, device=dev), ws, stream=stream)
+    torch.cuda.synchronize()
+    host = None
+    if with_cpu:  # the pools as the first timed step finds them, for the oracle
+        host = ((shared["k_cache"].cpu().view(torch.int16).numpy().view(np.uint16),
+                 shared["v_cache"].cpu().view(torch.int16).numpy().view(np.uint16)),
+                {k: v.cpu() for k, v in steps[0].items()})
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     log(f"[bench] warmup done ({warmup} steps); timing {steps_n} steps")
-    def timed(n, detail):
-        """n steps between two events on the step stream; with ``detail`` also
-        an event after every step and the library's per-kernel event pairs."""
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1 if detail else 2)]
-        if detail:
+    def timed(n, mode):
+        """n steps on the step stream.  mode "total": only two bracketing
+        events; "steps": an event after every step as well; "kernels": the
+        library's per-kernel event pairs instead (these add GPU time)."""
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1 if mode == "steps" else 2)]
+        if mode == "kernels":
             binding.profile_begin()
         torch.cuda.synchronize()
         w0 = time.perf_counter()
         evs[0].record(stream)
         for i in range(n):
             step(i)
-            if detail:
+            if mode == "steps":
                 evs[i + 1].record(stream)
-        if not detail:
+        if mode != "steps":
             evs[1].record(stream)
         torch.cuda.synchronize()
         wall_s = time.perf_counter() - w0
-        prof_ = binding.profile_end() if detail else None
-        per = (np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(n)]) if detail else None)
+        prof_ = binding.profile_end() if mode == "kernels" else None
+        per = (np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(n)])
+               if mode == "steps" else None)
         return float(evs[0].elapsed_time(evs[-1])), wall_s, per, prof_
 
     # headline region: only the two bracketing events
-    total_ms, wall, _, _ = timed(steps_n, False)
-    # second region, same steps: per-step latencies and per-kernel durations
-    _, _, per_step, prof = timed(steps_n, True)
+    total_ms, wall, _, _ = timed(steps_n, "total")
+    # per-step latencies (at least 100 steps), then per-kernel durations
+    n_lat = max(steps_n, 100)
+    _, _, per_step, _ = timed(n_lat, "steps")
+    _, _, _, prof = timed(n_lat, "kernels")
     tokens = sum(batches[i % len(batches)].num_tokens for i in range(steps_n))
     log(f"[bench] timed region {total_ms:.3f} ms (wall {wall * 1e3:.3f} ms)")
 
-    # algorithmic work over the timed steps
-    works = [work_of(batches[i % len(batches)]) for i in range(steps_n)]
-    tot = {k: sum(w[k] for w in works) for k in works[0]}
-    kern = {k: {"ms_per_step": v[0] / steps_n, "launches": v[1]} for k, v in prof.items()}
+    # algorithmic work over the steps of each region
+    def work_over(n):
+        ws_ = [work_of(batches[i % len(batches)]) for i in range(n)]
+        return {k: sum(w[k] for w in ws_) for k in ws_[0]}
+    tot = work_over(n_lat)
+    head = work_over(steps_n)
+    kern = {k: {"ms_per_step": v[0] / n_lat, "launches": v[1]} for k, v in prof.items()}
     dominant = max(("prefill", "decode"), key=lambda k: prof[k][0])
     wl_name = CONFIG_NAMES_SHORT[cfg]
     if dominant == "prefill":
@@ -230,6 +267,14 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0):
     roof["traffic"] = traffic_for(roof["kernel"], wl_name)
     # the other kernel's fraction, for mixes where both matter
     other = {}
+    # the step against the roofline: t_pf = prefill flops at the MFMA peak,
+    # t_hbm = decode + append bytes at the HBM peak, per headline step
+    t_pf = head["prefill_flops"] / steps_n / (PEAK_BF16_TFLOPS * 1e12)
+    t_hbm = (head["decode_bytes"] + head["append_bytes"]) / steps_n / (PEAK_HBM_GBS * 1e9)
+    t_step = total_ms * 1e-3 / steps_n
+    roof_step = {"t_pf_us": t_pf * 1e6, "t_hbm_us": t_hbm * 1e6,
+                 "serialized_frac": (t_pf + t_hbm) / t_step,
+                 "overlapped_frac": max(t_pf, t_hbm) / t_step}
     if prof["prefill"][1] and dominant != "prefill":
         a = tot["prefill_flops"] / (prof["prefill"][0] * 1e-3) / 1e12
         other["prefill_tflops"] = a
@@ -253,23 +298,49 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) bf16 q/k/v, seeded batch metadata and block tables)",
-        "config": {"workload": f"{wl_name}: {CONFIG_DESC[cfg]}",
+        "config": {"workload": f"{wl_name}: {CONFIG_DESC[cfg]}" + (f" [{sub} rows only]" if sub else ""),
                    "heads_q_kv": [b0.num_q_heads, b0.num_kv_heads], "head_dim": b0.head_dim,
                    "block_size": b0.block_size,
                    "tokens_per_step": tokens / steps_n, "iterations": len(batches),
                    "parallelism": "single GPU"},
         "latency_ms": {"median": float(np.median(per_step)),
                        "p10": float(np.percentile(per_step, 10)),
-                       "p90": float(np.percentile(per_step, 90))},
+                       "p90": float(np.percentile(per_step, 90)), "reps": n_lat},
         "wall_ms_per_step": wall * 1e3 / steps_n,
         "kernels": kern,
         "roofline": roof,
+        "roofline_step": roof_step,
         "other_kernel": other,
     }
+    if cold:
+        # cold steps: a 1 GiB buffer is rewritten before each (outside its
+        # events), which evicts the 256 MB MALL and the L2s
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        cold_ms = []
+        for i in range(cold):
+            flush.zero_()
+            ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ea.record(stream)
+            step(i)
+            eb.record(stream)
+            eb.synchronize()
+            cold_ms.append(ea.elapsed_time(eb))
+        res["cold_latency_ms"] = {"median": float(np.median(cold_ms)),
+                                  "p10": float(np.percentile(cold_ms, 10)),
+                                  "p90": float(np.percentile(cold_ms, 90)), "reps": cold}
+        del flush
     if with_cpu:
         log("[bench] timing the fp64 oracle on a host sample")
-        sub = [batches[0]]
-        res["cpu_baseline"] = cpu_baseline(sub, host[0], host[1], budget_s=cpu_budget)
+        res["cpu_baseline"] = cpu_baseline([batches[0]], host[0], host[1], budget_s=cpu_budget)
+        if cfg in (1, 2):
+            import oracle
+            n_all = oracle.num_threads()
+            oracle.set_threads(1)
+            try:
+                res["cpu_baseline_1thread"] = cpu_baseline([batches[0]], host[0], host[1],
+                                                           budget_s=cpu_budget / 3)
+            finally:
+                oracle.set_threads(n_all)
     else:
         res["cpu_baseline"] = None
     return res
@@ -292,6 +363,148 @@ def copy_calibration(mib, reps):
     print(json.dumps({"copy_calibration_bytes_per_launch": n, "launches": reps}), flush=True)
 
 
+def measured_peaks(reps=20):
+    """Achieved rates of plain library operations on this GPU, beside the
+    datasheet peaks: a large bf16 GEMM (torch.matmul), a device copy and a
+    read-only reduction."""
+    import torch
+    dev = torch.device("cuda", 0)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) * 1e-3 / reps
+
+    n = 8192
+    x = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    y = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    t_mm = timed(lambda: torch.matmul(x, y))
+    del x, y
+    m = 1 << 31  # bytes
+    src = torch.ones(m, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    t_cp = timed(lambda: dst.copy_(src))
+    del dst
+    f = src.view(torch.float32)
+    t_rd = timed(lambda: f.sum())
+    return {"measured_peaks": {
+        "bf16_gemm_8192_tflops": 2 * n ** 3 / t_mm / 1e12,
+        "copy_2gib_gbs_read_plus_write": 2 * m / t_cp / 1e9,
+        "sum_2gib_read_gbs": m / t_rd / 1e9,
+        "datasheet": {"bf16_tflops": PEAK_BF16_TFLOPS, "hbm_gbs": PEAK_HBM_GBS}}}
+
+
+LT_DECODE_ROWS = (0, 16, 64, 128, 256)
+LT_DECODE_CTX = (512, 2048, 8192)
+LT_CHUNKS = (0, 1, 2, 4)
+LT_CHUNK_LEN = (64, 256, 512, 1024)
+LT_PRIOR = (0, 4096, 16384)
+
+
+def latency_table(path, reps=5, seeds=(0, 1, 2)):
+    """Latency-vs-composition sweep at the Llama-3-8B shape (32/8 heads,
+    head_dim 128, block 16): decode rows x decode context median x prefill
+    chunks x chunk length x prior context, three seeds each.  One pre-filled
+    pool serves every composition; only block tables and metadata change.
+    Columns: the raw and derived batch features of the paper's latency
+    predictor (Table 1 without the memory-state features, Table 2), the exact
+    query-key pair count, and measured append / attention / step latency."""
+    import csv
+    import math
+    import numpy as np
+    import torch
+    import paper_2606_09061_amd as cp
+    import workloads as wl
+    from workloads.tensors import _randn_bf16
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    hq, hkv, d, bsz = 32, 8, 128, 16
+    pool = 560_000  # blocks (37 GB of K and V): 256 rows at the 32768 clip fit
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7000)
+    kc = _randn_bf16((pool, hkv, bsz, d), gen, dev)
+    vc = _randn_bf16((pool, hkv, d, bsz), gen, dev)
+    stream = torch.cuda.current_stream()
+    combos = []
+    for nd in LT_DECODE_ROWS:
+        for med in (LT_DECODE_CTX if nd else (0,)):
+            for nc in LT_CHUNKS:
+                for cl in (LT_CHUNK_LEN if nc else (0,)):
+                    for pr in (LT_PRIOR if nc else (0,)):
+                        if nd == 0 and nc == 0:
+                            continue
+                        combos.extend((nd, med, nc, cl, pr, sd) for sd in seeds)
+    log(f"[bench] latency table: {len(combos)} compositions x {reps} reps")
+    cols = ["decode_rows_cfg", "decode_ctx_median_cfg", "chunks_cfg", "chunk_len_cfg",
+            "prior_cfg", "seed", "prefill_tokens", "decode_tokens", "batch_request_count",
+            "sum_decode_context_len", "max_decode_context_len", "prefill_processed_tokens",
+            "max_prefill_processed_tokens", "bias", "scheduled_tokens", "avg_decode_ctx",
+            "decode_ctx_interaction", "prefill_interaction", "qk_pairs_per_head",
+            "append_us", "attn_us", "step_us", "host_us"]
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
+    with open(path, "w", newline="") as fh:
+        out = csv.writer(fh)
+        out.writerow(cols)
+        for k, (nd, med, nc, cl, pr, sd) in enumerate(combos):
+            rng = np.random.default_rng([nd, med, nc, cl, pr, sd])
+            sl = []
+            if nd:
+                ctx = np.clip(np.round(rng.lognormal(math.log(med), 1.0, nd)), 16, 32768)
+                sl += [(int(c) - 1, 1) for c in ctx]
+            sl += [(pr, cl)] * nc
+            b = wl.make_batch("lt", hq, hkv, d, bsz, sl, rng, pool=pool)
+            q, kn, vn, _ = wl.make_step_tensors(b, 7100 + k, dev)
+            desc = cp.desc_for(b)
+            bt = torch.from_numpy(b.block_tables).to(dev)
+            need = cp.workspace_bytes(desc, b.rows)
+            if need > ws.numel():
+                ws = torch.empty(need, dtype=torch.uint8, device=dev)
+            o = torch.empty(b.num_tokens, hq, d, dtype=torch.bfloat16, device=dev)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            t_app, t_att, t_host = [], [], []
+            for r in range(reps + 2):
+                torch.cuda.synchronize()
+                h0 = time.perf_counter()
+                ev[0].record(stream)
+                cp.kv_append(desc, kn, vn, kc, vc, bt, b.rows, ws, stream=stream)
+                ev[1].record(stream)
+                cp.attn_mixed(desc, q, kc, vc, bt, b.rows, o, ws, stream=stream)
+                ev[2].record(stream)
+                h1 = time.perf_counter()
+                ev[2].synchronize()
+                if r >= 2:
+                    t_app.append(ev[0].elapsed_time(ev[1]) * 1e3)
+                    t_att.append(ev[1].elapsed_time(ev[2]) * 1e3)
+                    t_host.append((h1 - h0) * 1e6)
+            rows = b.rows
+            dec = rows[rows[:, 2] == 1]
+            pf = rows[rows[:, 2] >= 2]
+            pf_tok = int(pf[:, 2].sum())
+            dec_tok = int(dec.shape[0])
+            sum_dctx = int(dec[:, 3].sum())
+            processed = int(pf[:, 1].sum())
+            pairs = int(sum(int(c) * int(s0) + int(c) * (int(c) + 1) // 2 for _, s0, c, _ in pf))
+            avg_dctx = sum_dctx / max(dec_tok, 1)
+            app, att = float(np.median(t_app)), float(np.median(t_att))
+            out.writerow([nd, med, nc, cl, pr, sd, pf_tok, dec_tok, b.n_rows, sum_dctx,
+                          int(dec[:, 3].max()) if dec_tok else 0, processed,
+                          int(pf[:, 1].max()) if pf.size else 0, 1, pf_tok + dec_tok,
+                          round(avg_dctx, 3), round(dec_tok * avg_dctx, 3), pf_tok * processed,
+                          pairs, round(app, 2), round(att, 2), round(app + att, 2),
+                          round(float(np.median(t_host)), 1)])
+            if k % 100 == 0:
+                log(f"[bench] latency table {k}/{len(combos)}")
+    return {"latency_table": path, "compositions": len(combos), "reps": reps}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -303,9 +516,23 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain copies of MIB MiB (counter calibration)")
+    ap.add_argument("--sub", choices=["prefill", "decode"], default=None,
+                    help="time only the prefill rows or only the decode rows of the mix")
+    ap.add_argument("--cold", type=int, default=0, metavar="N",
+                    help="also time N steps with the MALL and L2 flushed before each")
+    ap.add_argument("--peaks", action="store_true",
+                    help="only measure library GEMM / copy / read rates")
+    ap.add_argument("--latency-table", default=None, metavar="CSV",
+                    help="only run the latency-vs-composition sweep, written to CSV")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, args.steps)
+        return
+    if args.peaks:
+        print(json.dumps(measured_peaks()), flush=True)
+        return
+    if args.latency_table:
+        print(json.dumps(latency_table(args.latency_table)), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the attention step is "
@@ -315,7 +542,7 @@ def main():
     cfgs = [1, 2, 3, 4, 5] if args.all else [args.config]
     for c in cfgs:
         res = run_config(c, args.steps, args.warmup, with_cpu=not args.no_cpu,
-                         cpu_budget=args.cpu_seconds)
+                         cpu_budget=args.cpu_seconds, sub=args.sub, cold=args.cold)
         print(json.dumps(res), flush=True)
 
 

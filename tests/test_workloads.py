@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from workloads import make_config, make_tensors, replay_schedule
+from workloads import make_batch, make_config, make_tensors, replay_schedule
 from workloads.tensors import tail_slots
 
 
@@ -113,3 +113,29 @@ def test_tensors_poison_and_seed():
     for req, s, c, ctx in b.rows.tolist():
         for p in range(s):
             assert torch.isfinite(kc[b.block_tables[req, p // 16], :, p % 16].float()).all()
+
+
+def test_subset_keeps_rows_tables_and_pool():
+    from workloads import subset
+    b = make_config(2)
+    dec = subset(b, b.rows[:, 2] == 1, "decode")
+    pf = subset(b, b.rows[:, 2] >= 2, "prefill")
+    assert dec.n_rows + pf.n_rows == b.n_rows
+    assert (dec.rows[:, 2] == 1).all() and (pf.rows[:, 2] >= 2).all()
+    assert dec.block_tables is b.block_tables and pf.num_blocks == b.num_blocks
+    assert dec.num_tokens + pf.num_tokens == b.num_tokens
+
+
+def test_make_batch_in_fixed_pool_draws_distinct_blocks():
+    rng = np.random.default_rng(11)
+    sl = [(1000, 1), (4095, 1), (0, 300), (8192, 64)]
+    b = make_batch("pooled", 32, 8, 128, 16, sl, rng, pool=5000)
+    assert b.num_blocks == 5000
+    used = []
+    for rid, s, c, ctx in b.rows.tolist():
+        nb = -(-ctx // 16)
+        used.extend(b.block_tables[rid, :nb].tolist())
+    assert len(used) == len(set(used)) and max(used) < 5000 and min(used) >= 0
+    assert b.poison_block not in used
+    with pytest.raises(ValueError):
+        make_batch("small", 32, 8, 128, 16, sl, np.random.default_rng(1), pool=10)

@@ -13,6 +13,7 @@ from .configs import (  # noqa: F401
     make_batch,
     make_config,
     replay_schedule,
+    subset,
     tiny_batch,
 )
 from .tensors import make_caches, make_step_tensors, make_tensors  # noqa: F401

@@ -107,19 +107,26 @@ def _lognormal_int(rng, median, n, lo, hi):
 
 
 def make_batch(name, hq, hkv, d, bsz, starts_lens, rng, n_spare=2, shuffle_req_ids=True,
-               mbr=None) -> Batch:
+               mbr=None, pool=None) -> Batch:
     """Builds a batch whose block tables deal a random permutation of the pool.
 
     starts_lens: list of (chunk_start, chunk_len) in row order.
     The pool holds exactly the blocks the rows need plus ``n_spare`` spare
-    blocks; spare block ``poison_block`` backs every unused table entry.
+    blocks, unless ``pool`` fixes its size (then the rows' blocks are a random
+    draw without replacement from it); spare block ``poison_block`` backs
+    every unused table entry.
     """
     starts_lens = [(int(s), int(c)) for s, c in starts_lens]
     n = len(starts_lens)
     nblk = [-(-(s + c) // bsz) for s, c in starts_lens]
     used = int(sum(nblk))
-    pool = used + max(1, n_spare)
-    perm = rng.permutation(pool).astype(np.int64)
+    if pool is None:
+        pool = used + max(1, n_spare)
+        perm = rng.permutation(pool).astype(np.int64)
+    else:
+        if pool < used + 1:
+            raise ValueError(f"pool of {pool} blocks cannot hold {used} blocks and a spare")
+        perm = rng.permutation(pool)[: used + 1].astype(np.int64)
     poison = int(perm[used])  # first spare block in permutation order
     mbr = int(mbr if mbr is not None else max([1] + nblk))
     req_ids = rng.permutation(n) if shuffle_req_ids else np.arange(n)
@@ -134,6 +141,16 @@ def make_batch(name, hq, hkv, d, bsz, starts_lens, rng, n_spare=2, shuffle_req_i
     referenced = np.zeros(pool, dtype=bool)
     referenced[perm[:used]] = True
     return Batch(name, hq, hkv, d, bsz, rows, bt, pool, poison, referenced=referenced)
+
+
+def subset(batch: Batch, keep, suffix: str) -> Batch:
+    """The rows of ``batch`` selected by the boolean mask ``keep``, over the same
+    pool and block tables (their tokens are renumbered in row order)."""
+    keep = np.asarray(keep, dtype=bool)
+    return Batch(f"{batch.name}-{suffix}", batch.num_q_heads, batch.num_kv_heads,
+                 batch.head_dim, batch.block_size, batch.rows[keep].copy(),
+                 batch.block_tables, batch.num_blocks, batch.poison_block, batch.sm_scale,
+                 referenced=batch.referenced)
 
 
 def tiny_batch(seed: int = 1) -> Batch:
