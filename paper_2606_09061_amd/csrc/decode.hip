@@ -140,16 +140,18 @@ __global__ __launch_bounds__(256, G * D >= 512 ? 3 : 4) void decode_kernel(
   const int kt1 = (it.kv_end + TK - 1) / TK;
   const int32_t* bt_row = bt + (int64_t)it.req * mbr;
   // tile t: K rows [t*TK % B, +TK) of its block (contiguous), and the same
-  // slots of every V feature row of the block
+  // slots of every V feature row of the block.  Each K/V byte is read by one
+  // workgroup only, so the loads are non-temporal (streamed past the caches
+  // instead of displacing lines other workgroups reuse).
   auto load_tile = [&](int t, uint4* kr, uint4* vr) {
     const int64_t blk = ((int64_t)bt_row[(t * TK) / B] * hkv + kvh) * head_elems;
     const int toff = (t * TK) % B;
     const uint16_t* kp = k_cache + blk + toff * D + lane * 8;
     const uint16_t* vp = v_cache + blk + vrow * B + toff + tc * 8;
 #pragma unroll
-    for (int i = 0; i < NL; ++i) kr[i] = ld_global16(kp + i * 512);
+    for (int i = 0; i < NL; ++i) kr[i] = ld_global16_nt(kp + i * 512);
 #pragma unroll
-    for (int i = 0; i < NL; ++i) vr[i] = ld_global16(vp + i * DPI * B);
+    for (int i = 0; i < NL; ++i) vr[i] = ld_global16_nt(vp + i * DPI * B);
   };
 
   // one tile: scores, online softmax, weighted values
