@@ -12,7 +12,7 @@ import torch
 
 import oracle
 from gpu_util import assert_close, run_step, say, words
-from workloads import Batch, make_caches, make_config, make_step_tensors, make_tensors
+from workloads import Batch, make_batch, make_caches, make_config, make_step_tensors, make_tensors
 from workloads import replay_schedule
 
 pytestmark = pytest.mark.gpu
@@ -122,3 +122,23 @@ def test_block_ids_beyond_2g_elements():
     assert bool(torch.isnan(vc[nb - 1].float()).all()), "poison block written"
     ref = oracle.attn(small, ref_t["q"], kc_ref, vc_ref)
     assert_close(out, ref, "big pool")
+
+
+def test_long_context_prefill_unsplit(monkeypatch):
+    """A chunk over 70k cached keys with the planner told not to split key
+    ranges: each prefill workgroup walks ~4400 blocks of one request."""
+    monkeypatch.setenv("CP_PREFILL_MIN_SPLIT", "100000")
+    rng = np.random.default_rng(21)
+    batch = make_batch("long", 32, 8, 128, 16, [(70_000, 300), (3000, 1)], rng)
+    say(f"[gpu] long context: rows={batch.n_rows} T={batch.num_tokens} blocks={batch.num_blocks}")
+    dev = torch.device("cuda", 0)
+    t = make_tensors(batch, seed=7100, device=dev)
+    host = {k: v.cpu() for k, v in t.items() if k in ("q", "k_new", "v_new")}
+    kc0, vc0 = words(t["k_cache"]), words(t["v_cache"])
+    out = run_step(batch, t)
+    torch.cuda.synchronize()
+    kc_ref, vc_ref = oracle.kv_append(batch, host["k_new"], host["v_new"], kc0, vc0)
+    del kc0, vc0
+    assert np.array_equal(words(t["k_cache"]).reshape(-1), kc_ref.reshape(-1)), "K pool differs"
+    assert np.array_equal(words(t["v_cache"]).reshape(-1), vc_ref.reshape(-1)), "V pool differs"
+    check_sampled(batch, out, host["q"], kc_ref, vc_ref, "long context", seed=3)
