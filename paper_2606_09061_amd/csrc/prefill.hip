@@ -279,9 +279,12 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
   });
   const int krow0 = sigma(col);
 
-  // MFMA operand addresses inside a tile.  K read i: key half i & 1, k-step
-  // i >> 1; its swizzled chunk differs per k-step, so one lane offset per
-  // k-step, the key half being a constant (the swizzle repeats every 16 keys).
+  // MFMA operand addresses inside a tile.  K read i: key half i / NKS, k-step
+  // i % NKS, so each half's k-steps run back to back (one accumulator's chain
+  // at a time keeps the matrix pipe fuller, with two waves per SIMD, than
+  // alternating two accumulators).  Its swizzled chunk differs per k-step, so
+  // one lane offset per k-step, the key half being a constant (the swizzle
+  // repeats every 16 keys).
   // V read i: 16-key slice i / NDT, feature tile i % NDT; the swizzle depends
   // on the lane and, for 32-key blocks, on the slice parity.  The offsets are
   // made opaque so the compiler adds buffer and tile offsets as immediates
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
   });
   auto kop = [&](const uint8_t* kb, auto i_c) {
     constexpr int i = decltype(i_c)::value;
-    return *reinterpret_cast<const uint4*>(kb + kofs[i >> 1] + (i & 1) * 32 * D * 2);
+    return *reinterpret_cast<const uint4*>(kb + kofs[i % NKS] + (i / NKS) * 32 * D * 2);
   };
   auto vop = [&](const uint8_t* vb, auto i_c) {
     constexpr int i = decltype(i_c)::value;
@@ -384,7 +387,7 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
       if constexpr (i + kRing < NQK) ring[i % kRing] = kop(kb, std::integral_constant<int, i + kRing>());
       static_for<0, RG>([&](auto rg_c) {
         constexpr int rg = decltype(rg_c)::value;
-        snext[rg][i & 1] = mfma32x32x16(a, qreg[rg][i >> 1], snext[rg][i & 1]);
+        snext[rg][i / NKS] = mfma32x32x16(a, qreg[rg][i % NKS], snext[rg][i / NKS]);
       });
       if constexpr (WITH_EXP) {
         static_for<i * NP / NQK, (i + 1) * NP / NQK>([&](auto j_c) {
