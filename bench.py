@@ -11,6 +11,7 @@ decode rows) on one GPU and prints one JSON line.
                   [--sub prefill|decode] [--cold N] [--no-cpu]
   python bench.py --peaks
   python bench.py --latency-table out.csv
+  python bench.py --fit out.csv
 
 ``--config 5`` replays the 20-iteration 70B-shaped schedule (a step is one
 iteration, iterations cycle).  ``--all`` prints one line per mix.  ``--sub``
@@ -502,7 +503,47 @@ def latency_table(path, reps=5, seeds=(0, 1, 2)):
                           round(float(np.median(t_host)), 1)])
             if k % 100 == 0:
                 log(f"[bench] latency table {k}/{len(combos)}")
-    return {"latency_table": path, "compositions": len(combos), "reps": reps}
+    res = {"latency_table": path, "compositions": len(combos), "reps": reps}
+    res.update(fit_latency(path))
+    return res
+
+
+def fit_latency(path):
+    """Least-squares fits of the measured step latency on the latency
+    predictor's derived batch features (Table 2 of the paper: bias,
+    scheduled_tokens, avg_decode_ctx, decode_ctx_interaction,
+    prefill_interaction), and on the same set with prefill_interaction
+    replaced by the exact query-key pair count of the prefill rows
+    (sum c*s + c(c+1)/2).  Errors are MAE, RMSE and MAPE as the paper defines
+    them for its predictor; also the median step latency per (decode rows,
+    prefill chunks) cell."""
+    import csv
+    import numpy as np
+    with open(path) as fh:
+        rows = list(csv.DictReader(fh))
+    y = np.array([float(r["step_us"]) for r in rows])
+
+    def cols(names):
+        return np.array([[float(r[n]) for n in names] for r in rows])
+
+    base = ["bias", "scheduled_tokens", "avg_decode_ctx", "decode_ctx_interaction"]
+    fits = {}
+    for name, feats in (("table2", base + ["prefill_interaction"]),
+                        ("table2_exact_pairs", base + ["qk_pairs_per_head"])):
+        X = cols(feats)
+        scale = np.abs(X).max(axis=0)
+        scale[scale == 0] = 1.0
+        w, *_ = np.linalg.lstsq(X / scale, y, rcond=None)
+        e = (X / scale) @ w - y
+        fits[name] = {"features": feats, "mae_us": float(np.abs(e).mean()),
+                      "rmse_us": float(np.sqrt((e ** 2).mean())),
+                      "mape_pct": float(100.0 * np.abs(e / y).mean())}
+    grid = {}
+    for r, v in zip(rows, y):
+        grid.setdefault((int(r["decode_rows_cfg"]), int(r["chunks_cfg"])), []).append(v)
+    cells = {f"{d}x{c}": float(np.median(v)) for (d, c), v in sorted(grid.items())}
+    return {"fits": fits, "median_step_us_by_decode_rows_x_chunks": cells,
+            "median_host_us": float(np.median([float(r["host_us"]) for r in rows]))}
 
 
 def main():
@@ -524,6 +565,8 @@ def main():
                     help="only measure library GEMM / copy / read rates")
     ap.add_argument("--latency-table", default=None, metavar="CSV",
                     help="only run the latency-vs-composition sweep, written to CSV")
+    ap.add_argument("--fit", default=None, metavar="CSV",
+                    help="only fit a latency table written earlier (no GPU)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, args.steps)
@@ -533,6 +576,9 @@ def main():
         return
     if args.latency_table:
         print(json.dumps(latency_table(args.latency_table)), flush=True)
+        return
+    if args.fit:
+        print(json.dumps(fit_latency(args.fit)), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the attention step is "
