@@ -356,8 +356,16 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     dec_blocks += ceil_div(m.ctx_len, B) * Hkv;
   }
   if (dec_blocks > 0) {
-    const int64_t target =
-        t.decode_target_items > 0 ? t.decode_target_items : (int64_t)t.num_cus * 8;
+    // Items per CU grow with the decode bytes: ~3 per CU (the kernel keeps
+    // three workgroups resident) for small loads, where every extra item costs
+    // plan upload, partial rows for the merge and a workgroup's start-up,
+    // rising to 6 per CU at 4 GB and above, where finer items balance the
+    // tail better (measured on the 0.1, 0.8, 1.8 and 5.5 GB mixes).
+    const double dec_bytes = (double)dec_blocks * B * d.head_dim * 4.0;
+    const double per_cu = 3.0 + 3.0 * std::min(1.0, dec_bytes / 4.0e9);
+    const int64_t target = t.decode_target_items > 0
+                               ? t.decode_target_items
+                               : std::max<int64_t>(1, (int64_t)(t.num_cus * per_cu));
     int64_t sb = ceil_div(dec_blocks, target);
     sb = std::max<int64_t>(sb, 8);
     sb = ceil_div(sb, kDecodeWaves) * kDecodeWaves;

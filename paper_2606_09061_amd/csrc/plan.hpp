@@ -74,7 +74,7 @@ struct AppendItem {   // 16 bytes: one request's new tokens inside one block
 
 struct Tuning {
   int prefill_min_len = 2;      // rows with chunk_len >= this go to the MFMA kernel
-  int decode_target_items = 0;  // 0: derived from the CU count
+  int decode_target_items = 0;  // 0: derived from the CU count and the decode bytes
   int prefill_target_items = 0; // 0: split length chosen by the run-time estimate
   int prefill_min_split = 8;    // shortest prefill split, in kPrefillKeys steps
   int num_cus = 256;
