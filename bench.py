@@ -402,6 +402,17 @@ def measured_peaks(reps=20):
         "datasheet": {"bf16_tflops": PEAK_BF16_TFLOPS, "hbm_gbs": PEAK_HBM_GBS}}}
 
 
+def gpu_mem_mb():
+    """The four GPU-memory features of the latency predictor's raw inputs
+    (Table 1): device memory used and free, and the torch caching
+    allocator's allocated and reserved bytes, in MB."""
+    import torch
+    free, total = torch.cuda.mem_get_info()
+    mb = 1.0 / (1 << 20)
+    return [round((total - free) * mb, 1), round(free * mb, 1),
+            round(torch.cuda.memory_allocated() * mb, 1), round(torch.cuda.memory_reserved() * mb, 1)]
+
+
 LT_DECODE_ROWS = (0, 16, 64, 128, 256)
 LT_DECODE_CTX = (512, 2048, 8192)
 LT_CHUNKS = (0, 1, 2, 4)
@@ -449,7 +460,8 @@ def latency_table(path, reps=5, seeds=(0, 1, 2)):
             "sum_decode_context_len", "max_decode_context_len", "prefill_processed_tokens",
             "max_prefill_processed_tokens", "bias", "scheduled_tokens", "avg_decode_ctx",
             "decode_ctx_interaction", "prefill_interaction", "qk_pairs_per_head",
-            "append_us", "attn_us", "step_us", "host_us"]
+            "append_us", "attn_us", "step_us", "host_us",
+            "gpu_mem_used_mb", "gpu_mem_free_mb", "cuda_allocated_mb", "cuda_reserved_mb"]
     ws = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
     with open(path, "w", newline="") as fh:
         out = csv.writer(fh)
@@ -500,7 +512,7 @@ def latency_table(path, reps=5, seeds=(0, 1, 2)):
                           int(pf[:, 1].max()) if pf.size else 0, 1, pf_tok + dec_tok,
                           round(avg_dctx, 3), round(dec_tok * avg_dctx, 3), pf_tok * processed,
                           pairs, round(app, 2), round(att, 2), round(app + att, 2),
-                          round(float(np.median(t_host)), 1)])
+                          round(float(np.median(t_host)), 1), *gpu_mem_mb()])
             if k % 100 == 0:
                 log(f"[bench] latency table {k}/{len(combos)}")
     res = {"latency_table": path, "compositions": len(combos), "reps": reps}

@@ -1,4 +1,5 @@
-"""Builds libcpattn.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree."""
+"""Builds, in-tree, libcpattn.so (HIP kernels + C ABI, gfx950, hipcc) and
+libcpsched.so (the host scheduler, plain C++17, g++)."""
 
 from __future__ import annotations
 
@@ -12,6 +13,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcpattn.so")
+SCHED_LIB = os.path.join(PKG, "libcpsched.so")
+CXX = os.environ.get("CXX", "g++")
 SOURCES = ["api.hip", "plan.cpp", "append.hip", "decode.hip", "prefill.hip", "merge.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -44,7 +47,19 @@ def build(jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
+    build_sched()
     return LIB
+
+
+def build_sched() -> str:
+    tmp = SCHED_LIB + ".tmp"
+    cmd = [CXX, "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall", "-Wextra",
+           "-I", os.path.join(ROOT, "include"), os.path.join(CSRC, "sched.cpp"), "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"{CXX} failed on sched.cpp:\n{r.stderr}")
+    os.replace(tmp, SCHED_LIB)
+    return SCHED_LIB
 
 
 if __name__ == "__main__":
