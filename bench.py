@@ -426,8 +426,10 @@ def latency_table(path, reps=5, seeds=(0, 1, 2)):
     chunks x chunk length x prior context, three seeds each.  One pre-filled
     pool serves every composition; only block tables and metadata change.
     Columns: the raw and derived batch features of the paper's latency
-    predictor (Table 1 without the memory-state features, Table 2), the exact
-    query-key pair count, and measured append / attention / step latency."""
+    predictor (Table 1, Table 2), the exact
+    query-key pair count, measured append / attention / step latency, and
+    Table 1's four GPU-memory features (constant here: one pool serves every
+    composition)."""
     import csv
     import math
     import numpy as np
@@ -558,6 +560,136 @@ def fit_latency(path):
             "median_host_us": float(np.median([float(r["host_us"]) for r in rows]))}
 
 
+# --------------------------------------------------------------------------- closed-loop scheduling
+
+SCHED_BASE = dict(policy=0, max_tokens=1024, max_seqs=256, max_seq_len=4096, delta=32,
+                  lambda_u=1.0, lambda_o=4.0, max_active=4, min_chunk=16)
+HIGH_US, REGULAR_US = 150.0, 1500.0  # request inter-arrival times (fixed interval)
+
+
+def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
+    """Closed-loop serving of the Qwen3-8B / Llama-3-8B attention step (32/8
+    heads, head_dim 128, block 16, 256 slots of up to 4,096 tokens) under the
+    C++ scheduler, the clock advanced by each round's measured step latency:
+      1. samples: the token-budget scheduler on uniform and short/long request
+         streams at several budgets and loads (the paper's offline profiling,
+         Sec. 3.2.1); each round gives the 16 features and the step latency;
+      2. the predictor: Table 7's MLP on the weighted asymmetric Huber loss,
+         8:1:1 split, test accuracy as Table 8 (and a Table-2 linear fit);
+      3. LPRS (Algorithm 1) against the token budget of 1,024 (Table 9's
+         comparison) at high and regular load, with and without APC, T* = the
+         token-budget run's mean step latency at high load;
+      4. Aging against FCFS (Sec. 4.2) on a short-prompt-heavy stream;
+      5. APC off / on under LPRS on the 49:1 short/long mix (Table 10)."""
+    import numpy as np
+    import torch
+    import workloads as wl
+    from paper_2606_09061_amd import lprs, sched, serve
+
+    os.makedirs(out_dir, exist_ok=True)
+    torch.cuda.set_device(0)
+    eng = serve.StepEngine(max_seqs=256, max_seq_len=4096, max_tokens=2048)
+
+    def cfg(**kw):
+        d = dict(SCHED_BASE)
+        d.update(kw)
+        return sched.make_config(**d)
+
+    def strip(r):
+        return {k: v for k, v in r.items() if not k.startswith("_")}
+
+    out = {"workload": "qwen3-8b-attention-closed-loop", "shape": "32/8 heads, d128, B16",
+           "high_interval_us": HIGH_US, "regular_interval_us": REGULAR_US}
+    serve.serve(cfg(), wl.uniform_stream(60, HIGH_US, seed=99), eng)  # warm-up
+    log("[sched] warm-up done")
+
+    # 1. samples
+    X, Y, runs = [], [], []
+    plan = [(b, iv, "uniform") for b in (256, 512, 1024, 2048) for iv in (HIGH_US, REGULAR_US)]
+    plan += [(256, None, "short_long"), (1024, None, "short_long")]
+    for i, (bmax, iv, kind) in enumerate(plan):
+        reqs = (wl.uniform_stream(n_collect, iv, seed=10 + i) if kind == "uniform"
+                else wl.short_long_stream(n_collect, seed=10 + i))
+        t0 = time.time()
+        r = serve.serve(cfg(max_tokens=bmax), reqs, eng, record=True)
+        X.append(r["_features"])
+        Y.append(r["_step_us"])
+        runs.append({"max_tokens": bmax, "interval_us": iv, "stream": kind, "rounds": r["rounds"]})
+        log(f"[sched] samples {i + 1}/{len(plan)}: B={bmax} {kind} {iv}: {r['rounds']} rounds, "
+            f"{time.time() - t0:.1f}s")
+    X = np.concatenate(X)
+    Y = np.concatenate(Y)
+    np.savetxt(os.path.join(out_dir, "samples.csv"), np.column_stack([X, Y]), delimiter=",",
+               header=",".join(list(sched.FEATURES) + ["step_us"]), comments="", fmt="%.6g")
+    out["samples"] = {"n": int(len(Y)), "runs": runs}
+
+    # 2. predictor
+    keep = lprs.downsample(X, Y, cap=3000, seed=0)
+    X, Y = X[keep], Y[keep]
+    out["samples"]["kept_after_downsampling"] = int(len(Y))
+    tr, va, te = lprs.split_811(len(Y), seed=0)
+    t0 = time.time()
+    model = lprs.LatencyPredictor().fit(
+        X[tr], Y[tr], X[va], Y[va], epochs=epochs,
+        progress=lambda ep, loss: log(f"[sched] predictor epoch {ep}: val loss {loss:.5f}"))
+    out["predictor"] = {"train_s": time.time() - t0, "split": [len(tr), len(va), len(te)],
+                        "test": lprs.accuracy(Y[te], model.predict(X[te]))}
+    lin = [sched.FEATURES.index(f) for f in ("bias", "scheduled_tokens", "avg_decode_ctx",
+                                               "decode_ctx_interaction", "prefill_interaction")]
+    sc = np.abs(X[tr][:, lin]).max(axis=0)
+    sc[sc == 0] = 1
+    w, *_ = np.linalg.lstsq(X[tr][:, lin] / sc, Y[tr], rcond=None)
+    out["predictor"]["table2_linear_test"] = lprs.accuracy(Y[te], (X[te][:, lin] / sc) @ w)
+    log(f"[sched] predictor: {json.dumps(out['predictor']['test'])}")
+
+    # 3. LPRS vs token budget
+    cmp = {}
+    for name, iv in (("high", HIGH_US), ("regular", REGULAR_US)):
+        reqs = wl.uniform_stream(n_req, iv, seed=1000)
+        tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
+        if name == "high":
+            t_star = float(round(tb["step_us"]["mean"]))
+            out["target_us"] = t_star
+        tb_t = dict(strip(tb))
+        st = tb["_step_us"]
+        tb_t["frac_over_target"] = float((st > t_star).mean())
+        tb_t["mean_abs_dev_from_target_us"] = float(np.abs(st - t_star).mean())
+        row = {"token_budget_1024": tb_t}
+        for bmax, apc_on in ((1024, False), (1024, True), (2048, True)):
+            r = serve.serve(cfg(max_tokens=bmax, chunking=sched.CHUNK_LPRS, target_us=t_star,
+                                apc=apc_on), reqs, eng, predictor=model)
+            row[f"lprs_B{bmax}" + ("_apc" if apc_on else "")] = strip(r)
+        cmp[name] = row
+        log(f"[sched] LPRS vs token budget at {name} load done")
+    out["lprs_vs_token_budget"] = cmp
+
+    # 4. Aging vs FCFS (short-prompt-heavy stream, fine chunks)
+    aging = {}
+    reqs = wl.uniform_stream(n_req, 40.0, seed=2000, max_seq_len=1024, prompt_median=19,
+                             output_median=64, sigma=1.75)
+    for bmax in (128, 512):
+        row = {"fcfs": strip(serve.serve(cfg(max_tokens=bmax, policy=sched.POLICY_FCFS), reqs, eng))}
+        for ratio in (0.01, 0.1):
+            row[f"aging_alpha_over_beta_{ratio}"] = strip(serve.serve(
+                cfg(max_tokens=bmax, policy=sched.POLICY_AGING, alpha=ratio, beta=-1.0), reqs, eng))
+        aging[f"B{bmax}"] = row
+    out["aging_vs_fcfs"] = aging
+    log("[sched] aging vs FCFS done")
+
+    # 5. APC ablation under LPRS (49:1 short/long mix)
+    reqs = wl.short_long_stream(n_req, seed=3000)
+    apc = {}
+    for on in (False, True):
+        apc["on" if on else "off"] = strip(serve.serve(
+            cfg(max_tokens=1024, chunking=sched.CHUNK_LPRS, target_us=out["target_us"], apc=on),
+            reqs, eng, predictor=model))
+    out["apc_ablation"] = apc
+    log("[sched] APC ablation done")
+    with open(os.path.join(out_dir, "sched_results.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -577,6 +709,8 @@ def main():
                     help="only measure library GEMM / copy / read rates")
     ap.add_argument("--latency-table", default=None, metavar="CSV",
                     help="only run the latency-vs-composition sweep, written to CSV")
+    ap.add_argument("--sched", default=None, metavar="DIR",
+                    help="only run the closed-loop scheduling experiment, results under DIR")
     ap.add_argument("--fit", default=None, metavar="CSV",
                     help="only fit a latency table written earlier (no GPU)")
     args = ap.parse_args()
@@ -591,6 +725,9 @@ def main():
         return
     if args.fit:
         print(json.dumps(fit_latency(args.fit)), flush=True)
+        return
+    if args.sched:
+        print(json.dumps(sched_experiment(args.sched)), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the attention step is "

@@ -28,11 +28,13 @@ struct Request {
 
 struct Mlp {
   std::vector<int32_t> dims;
-  std::vector<double> w, b, mean, inv_std;
+  std::vector<double> wt, b, mean, inv_std;  // wt: per layer [din][dout] (transposed)
   double y_scale = 1.0;
   bool loaded() const { return !dims.empty(); }
 
-  // Forward pass over n rows of x[n][NF]; out[n].
+  // Forward pass over n rows of x[n][NF]; out[n].  Each layer accumulates
+  // input-by-input into all outputs (contiguous, vectorisable), skipping
+  // inputs that the previous ReLU zeroed.
   void forward(const double* x, int n, double* out) const {
     const int L = (int)dims.size() - 1;
     int widest = 0;
@@ -43,13 +45,18 @@ struct Mlp {
       size_t wo = 0, bo = 0;
       for (int l = 0; l < L; ++l) {
         const int din = dims[l], dout = dims[l + 1];
-        for (int o = 0; o < dout; ++o) {
-          const double* wr = &w[wo + (size_t)o * din];
-          double acc = b[bo + o];
-          for (int i = 0; i < din; ++i) acc += wr[i] * a[i];
-          z[o] = (l + 1 < L) ? std::max(acc, 0.0) : acc;
+        double* __restrict zz = z.data();
+        for (int o = 0; o < dout; ++o) zz[o] = b[bo + o];
+        for (int i = 0; i < din; ++i) {
+          const double ai = a[i];
+          if (ai == 0.0) continue;
+          const double* __restrict wr = &wt[wo + (size_t)i * dout];
+          for (int o = 0; o < dout; ++o) zz[o] += ai * wr[o];
         }
-        std::copy(z.begin(), z.begin() + dout, a.begin());
+        if (l + 1 < L)
+          for (int o = 0; o < dout; ++o) a[o] = std::max(zz[o], 0.0);
+        else
+          for (int o = 0; o < dout; ++o) a[o] = zz[o];
         wo += (size_t)din * dout;
         bo += dout;
       }
@@ -69,10 +76,10 @@ bool valid_config(const cps_config& c) {
          c.max_active >= 1 && c.min_chunk >= 1;
 }
 
-void features(const cp_row_meta* rows, int n, const double* mem, double* f) {
+// Raw batch statistics of Table 1 (all but the memory state), accumulated row by row.
+struct Agg {
   double pf_tok = 0, dec_tok = 0, count = 0, sum_dctx = 0, max_dctx = 0, proc = 0, max_proc = 0;
-  for (int i = 0; i < n; ++i) {
-    const cp_row_meta& r = rows[i];
+  void add(const cp_row_meta& r) {
     if (r.chunk_len > 0) count += 1;
     if (r.chunk_len == 1) {
       dec_tok += 1;
@@ -84,11 +91,20 @@ void features(const cp_row_meta* rows, int n, const double* mem, double* f) {
       max_proc = std::max(max_proc, (double)r.chunk_start);
     }
   }
-  const double avg = sum_dctx / std::max(dec_tok, 1.0);
-  const double v[NF] = {pf_tok,  dec_tok, count,  sum_dctx, max_dctx,      proc,
-                        max_proc, mem[0], mem[1], mem[2],   mem[3],        1.0,
-                        dec_tok + pf_tok, avg, dec_tok * avg, pf_tok * proc};
-  std::memcpy(f, v, sizeof(v));
+  // Table 1 followed by the derived features of Table 2.
+  void emit(const double* mem, double* f) const {
+    const double avg = sum_dctx / std::max(dec_tok, 1.0);
+    const double v[NF] = {pf_tok,  dec_tok, count,  sum_dctx, max_dctx,      proc,
+                          max_proc, mem[0], mem[1], mem[2],   mem[3],        1.0,
+                          dec_tok + pf_tok, avg, dec_tok * avg, pf_tok * proc};
+    std::memcpy(f, v, sizeof(v));
+  }
+};
+
+void features(const cp_row_meta* rows, int n, const double* mem, double* f) {
+  Agg g;
+  for (int i = 0; i < n; ++i) g.add(rows[i]);
+  g.emit(mem, f);
 }
 
 // Eq. 8: {1, h} together with the positive multiples of delta up to h, ascending.
@@ -142,7 +158,6 @@ struct cps_sched {
   cps_stats stats{};
   // Scratch of Algorithm 1.
   std::vector<int32_t> cand;
-  std::vector<cp_row_meta> rows_tmp;
   std::vector<double> feat, pred;
 
   static bool heap_less(const Entry& a, const Entry& b) {
@@ -177,14 +192,14 @@ struct cps_sched {
     const int32_t h = (int32_t)h64;
     candidates(h, cfg.delta, cand);
     const int nc = (int)cand.size();
-    rows_tmp.assign(committed, committed + n);
-    rows_tmp.push_back({slot, processed, 0, processed});
+    Agg base;
+    for (int32_t i = 0; i < n; ++i) base.add(committed[i]);
     feat.resize((size_t)nc * NF);
     pred.resize(nc);
     for (int k = 0; k < nc; ++k) {
-      rows_tmp.back().chunk_len = cand[k];
-      rows_tmp.back().ctx_len = processed + cand[k];
-      features(rows_tmp.data(), n + 1, mem, &feat[(size_t)k * NF]);
+      Agg g = base;
+      g.add({slot, processed, cand[k], processed + cand[k]});
+      g.emit(mem, &feat[(size_t)k * NF]);
     }
     mlp.forward(feat.data(), nc, pred.data());  // Eq. 9
     stats.lprs_calls += 1;
@@ -245,7 +260,11 @@ int cps_set_predictor(cps_sched* s, int32_t n_layers, const int32_t* dims, const
     if (!(x_std[k] > 0.0) || !std::isfinite(x_mean[k])) return CPS_ERR_INVALID_ARG;
   Mlp m;
   m.dims.assign(dims, dims + n_layers + 1);
-  m.w.assign(weights, weights + nw);
+  m.wt.resize(nw);
+  for (int32_t l = 0, off = 0; l < n_layers; off += dims[l] * dims[l + 1], ++l)
+    for (int32_t o = 0; o < dims[l + 1]; ++o)
+      for (int32_t i = 0; i < dims[l]; ++i)
+        m.wt[(size_t)off + (size_t)i * dims[l + 1] + o] = weights[(size_t)off + (size_t)o * dims[l] + i];
   m.b.assign(biases, biases + nb);
   m.mean.assign(x_mean, x_mean + NF);
   m.inv_std.resize(NF);

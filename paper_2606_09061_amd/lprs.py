@@ -51,6 +51,25 @@ def table_features(columns: dict) -> np.ndarray:
     return np.stack([raw[k] for k in FEATURES], axis=1)
 
 
+def downsample(X, y, cap=3000, seed=0):
+    """Caps over-represented batch shapes (Sec. 3.2.1's downsampling): samples
+    are grouped by the power-of-two bucket of their scheduled tokens and by
+    whether the batch holds prefill work, and each group keeps at most
+    ``cap`` samples drawn at random.  Returns the kept indices, sorted."""
+    X = np.asarray(X, dtype=np.float64)
+    st = X[:, FEATURES.index("scheduled_tokens")]
+    has_pf = X[:, FEATURES.index("prefill_tokens")] > 0
+    group = np.floor(np.log2(np.maximum(st, 1.0))).astype(np.int64) * 2 + has_pf
+    rng = np.random.default_rng(seed)
+    keep = []
+    for g in np.unique(group):
+        idx = np.flatnonzero(group == g)
+        if len(idx) > cap:
+            idx = rng.choice(idx, cap, replace=False)
+        keep.append(idx)
+    return np.sort(np.concatenate(keep))
+
+
 def split_811(n: int, seed: int = 0):
     """Random 8:1:1 train / validation / test index split (Sec. 4.1)."""
     p = np.random.default_rng(seed).permutation(n)
@@ -113,7 +132,7 @@ class LatencyPredictor:
     weights: list = field(default=None, repr=False)  # [(W [out, in], b [out]), ...]
 
     def fit(self, X, y, X_val=None, y_val=None, epochs=300, lr=2e-3, weight_decay=1e-3,
-            batch_size=256, seed=0, verbose=False):
+            batch_size=256, seed=0, verbose=False, progress=None):
         """AdamW on the weighted asymmetric Huber loss (Eq. 5); keeps the
         epoch with the lowest validation loss (training loss if no split)."""
         import torch
@@ -162,6 +181,8 @@ class LatencyPredictor:
                 best_state = [p.detach().clone() for p in net.parameters()]
             if verbose and ep % 50 == 0:
                 print(f"epoch {ep}: loss {cur:.5f}")
+            if progress is not None and (ep + 1) % 25 == 0:
+                progress(ep + 1, cur)
         with torch.no_grad():
             for p, b in zip(net.parameters(), best_state):
                 p.copy_(b)

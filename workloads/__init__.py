@@ -17,3 +17,4 @@ from .configs import (  # noqa: F401
     tiny_batch,
 )
 from .tensors import make_caches, make_step_tensors, make_tensors  # noqa: F401
+from .serving import short_long_stream, uniform_stream  # noqa: F401
