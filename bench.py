@@ -577,10 +577,12 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
       2. the predictor: Table 7's MLP on the weighted asymmetric Huber loss,
          8:1:1 split, test accuracy as Table 8 (and a Table-2 linear fit);
       3. LPRS (Algorithm 1) against the token budget of 1,024 (Table 9's
-         comparison) at high and regular load, with and without APC, T* = the
-         token-budget run's mean step latency at high load;
+         comparison) at high and regular load, with APC, for B_max 1,024 and
+         2,048 and T* at the mean, 75th and 90th percentile of the token-budget
+         run's step latency at high load (and LPRS alone at the 90th);
       4. Aging against FCFS (Sec. 4.2) on a short-prompt-heavy stream;
-      5. APC off / on under LPRS on the 49:1 short/long mix (Table 10)."""
+      5. APC off / on under LPRS on the 49:1 short/long mix (Table 10), T* =
+         the token-budget run's mean step latency on that stream."""
     import numpy as np
     import torch
     import workloads as wl
@@ -643,24 +645,40 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
     log(f"[sched] predictor: {json.dumps(out['predictor']['test'])}")
 
     # 3. LPRS vs token budget
+    def vs_target(r, steps, t):
+        r = dict(r)
+        r["target_us"] = t
+        r["frac_over_target"] = float((steps > t).mean())
+        r["mean_abs_dev_from_target_us"] = float(np.abs(steps - t).mean())
+        return r
+
     cmp = {}
-    for name, iv in (("high", HIGH_US), ("regular", REGULAR_US)):
-        reqs = wl.uniform_stream(n_req, iv, seed=1000)
-        tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
-        if name == "high":
-            t_star = float(round(tb["step_us"]["mean"]))
-            out["target_us"] = t_star
-        tb_t = dict(strip(tb))
-        st = tb["_step_us"]
-        tb_t["frac_over_target"] = float((st > t_star).mean())
-        tb_t["mean_abs_dev_from_target_us"] = float(np.abs(st - t_star).mean())
-        row = {"token_budget_1024": tb_t}
-        for bmax, apc_on in ((1024, False), (1024, True), (2048, True)):
-            r = serve.serve(cfg(max_tokens=bmax, chunking=sched.CHUNK_LPRS, target_us=t_star,
-                                apc=apc_on), reqs, eng, predictor=model)
-            row[f"lprs_B{bmax}" + ("_apc" if apc_on else "")] = strip(r)
-        cmp[name] = row
-        log(f"[sched] LPRS vs token budget at {name} load done")
+    reqs = wl.uniform_stream(n_req, HIGH_US, seed=1000)
+    tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
+    st = tb["_step_us"]
+    targets = {"mean": float(np.mean(st)), "p75": float(np.percentile(st, 75)),
+               "p90": float(np.percentile(st, 90))}
+    out["targets_us"] = targets
+    row = {"token_budget_1024": vs_target(strip(tb), st, targets["p90"])}
+    r = serve.serve(cfg(max_tokens=1024, chunking=sched.CHUNK_LPRS, target_us=targets["p90"]),
+                    reqs, eng, predictor=model)
+    row["lprs_B1024_T_p90"] = strip(r)
+    for tname, t in targets.items():
+        for bmax in (1024, 2048):
+            r = serve.serve(cfg(max_tokens=bmax, chunking=sched.CHUNK_LPRS, target_us=t, apc=True),
+                            reqs, eng, predictor=model)
+            row[f"lprs_apc_B{bmax}_T_{tname}"] = strip(r)
+        log(f"[sched] LPRS at T*={tname} ({t:.1f} us) done")
+    cmp["high"] = row
+    reqs = wl.uniform_stream(n_req, REGULAR_US, seed=1001)
+    tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
+    row = {"token_budget_1024": vs_target(strip(tb), tb["_step_us"], targets["p90"])}
+    for bmax in (1024, 2048):
+        r = serve.serve(cfg(max_tokens=bmax, chunking=sched.CHUNK_LPRS, target_us=targets["p90"],
+                            apc=True), reqs, eng, predictor=model)
+        row[f"lprs_apc_B{bmax}_T_p90"] = strip(r)
+    cmp["regular"] = row
+    log("[sched] LPRS vs token budget at regular load done")
     out["lprs_vs_token_budget"] = cmp
 
     # 4. Aging vs FCFS (short-prompt-heavy stream, fine chunks)
@@ -676,12 +694,14 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
     out["aging_vs_fcfs"] = aging
     log("[sched] aging vs FCFS done")
 
-    # 5. APC ablation under LPRS (49:1 short/long mix)
-    reqs = wl.short_long_stream(n_req, seed=3000)
-    apc = {}
+    # 5. APC ablation under LPRS (49:1 short/long mix, busy and quiet phases)
+    reqs = wl.short_long_stream(n_req, busy_interval_us=20.0, quiet_interval_us=200.0, seed=3000)
+    tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
+    t_apc = float(np.mean(tb["_step_us"]))
+    apc = {"target_us": t_apc, "token_budget_1024": vs_target(strip(tb), tb["_step_us"], t_apc)}
     for on in (False, True):
         apc["on" if on else "off"] = strip(serve.serve(
-            cfg(max_tokens=1024, chunking=sched.CHUNK_LPRS, target_us=out["target_us"], apc=on),
+            cfg(max_tokens=1024, chunking=sched.CHUNK_LPRS, target_us=t_apc, apc=on),
             reqs, eng, predictor=model))
     out["apc_ablation"] = apc
     log("[sched] APC ablation done")

@@ -14,7 +14,9 @@
  *      CPS_POLICY_FCFS).  For each, h_i = min(r_i, B_max - U_t) (Eq. 6); the
  *      chunk is c = h_i under CPS_CHUNK_TOKEN_BUDGET (Eq. 7) or Algorithm 1's
  *      c* under CPS_CHUNK_LPRS; with APC on, Eq. 14 then accepts c*, replaces
- *      it by the warm-start chunk, or blocks it.  A request gets at most one
+ *      it by the warm-start chunk, or blocks it; once the round holds
+ *      |P_t| > 0 prefill chunks and |P_t| >= C_t, Eq. 14 returns 0 for every
+ *      later candidate, so the scan stops there.  A request gets at most one
  *      chunk per round; its remaining work drops by c (Eq. 2) and it goes back
  *      to the heap with its new key if prompt tokens remain;
  *   4. the batch comes back as cp_row_meta rows (decode rows first), ready
@@ -107,6 +109,9 @@ typedef struct {
   int64_t apc_blocked_min;   /* Eq. 14 "otherwise": c* < m_i and |P_t| > 0     */
   int64_t apc_warm_starts;   /* Eq. 14 second case taken with c != c*          */
   int64_t skipped_no_slot;   /* candidates passed over: every slot taken      */
+  int64_t apc_not_scored;    /* candidates left unscored: the round's active
+                                set was full (|P_t| > 0 and |P_t| >= C_t, so
+                                Eq. 14 gives 0 whatever c* is)                 */
   int64_t finished;          /* requests that emitted their last token        */
 } cps_stats;
 

@@ -20,7 +20,10 @@ Readings where the paper is silent (the same ones the product takes):
   * equal priorities go to the earlier arrival, then to the earlier
     registered request; a request without a slot is passed over while every
     slot is taken; new requests take the lowest free slot;
-  * Algorithm 1 scores that are NaN never win (both comparisons are false).
+  * Algorithm 1 scores that are NaN never win (both comparisons are false);
+  * with APC on, the scan of a round's queue stops once |P_t| >= C_t with
+    |P_t| > 0: Eq. 14 then gives 0 to every remaining candidate (C_t only
+    shrinks as the round fills), so they are not scored.
 """
 
 from __future__ import annotations
@@ -156,7 +159,7 @@ class Scheduler:
         self.free = set(range(cfg["max_seqs"]))
         self.last = None            # [(index, chunk_len)] of the batch awaiting completion
         self.counts = {"blocked_cap": 0, "blocked_min_chunk": 0, "warm_start": 0,
-                       "skipped_no_slot": 0}
+                       "skipped_no_slot": 0, "not_scored": 0}
 
     def add(self, rid, arrival, prompt_len, max_new):
         self.reqs.append({"id": rid, "arrival": arrival, "prompt": prompt_len,
@@ -189,9 +192,17 @@ class Scheduler:
             u += 1
         n_decode = len(rows)
         n_active = 0
-        for i in self._queue(t):
+        queue = self._queue(t)
+        for pos_in_queue, i in enumerate(queue):
             if u >= cfg["max_tokens"] or len(rows) >= cfg["max_seqs"]:
                 break
+            if cfg["apc"] and n_active > 0:
+                cap = min(cfg["max_active"], cfg["max_seqs"] - n_decode,
+                          (cfg["max_tokens"] - u) // cfg["min_chunk"])
+                if n_active >= cap:
+                    # Eq. 14 gives 0 to every remaining candidate
+                    self.counts["not_scored"] += len(queue) - pos_in_queue
+                    break
             r = self.reqs[i]
             if r["slot"] is None and not self.free:
                 self.counts["skipped_no_slot"] += 1

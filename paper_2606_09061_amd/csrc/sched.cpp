@@ -116,12 +116,16 @@ void candidates(int32_t h, int32_t delta, std::vector<int32_t>& c) {
   if (h > 1 && c.back() != h) c.push_back(h);
 }
 
+// C_t of Eq. 12.
+int64_t activity_cap(const cps_config& cfg, int32_t n_decode, int64_t committed) {
+  const int64_t by_budget = ((int64_t)cfg.max_tokens - committed) / cfg.min_chunk;
+  return std::min<int64_t>({(int64_t)cfg.max_active, (int64_t)cfg.max_seqs - n_decode, by_budget});
+}
+
 // Eq. 12–14.  Returns the chunk; *reason as documented in the header.
 int32_t apc_rule(const cps_config& cfg, int32_t c_star, int32_t h, int32_t remaining,
                  int32_t n_decode, int32_t n_active, int32_t committed, int32_t* reason) {
-  const int64_t by_budget = (int64_t)(cfg.max_tokens - committed) / cfg.min_chunk;
-  const int64_t cap = std::min<int64_t>({(int64_t)cfg.max_active,
-                                         (int64_t)cfg.max_seqs - n_decode, by_budget});
+  const int64_t cap = activity_cap(cfg, n_decode, committed);
   const int32_t m = std::min(remaining, cfg.min_chunk);  // Eq. 13
   if (n_active < cap && c_star >= m) {
     *reason = 0;
@@ -331,6 +335,10 @@ int cps_schedule(cps_sched* s, double now, cp_row_meta* rows, int64_t* ids, int3
   int32_t n_active = 0;
   std::vector<int32_t> popped;
   while (!s->heap.empty() && u < cfg.max_tokens && n < cap) {
+    if (cfg.apc && n_active > 0 && n_active >= activity_cap(cfg, n_decode, u)) {
+      s->stats.apc_not_scored += (int64_t)s->heap.size();
+      break;
+    }
     const int32_t idx = s->pop();
     popped.push_back(idx);
     Request& r = s->reqs[idx];

@@ -121,8 +121,8 @@ def bucket_weights(scheduled_tokens, n_buckets=N_BUCKETS) -> np.ndarray:
 @dataclass
 class LatencyPredictor:
     """MLP f_theta: features -> step latency (us).  Inputs are standardised
-    with the training set's mean and spread; the target is divided by the
-    training set's median latency."""
+    with the training set's mean and spread (constant features map to 0);
+    the target is divided by the training set's median latency."""
 
     hidden: tuple = (128, 64, 32)
     dropout: float = 0.1
@@ -141,7 +141,11 @@ class LatencyPredictor:
         y = np.asarray(y, dtype=np.float64)
         self.x_mean = X.mean(axis=0)
         sd = X.std(axis=0)
-        self.x_std = np.where(sd > 0, sd, 1.0)
+        # A feature constant over the training set (the bias; the memory
+        # state when it never changed) carries no information: its
+        # standardised input is pinned to 0 so that a later shift in it
+        # cannot move the prediction.
+        self.x_std = np.where(sd > 0, sd, np.inf)
         self.y_scale = float(np.median(y))
         st = X[:, FEATURES.index("scheduled_tokens")]
         w = bucket_weights(st)

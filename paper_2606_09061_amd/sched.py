@@ -57,7 +57,7 @@ class Stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in (
         "rounds", "decode_rows", "prefill_rows", "prefill_tokens", "lprs_calls",
         "predictor_rows", "apc_blocked_cap", "apc_blocked_min", "apc_warm_starts",
-        "skipped_no_slot", "finished")]
+        "skipped_no_slot", "apc_not_scored", "finished")]
 
 
 class RequestInfo(ctypes.Structure):

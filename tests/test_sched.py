@@ -211,6 +211,7 @@ def test_schedule_matches_reference(policy, chunking, apc_on, seed):
     assert st["apc_blocked_cap"] == o.counts["blocked_cap"]
     assert st["apc_blocked_min"] == o.counts["blocked_min_chunk"]
     assert st["apc_warm_starts"] == o.counts["warm_start"]
+    assert st["apc_not_scored"] == o.counts["not_scored"]
     if chunking == "lprs" and not apc_on:
         # LPRS alone fragments the budget into one-token chunks once the
         # target is reached (Sec. 3.3's motivation); APC removes them.
