@@ -26,41 +26,65 @@ struct Request {
   double first_token = -1.0, finish = -1.0;
 };
 
+// Rows of the MLP evaluated together: each weight row loaded from cache
+// feeds this many accumulators.
+constexpr int kRowBlock = 4;
+
+// One affine layer for kRowBlock rows: z[r][o] = b[o] + sum_i a[r][i] * wt[i][o].
+// Built for several x86-64 levels (ifunc-dispatched at load time) so that the
+// inner loop runs as 4- or 8-wide double FMAs where the CPU has them.
+__attribute__((target_clones("avx512f", "avx2,fma", "default"))) void affine_block(
+    const double* __restrict a, int lda, int din, const double* __restrict wt, int dout,
+    const double* __restrict bias, double* __restrict z, int ldz) {
+  for (int r = 0; r < kRowBlock; ++r)
+    for (int o = 0; o < dout; ++o) z[r * ldz + o] = bias[o];
+  for (int i = 0; i < din; ++i) {
+    const double* __restrict w = wt + (size_t)i * dout;
+    const double a0 = a[0 * lda + i], a1 = a[1 * lda + i], a2 = a[2 * lda + i],
+                 a3 = a[3 * lda + i];
+    for (int o = 0; o < dout; ++o) {
+      const double wo = w[o];
+      z[0 * ldz + o] += a0 * wo;
+      z[1 * ldz + o] += a1 * wo;
+      z[2 * ldz + o] += a2 * wo;
+      z[3 * ldz + o] += a3 * wo;
+    }
+  }
+}
+
 struct Mlp {
   std::vector<int32_t> dims;
   std::vector<double> wt, b, mean, inv_std;  // wt: per layer [din][dout] (transposed)
   double y_scale = 1.0;
   bool loaded() const { return !dims.empty(); }
 
-  // Forward pass over n rows of x[n][NF]; out[n].  Each layer accumulates
-  // input-by-input into all outputs (contiguous, vectorisable), skipping
-  // inputs that the previous ReLU zeroed.
+  // Forward pass over n rows of x[n][NF]; out[n].  Rows go through the
+  // layers kRowBlock at a time (a short last block is padded with zeros).
   void forward(const double* x, int n, double* out) const {
     const int L = (int)dims.size() - 1;
     int widest = 0;
     for (int d : dims) widest = std::max(widest, d);
-    std::vector<double> a((size_t)widest), z((size_t)widest);
-    for (int r = 0; r < n; ++r) {
-      for (int k = 0; k < NF; ++k) a[k] = (x[(size_t)r * NF + k] - mean[k]) * inv_std[k];
+    std::vector<double> a((size_t)kRowBlock * widest), z((size_t)kRowBlock * widest);
+    for (int r0 = 0; r0 < n; r0 += kRowBlock) {
+      const int nr = std::min(kRowBlock, n - r0);
+      for (int r = 0; r < kRowBlock; ++r)
+        for (int k = 0; k < NF; ++k)
+          a[(size_t)r * widest + k] =
+              r < nr ? (x[(size_t)(r0 + r) * NF + k] - mean[k]) * inv_std[k] : 0.0;
       size_t wo = 0, bo = 0;
       for (int l = 0; l < L; ++l) {
         const int din = dims[l], dout = dims[l + 1];
-        double* __restrict zz = z.data();
-        for (int o = 0; o < dout; ++o) zz[o] = b[bo + o];
-        for (int i = 0; i < din; ++i) {
-          const double ai = a[i];
-          if (ai == 0.0) continue;
-          const double* __restrict wr = &wt[wo + (size_t)i * dout];
-          for (int o = 0; o < dout; ++o) zz[o] += ai * wr[o];
-        }
-        if (l + 1 < L)
-          for (int o = 0; o < dout; ++o) a[o] = std::max(zz[o], 0.0);
-        else
-          for (int o = 0; o < dout; ++o) a[o] = zz[o];
+        affine_block(a.data(), widest, din, &wt[wo], dout, &b[bo], z.data(), widest);
+        const bool relu = l + 1 < L;
+        for (int r = 0; r < kRowBlock; ++r)
+          for (int o = 0; o < dout; ++o) {
+            const double v = z[(size_t)r * widest + o];
+            a[(size_t)r * widest + o] = relu ? std::max(v, 0.0) : v;
+          }
         wo += (size_t)din * dout;
         bo += dout;
       }
-      out[r] = a[0] * y_scale;
+      for (int r = 0; r < nr; ++r) out[r0 + r] = a[(size_t)r * widest] * y_scale;
     }
   }
 };
@@ -139,6 +163,98 @@ int32_t apc_rule(const cps_config& cfg, int32_t c_star, int32_t h, int32_t remai
   return 0;
 }
 
+// Scratch buffers of Algorithm 1, reused across calls, and the predictions
+// already made against the current committed rows: the features of a
+// candidate depend only on the committed rows, its processed tokens and c
+// (not on the request), so within a round, until another row is committed,
+// requests at the same prefill progress (every new arrival has 0) share them.
+struct SelectScratch {
+  std::vector<int32_t> cand, miss;
+  std::vector<double> feat, pred;
+  std::unordered_map<int64_t, double> seen;  // (processed << 32 | c) -> T_hat
+  // (processed << 32 | h) -> (c*, T_hat(c*)): the whole decision is shared too
+  std::unordered_map<int64_t, std::pair<int32_t, double>> decided;
+  Agg base;  // statistics of the committed rows
+  int64_t base_tokens = 0;
+  bool base_valid = false;
+  void forget() {
+    seen.clear();
+    decided.clear();
+    base_valid = false;
+  }
+};
+
+// Algorithm 1 over the rows committed so far (U_t = their tokens): the
+// candidate set of Eq. 8 scored by Eq. 10 on the predictions of Eq. 9, argmin
+// with ties to the larger chunk (Eq. 11), then the empty-batch guard.
+int32_t select_chunk(const cps_config& cfg, const Mlp& mlp, const double* mem,
+                     const cp_row_meta* committed, int32_t n, int32_t slot, int32_t processed,
+                     int32_t remaining, SelectScratch& sc, double* predicted,
+                     int64_t* rows_scored) {
+  if (!sc.base_valid) {
+    sc.base = Agg();
+    sc.base_tokens = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      sc.base.add(committed[i]);
+      sc.base_tokens += committed[i].chunk_len;
+    }
+    sc.base_valid = true;
+  }
+  const int64_t u = sc.base_tokens;
+  const int64_t h64 = std::min<int64_t>(remaining, (int64_t)cfg.max_tokens - u);  // Eq. 6
+  *predicted = std::numeric_limits<double>::quiet_NaN();
+  if (h64 <= 0) return 0;
+  const int32_t h = (int32_t)h64;
+  const int64_t dkey = ((int64_t)processed << 32) | h;
+  auto dit = sc.decided.find(dkey);
+  if (dit != sc.decided.end()) {
+    *predicted = dit->second.second;
+    return dit->second.first;
+  }
+  candidates(h, cfg.delta, sc.cand);
+  const int nc = (int)sc.cand.size();
+  const Agg& base = sc.base;
+  sc.feat.resize((size_t)nc * NF);
+  sc.pred.resize(nc);
+  sc.miss.clear();
+  for (int k = 0; k < nc; ++k) {
+    auto it = sc.seen.find(((int64_t)processed << 32) | sc.cand[k]);
+    if (it != sc.seen.end()) {
+      sc.pred[k] = it->second;
+      continue;
+    }
+    Agg g = base;
+    g.add({slot, processed, sc.cand[k], processed + sc.cand[k]});
+    g.emit(mem, &sc.feat[sc.miss.size() * NF]);
+    sc.miss.push_back(k);
+  }
+  if (!sc.miss.empty()) {
+    std::vector<double> t(sc.miss.size());
+    mlp.forward(sc.feat.data(), (int)sc.miss.size(), t.data());  // Eq. 9
+    for (size_t j = 0; j < sc.miss.size(); ++j) {
+      const int k = sc.miss[j];
+      sc.pred[k] = t[j];
+      sc.seen.emplace(((int64_t)processed << 32) | sc.cand[k], t[j]);
+    }
+    *rows_scored += (int64_t)sc.miss.size();
+  }
+  double best = std::numeric_limits<double>::infinity();
+  int32_t c_star = 0;
+  for (int k = 0; k < nc; ++k) {  // ascending c
+    const double t = sc.pred[k];
+    const double score = t <= cfg.target_us ? cfg.lambda_u * (cfg.target_us - t)
+                                            : cfg.lambda_o * (t - cfg.target_us);  // Eq. 10
+    if (score < best || (score == best && sc.cand[k] > c_star)) {  // Eq. 11
+      best = score;
+      c_star = sc.cand[k];
+      *predicted = t;
+    }
+  }
+  if (c_star == 0 && u == 0 && h >= 1) c_star = 1;  // starvation guard
+  sc.decided.emplace(dkey, std::make_pair(c_star, *predicted));
+  return c_star;
+}
+
 }  // namespace
 
 struct cps_sched {
@@ -160,9 +276,7 @@ struct cps_sched {
   std::vector<int32_t> batch_len;
   bool pending_batch = false;
   cps_stats stats{};
-  // Scratch of Algorithm 1.
-  std::vector<int32_t> cand;
-  std::vector<double> feat, pred;
+  SelectScratch scratch;
 
   static bool heap_less(const Entry& a, const Entry& b) {
     // max-heap on key; equal keys: earlier arrival, then lower index first
@@ -185,43 +299,11 @@ struct cps_sched {
     return idx;
   }
 
-  // Algorithm 1 over the rows committed so far.
   int32_t select(const cp_row_meta* committed, int32_t n, int32_t slot, int32_t processed,
                  int32_t remaining, double* predicted) {
-    int64_t u = 0;
-    for (int32_t i = 0; i < n; ++i) u += committed[i].chunk_len;
-    const int64_t h64 = std::min<int64_t>(remaining, (int64_t)cfg.max_tokens - u);  // Eq. 6
-    *predicted = std::numeric_limits<double>::quiet_NaN();
-    if (h64 <= 0) return 0;
-    const int32_t h = (int32_t)h64;
-    candidates(h, cfg.delta, cand);
-    const int nc = (int)cand.size();
-    Agg base;
-    for (int32_t i = 0; i < n; ++i) base.add(committed[i]);
-    feat.resize((size_t)nc * NF);
-    pred.resize(nc);
-    for (int k = 0; k < nc; ++k) {
-      Agg g = base;
-      g.add({slot, processed, cand[k], processed + cand[k]});
-      g.emit(mem, &feat[(size_t)k * NF]);
-    }
-    mlp.forward(feat.data(), nc, pred.data());  // Eq. 9
     stats.lprs_calls += 1;
-    stats.predictor_rows += nc;
-    double best = std::numeric_limits<double>::infinity();
-    int32_t c_star = 0;
-    for (int k = 0; k < nc; ++k) {  // ascending c
-      const double t = pred[k];
-      const double score = t <= cfg.target_us ? cfg.lambda_u * (cfg.target_us - t)
-                                              : cfg.lambda_o * (t - cfg.target_us);  // Eq. 10
-      if (score < best || (score == best && cand[k] > c_star)) {  // Eq. 11, ties to larger c
-        best = score;
-        c_star = cand[k];
-        *predicted = t;
-      }
-    }
-    if (c_star == 0 && u == 0 && h >= 1) return 1;  // starvation guard
-    return c_star;
+    return select_chunk(cfg, mlp, mem, committed, n, slot, processed, remaining, scratch,
+                        predicted, &stats.predictor_rows);
   }
 };
 
@@ -333,6 +415,7 @@ int cps_schedule(cps_sched* s, double now, cp_row_meta* rows, int64_t* ids, int3
   }
   const int32_t n_decode = n;
   int32_t n_active = 0;
+  s->scratch.forget();
   std::vector<int32_t> popped;
   while (!s->heap.empty() && u < cfg.max_tokens && n < cap) {
     if (cfg.apc && n_active > 0 && n_active >= activity_cap(cfg, n_decode, u)) {
@@ -368,6 +451,7 @@ int cps_schedule(cps_sched* s, double now, cp_row_meta* rows, int64_t* ids, int3
       s->free_slots.pop_back();
     }
     rows[n] = {r.slot, r.processed, c, r.processed + c};
+    s->scratch.forget();  // the committed rows changed
     ids[n] = r.id;
     s->batch_idx.push_back(idx);
     s->batch_len.push_back(c);
@@ -469,13 +553,11 @@ int cps_select_chunk(const cps_sched* s, const cp_row_meta* committed, int32_t n
       remaining < 0 || !chunk || !predicted)
     return CPS_ERR_INVALID_ARG;
   if (!s->mlp.loaded()) return CPS_ERR_NO_PREDICTOR;
-  // Algorithm 1 keeps scratch and counters in the scheduler; this entry point
-  // evaluates it on a copy so that the caller's scheduler is left unchanged.
-  cps_sched tmp;
-  tmp.cfg = s->cfg;
-  tmp.mlp = s->mlp;
-  std::memcpy(tmp.mem, s->mem, sizeof(tmp.mem));
-  *chunk = tmp.select(committed, n_committed, slot, processed, remaining, predicted);
+  // Own scratch and counter: the scheduler's state is left unchanged.
+  SelectScratch sc;
+  int64_t scored = 0;
+  *chunk = select_chunk(s->cfg, s->mlp, s->mem, committed, n_committed, slot, processed,
+                        remaining, sc, predicted, &scored);
   return CPS_OK;
 }
 
