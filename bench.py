@@ -564,54 +564,86 @@ def fit_latency(path):
 
 SCHED_BASE = dict(policy=0, max_tokens=1024, max_seqs=256, max_seq_len=4096, delta=32,
                   lambda_u=1.0, lambda_o=4.0, max_active=4, min_chunk=16)
-HIGH_US, REGULAR_US = 150.0, 1500.0  # request inter-arrival times (fixed interval)
+# Per engine: slots, request inter-arrival times (us) of the high / regular
+# load, the short-prompt (aging) stream and the busy / quiet phases of the
+# short/long (APC) stream, stream sizes, the T* quantiles swept, and the
+# aging ratios alpha/|beta| (tokens of remaining work per us of waiting; a
+# model round is ~100x longer than a step, so its ratios are ~100x smaller
+# for the same trade-off per round).
+SCHED_PROFILES = {
+    "step": dict(slots=256, high=150.0, regular=1500.0, aging=40.0, apc_busy=20.0,
+                 apc_quiet=200.0, n_req=1000, n_collect=600, n_collect_regular=600,
+                 regular_budgets=(256, 512, 1024, 2048), targets=("mean", "p75", "p90"),
+                 aging_budgets=(128, 512), aging_ratios=(0.01, 0.1), n_regular=1000,
+                 workload="qwen3-8b-attention-closed-loop"),
+    "model": dict(slots=128, high=15000.0, regular=150000.0, aging=4000.0, apc_busy=2000.0,
+                  apc_quiet=20000.0, n_req=500, n_collect=300, n_collect_regular=150,
+                  regular_budgets=(1024,), targets=("p75", "p90"), aging_budgets=(128, 512),
+                  aging_ratios=(1e-4, 1e-3),
+                  n_regular=160, workload="qwen3-8b-36-layer-closed-loop"),
+}
 
 
-def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
-    """Closed-loop serving of the Qwen3-8B / Llama-3-8B attention step (32/8
-    heads, head_dim 128, block 16, 256 slots of up to 4,096 tokens) under the
-    C++ scheduler, the clock advanced by each round's measured step latency:
+def sched_experiment(out_dir, engine="step", epochs=300, parts=("lprs", "aging", "apc")):
+    """Closed-loop serving under the C++ scheduler, the clock advanced by each
+    round's measured latency.  engine "step": the Qwen3-8B / Llama-3-8B
+    attention step alone (32/8 heads, head_dim 128, block 16, 256 slots of up
+    to 4,096 tokens); engine "model": the whole 36-layer synthetic Qwen3-8B
+    iteration (128 slots), the quantity the paper's predictor targets.
       1. samples: the token-budget scheduler on uniform and short/long request
          streams at several budgets and loads (the paper's offline profiling,
-         Sec. 3.2.1); each round gives the 16 features and the step latency;
+         Sec. 3.2.1); each round gives the 16 features and the latency;
       2. the predictor: Table 7's MLP on the weighted asymmetric Huber loss,
          8:1:1 split, test accuracy as Table 8 (and a Table-2 linear fit);
       3. LPRS (Algorithm 1) against the token budget of 1,024 (Table 9's
          comparison) at high and regular load, with APC, for B_max 1,024 and
-         2,048 and T* at the mean, 75th and 90th percentile of the token-budget
-         run's step latency at high load (and LPRS alone at the 90th);
+         2,048 and T* at quantiles of the token-budget run's round latency at
+         high load (and LPRS alone at the 90th percentile);
       4. Aging against FCFS (Sec. 4.2) on a short-prompt-heavy stream;
       5. APC off / on under LPRS on the 49:1 short/long mix (Table 10), T* =
-         the token-budget run's mean step latency on that stream."""
+         the token-budget run's mean round latency on that stream."""
     import numpy as np
     import torch
     import workloads as wl
     from paper_2606_09061_amd import lprs, sched, serve
 
+    P = SCHED_PROFILES[engine]
+    n_req, n_collect = P["n_req"], P["n_collect"]
+    HIGH, REGULAR = P["high"], P["regular"]
     os.makedirs(out_dir, exist_ok=True)
     torch.cuda.set_device(0)
-    eng = serve.StepEngine(max_seqs=256, max_seq_len=4096, max_tokens=2048)
+    if engine == "model":
+        from paper_2606_09061_amd import model as M
+        eng = M.ModelEngine(M.Model(M.QWEN3_8B, max_seqs=P["slots"], max_seq_len=4096,
+                                    max_tokens=2048))
+    else:
+        eng = serve.StepEngine(max_seqs=P["slots"], max_seq_len=4096, max_tokens=2048)
 
     def cfg(**kw):
         d = dict(SCHED_BASE)
+        d["max_seqs"] = P["slots"]
         d.update(kw)
         return sched.make_config(**d)
 
     def strip(r):
         return {k: v for k, v in r.items() if not k.startswith("_")}
 
-    out = {"workload": "qwen3-8b-attention-closed-loop", "shape": "32/8 heads, d128, B16",
-           "high_interval_us": HIGH_US, "regular_interval_us": REGULAR_US}
-    serve.serve(cfg(), wl.uniform_stream(60, HIGH_US, seed=99), eng)  # warm-up
+    out = {"workload": P["workload"], "shape": "32/8 heads, d128, B16", "engine": engine,
+           "slots": P["slots"], "high_interval_us": HIGH, "regular_interval_us": REGULAR}
+    serve.serve(cfg(), wl.uniform_stream(30, HIGH, seed=99), eng)  # warm-up
     log("[sched] warm-up done")
 
+    need_model = "lprs" in parts or "apc" in parts
     # 1. samples
     X, Y, runs = [], [], []
-    plan = [(b, iv, "uniform") for b in (256, 512, 1024, 2048) for iv in (HIGH_US, REGULAR_US)]
+    plan = [(b, HIGH, "uniform") for b in (256, 512, 1024, 2048)]
+    plan += [(b, REGULAR, "uniform") for b in P["regular_budgets"]]
     plan += [(256, None, "short_long"), (1024, None, "short_long")]
-    for i, (bmax, iv, kind) in enumerate(plan):
-        reqs = (wl.uniform_stream(n_collect, iv, seed=10 + i) if kind == "uniform"
-                else wl.short_long_stream(n_collect, seed=10 + i))
+    for i, (bmax, iv, kind) in enumerate(plan if need_model else []):
+        reqs = (wl.uniform_stream(n_collect if iv == HIGH else P["n_collect_regular"], iv,
+                                  seed=10 + i) if kind == "uniform"
+                else wl.short_long_stream(n_collect, busy_interval_us=5 * P["apc_busy"],
+                                          quiet_interval_us=5 * P["apc_quiet"], seed=10 + i))
         t0 = time.time()
         r = serve.serve(cfg(max_tokens=bmax), reqs, eng, record=True)
         X.append(r["_features"])
@@ -619,6 +651,31 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
         runs.append({"max_tokens": bmax, "interval_us": iv, "stream": kind, "rounds": r["rounds"]})
         log(f"[sched] samples {i + 1}/{len(plan)}: B={bmax} {kind} {iv}: {r['rounds']} rounds, "
             f"{time.time() - t0:.1f}s")
+    if need_model:
+        model = _train_predictor(out, out_dir, X, Y, runs, epochs)
+    if "lprs" in parts:
+        _lprs_runs(out, P, cfg, strip, eng, model)
+    if "aging" in parts:
+        _aging_runs(out, P, cfg, strip, eng)
+    if "apc" in parts:
+        _apc_runs(out, P, cfg, strip, eng, model)
+    with open(os.path.join(out_dir, "sched_results.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
+    return out
+
+
+def _vs_target(r, steps, t):
+    import numpy as np
+    r = dict(r)
+    r["target_us"] = t
+    r["frac_over_target"] = float((steps > t).mean())
+    r["mean_abs_dev_from_target_us"] = float(np.abs(steps - t).mean())
+    return r
+
+
+def _train_predictor(out, out_dir, X, Y, runs, epochs):
+    import numpy as np
+    from paper_2606_09061_amd import lprs, sched
     X = np.concatenate(X)
     Y = np.concatenate(Y)
     np.savetxt(os.path.join(out_dir, "samples.csv"), np.column_stack([X, Y]), delimiter=",",
@@ -643,21 +700,22 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
     w, *_ = np.linalg.lstsq(X[tr][:, lin] / sc, Y[tr], rcond=None)
     out["predictor"]["table2_linear_test"] = lprs.accuracy(Y[te], (X[te][:, lin] / sc) @ w)
     log(f"[sched] predictor: {json.dumps(out['predictor']['test'])}")
+    return model
 
-    # 3. LPRS vs token budget
-    def vs_target(r, steps, t):
-        r = dict(r)
-        r["target_us"] = t
-        r["frac_over_target"] = float((steps > t).mean())
-        r["mean_abs_dev_from_target_us"] = float(np.abs(steps - t).mean())
-        return r
 
+def _lprs_runs(out, P, cfg, strip, eng, model):
+    import numpy as np
+    import workloads as wl
+    from paper_2606_09061_amd import sched, serve
+    n_req, HIGH, REGULAR = P["n_req"], P["high"], P["regular"]
+    vs_target = _vs_target
     cmp = {}
-    reqs = wl.uniform_stream(n_req, HIGH_US, seed=1000)
+    reqs = wl.uniform_stream(n_req, HIGH, seed=1000)
     tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
     st = tb["_step_us"]
-    targets = {"mean": float(np.mean(st)), "p75": float(np.percentile(st, 75)),
-               "p90": float(np.percentile(st, 90))}
+    all_targets = {"mean": float(np.mean(st)), "p75": float(np.percentile(st, 75)),
+                   "p90": float(np.percentile(st, 90))}
+    targets = {k: all_targets[k] for k in P["targets"]}
     out["targets_us"] = targets
     row = {"token_budget_1024": vs_target(strip(tb), st, targets["p90"])}
     r = serve.serve(cfg(max_tokens=1024, chunking=sched.CHUNK_LPRS, target_us=targets["p90"]),
@@ -670,7 +728,7 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
             row[f"lprs_apc_B{bmax}_T_{tname}"] = strip(r)
         log(f"[sched] LPRS at T*={tname} ({t:.1f} us) done")
     cmp["high"] = row
-    reqs = wl.uniform_stream(n_req, REGULAR_US, seed=1001)
+    reqs = wl.uniform_stream(P["n_regular"], REGULAR, seed=1001)
     tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
     row = {"token_budget_1024": vs_target(strip(tb), tb["_step_us"], targets["p90"])}
     for bmax in (1024, 2048):
@@ -681,21 +739,32 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
     log("[sched] LPRS vs token budget at regular load done")
     out["lprs_vs_token_budget"] = cmp
 
-    # 4. Aging vs FCFS (short-prompt-heavy stream, fine chunks)
+
+def _aging_runs(out, P, cfg, strip, eng):
+    import workloads as wl
+    from paper_2606_09061_amd import sched, serve
+    n_req = P["n_req"]
     aging = {}
-    reqs = wl.uniform_stream(n_req, 40.0, seed=2000, max_seq_len=1024, prompt_median=19,
+    reqs = wl.uniform_stream(n_req, P["aging"], seed=2000, max_seq_len=1024, prompt_median=19,
                              output_median=64, sigma=1.75)
-    for bmax in (128, 512):
+    for bmax in P["aging_budgets"]:
         row = {"fcfs": strip(serve.serve(cfg(max_tokens=bmax, policy=sched.POLICY_FCFS), reqs, eng))}
-        for ratio in (0.01, 0.1):
+        for ratio in P["aging_ratios"]:
             row[f"aging_alpha_over_beta_{ratio}"] = strip(serve.serve(
                 cfg(max_tokens=bmax, policy=sched.POLICY_AGING, alpha=ratio, beta=-1.0), reqs, eng))
         aging[f"B{bmax}"] = row
     out["aging_vs_fcfs"] = aging
     log("[sched] aging vs FCFS done")
 
-    # 5. APC ablation under LPRS (49:1 short/long mix, busy and quiet phases)
-    reqs = wl.short_long_stream(n_req, busy_interval_us=20.0, quiet_interval_us=200.0, seed=3000)
+
+def _apc_runs(out, P, cfg, strip, eng, model):
+    import numpy as np
+    import workloads as wl
+    from paper_2606_09061_amd import sched, serve
+    n_req = P["n_req"]
+    vs_target = _vs_target
+    reqs = wl.short_long_stream(n_req, busy_interval_us=P["apc_busy"],
+                                quiet_interval_us=P["apc_quiet"], seed=3000)
     tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
     t_apc = float(np.mean(tb["_step_us"]))
     apc = {"target_us": t_apc, "token_budget_1024": vs_target(strip(tb), tb["_step_us"], t_apc)}
@@ -705,8 +774,63 @@ def sched_experiment(out_dir, n_req=1000, n_collect=600, epochs=300):
             reqs, eng, predictor=model))
     out["apc_ablation"] = apc
     log("[sched] APC ablation done")
-    with open(os.path.join(out_dir, "sched_results.json"), "w") as fh:
-        json.dump(out, fh, indent=1)
+
+
+def model_bench(reps=5, max_seqs=128, only=None):
+    """Whole-iteration latency of the synthetic Qwen3-8B stack (36 layers,
+    hidden 4096, 32/8 heads, d 128, FFN 12288, vocab 151936) on typical
+    batches, with the per-iteration host time of issuing it."""
+    import math
+    import numpy as np
+    import torch
+    from paper_2606_09061_amd import model as M
+
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    m = M.Model(M.QWEN3_8B, max_seqs=max_seqs, max_seq_len=4096, max_tokens=2048, fill_caches=True)
+    torch.cuda.synchronize()
+    log(f"[model] built in {time.time() - t0:.1f}s, "
+        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated")
+    rng = np.random.default_rng(0)
+    ctx = np.clip(np.round(rng.lognormal(math.log(1024), 1.0, max_seqs)), 16, 4000).astype(int)
+    dec = [(i, int(c) - 1, 1, int(c)) for i, c in enumerate(ctx)]
+    cases = {
+        "decode_128_ctx_med1024": dec,
+        "decode_32_ctx_med1024": dec[:32],
+        "prefill_1x1024_at_0": [(0, 0, 1024, 1024)],
+        "prefill_1x1024_at_2048": [(0, 2048, 1024, 3072)],
+        "prefill_2x1024_at_0": [(0, 0, 1024, 1024), (1, 0, 1024, 1024)],
+        "mixed_64dec_plus_960_at_2048": dec[:64] + [(100, 2048, 960, 3008)],
+        "mixed_127dec_plus_896_at_0": dec[1:] + [(0, 0, 896, 896)],
+    }
+    eng = M.ModelEngine(m)
+    out = {"model": "qwen3-8b-synthetic", "layers": m.cfg.layers, "cases": {}}
+    n_params = sum(t.numel() for L in m.layers for t in L.values()) + m.lm_head.numel()
+    for name, rows in cases.items():
+        if only and name not in only:
+            continue
+        rows = np.array(rows, np.int32)
+        T = int(rows[:, 2].sum())
+        for _ in range(2):
+            eng.step(rows)
+        gpu, host = [], []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            h0 = time.perf_counter()
+            eng.ev[0].record(eng.stream)
+            m.forward(rows, eng.stream)
+            eng.ev[1].record(eng.stream)
+            h1 = time.perf_counter()
+            eng.ev[1].synchronize()
+            gpu.append(eng.ev[0].elapsed_time(eng.ev[1]))
+            host.append((h1 - h0) * 1e3)
+        ms = float(np.median(gpu))
+        flops = 2.0 * n_params * T  # weight GEMMs only (attention excluded)
+        out["cases"][name] = {"tokens": T, "rows": int(len(rows)), "gpu_ms": ms,
+                              "host_issue_ms": float(np.median(host)),
+                              "tokens_per_s": T / ms * 1e3,
+                              "gemm_tflops": flops / (ms * 1e-3) / 1e12}
+        log(f"[model] {name}: {ms:.2f} ms GPU, {np.median(host):.2f} ms host, T={T}")
     return out
 
 
@@ -731,6 +855,14 @@ def main():
                     help="only run the latency-vs-composition sweep, written to CSV")
     ap.add_argument("--sched", default=None, metavar="DIR",
                     help="only run the closed-loop scheduling experiment, results under DIR")
+    ap.add_argument("--sched-engine", choices=["step", "model"], default="step",
+                    help="with --sched: the attention step alone or the whole 36-layer model")
+    ap.add_argument("--sched-parts", default="lprs,aging,apc",
+                    help="with --sched: comma-separated subset of lprs, aging, apc")
+    ap.add_argument("--model", action="store_true",
+                    help="only time whole iterations of the synthetic Qwen3-8B stack")
+    ap.add_argument("--model-case", action="append", default=None,
+                    help="with --model: time only this batch (repeatable)")
     ap.add_argument("--fit", default=None, metavar="CSV",
                     help="only fit a latency table written earlier (no GPU)")
     args = ap.parse_args()
@@ -747,7 +879,11 @@ def main():
         print(json.dumps(fit_latency(args.fit)), flush=True)
         return
     if args.sched:
-        print(json.dumps(sched_experiment(args.sched)), flush=True)
+        print(json.dumps(sched_experiment(args.sched, engine=args.sched_engine,
+                                          parts=tuple(args.sched_parts.split(",")))), flush=True)
+        return
+    if args.model:
+        print(json.dumps(model_bench(only=args.model_case)), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the attention step is "

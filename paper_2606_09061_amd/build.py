@@ -1,5 +1,6 @@
-"""Builds, in-tree, libcpattn.so (HIP kernels + C ABI, gfx950, hipcc) and
-libcpsched.so (the host scheduler, plain C++17, g++)."""
+"""Builds, in-tree, libcpattn.so (the attention step: HIP kernels + C ABI,
+gfx950, hipcc), libcplayer.so (the element-wise kernels of the decoder layer
+around it, gfx950) and libcpsched.so (the host scheduler, plain C++17, g++)."""
 
 from __future__ import annotations
 
@@ -14,6 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcpattn.so")
 SCHED_LIB = os.path.join(PKG, "libcpsched.so")
+LAYER_LIB = os.path.join(PKG, "libcplayer.so")
+LAYER_SOURCES = ["layer.hip"]
 CXX = os.environ.get("CXX", "g++")
 SOURCES = ["api.hip", "plan.cpp", "append.hip", "decode.hip", "prefill.hip", "merge.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -40,15 +43,20 @@ def _compile(src: str) -> str:
 def build(jobs: int = 8) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(_compile, SOURCES + LAYER_SOURCES))
+    _link(objs[:len(SOURCES)], LIB)
+    _link(objs[len(SOURCES):], LAYER_LIB)
+    build_sched()
+    return LIB
+
+
+def _link(objs, out):
+    tmp = out + ".tmp"
     r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp],
                        capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
-    build_sched()
-    return LIB
+        raise RuntimeError(f"link of {os.path.basename(out)} failed:\n{r.stderr}")
+    os.replace(tmp, out)
 
 
 def build_sched() -> str:

@@ -1,0 +1,188 @@
+// Element-wise kernels around the attention step of one decoder layer
+// (include/cp_layer.h): RMSNorm, the QKV split with per-head RMSNorm and
+// rotary embedding, and SwiGLU.  All three are bound by HBM traffic: each
+// reads its input once and writes its output once with 16-byte (or, for the
+// per-head kernel, 128-byte-per-wave) coalesced accesses.
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "cp_layer.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float a) {
+  return __builtin_bit_cast(uint16_t, (__bf16)a);  // nearest even
+}
+
+__device__ __forceinline__ float lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ uint32_t pack(float a, float b) {
+  return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
+  return x;
+}
+
+__device__ __forceinline__ float sumsq8(const uint4& a) {
+  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) s += lo(w[i]) * lo(w[i]) + hi(w[i]) * hi(w[i]);
+  return s;
+}
+
+// One block per row.  x and out may alias: every element is read and then
+// written by the same thread, after the block-wide reduction barrier.
+__global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const uint4* x, const uint4* w,
+                                                           uint4* out, int width8,
+                                                           float inv_width, float eps) {
+  const size_t row = blockIdx.x;
+  const uint4* xr = x + row * width8;
+  uint4* orow = out + row * width8;
+  float ss = 0.f;
+  for (int v = threadIdx.x; v < width8; v += kThreads) ss += sumsq8(xr[v]);
+  ss = wave_sum(ss);
+  __shared__ float part[kThreads / 64];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float total = 0.f;
+#pragma unroll
+  for (int i = 0; i < kThreads / 64; ++i) total += part[i];
+  const float scale = 1.0f / sqrtf(total * inv_width + eps);
+  for (int v = threadIdx.x; v < width8; v += kThreads) {
+    const uint4 a = xr[v], g = w[v];
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, gw[4] = {g.x, g.y, g.z, g.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      o[i] = pack(lo(aw[i]) * scale * lo(gw[i]), hi(aw[i]) * scale * hi(gw[i]));
+    orow[v] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// One wave per (token, head) of the fused projection; lane l < D/2 owns the
+// rotation pair (l, l + D/2).  Heads [0, hq) are queries, [hq, hq + hkv) keys,
+// the rest values.
+__global__ __launch_bounds__(kThreads) void qkv_rope_kernel(
+    const uint16_t* __restrict qkv, const uint16_t* __restrict qw, const uint16_t* __restrict kw,
+    const int32_t* __restrict positions, int n_tokens, int hq, int hkv, int D, double log2_theta,
+    float eps, uint16_t* __restrict q, uint16_t* __restrict k, uint16_t* __restrict v) {
+  const int nh = hq + 2 * hkv;
+  const int64_t g = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (g >= (int64_t)n_tokens * nh) return;  // whole wave
+  const int t = (int)(g / nh), hh = (int)(g % nh), lane = threadIdx.x & 63, half = D >> 1;
+  const bool on = lane < half;
+  const uint16_t* in = qkv + ((size_t)t * nh + hh) * D;
+  const float e0 = on ? bf16_to_f32(in[lane]) : 0.f;
+  const float e1 = on ? bf16_to_f32(in[lane + half]) : 0.f;
+  if (hh >= hq + hkv) {
+    if (on) {
+      uint16_t* o = v + ((size_t)t * hkv + (hh - hq - hkv)) * D;
+      o[lane] = in[lane];
+      o[lane + half] = in[lane + half];
+    }
+    return;
+  }
+  const bool is_q = hh < hq;
+  const float ss = wave_sum(e0 * e0 + e1 * e1);
+  const float scale = 1.0f / sqrtf(ss / (float)D + eps);
+  if (!on) return;
+  const uint16_t* wn = is_q ? qw : kw;
+  const float y0 = e0 * scale * bf16_to_f32(wn[lane]);
+  const float y1 = e1 * scale * bf16_to_f32(wn[lane + half]);
+  // angle = pos * theta^(-2 lane / D), formed and reduced to [-pi, pi] in
+  // double (long positions keep their fraction), then sine and cosine in fp32
+  const double inv_freq = exp2(-(2.0 * lane / D) * log2_theta);
+  const double angle = (double)positions[t] * inv_freq;
+  const double two_pi = 6.283185307179586476925286766559;
+  const float r = (float)(angle - two_pi * rint(angle * (1.0 / two_pi)));
+  float sf, cf;
+  sincosf(r, &sf, &cf);
+  uint16_t* o = is_q ? q + ((size_t)t * hq + hh) * D : k + ((size_t)t * hkv + (hh - hq)) * D;
+  o[lane] = f32_to_bf16(y0 * cf - y1 * sf);
+  o[lane + half] = f32_to_bf16(y1 * cf + y0 * sf);
+}
+
+__global__ __launch_bounds__(kThreads) void swiglu_kernel(const uint4* __restrict gu,
+                                                          uint4* __restrict out, int inter8,
+                                                          int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n) return;
+  const int64_t t = i / inter8, c = i % inter8;
+  const uint4 g = gu[t * 2 * inter8 + c], u = gu[t * 2 * inter8 + inter8 + c];
+  const uint32_t gw[4] = {g.x, g.y, g.z, g.w}, uw[4] = {u.x, u.y, u.z, u.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float g0 = lo(gw[j]), g1 = hi(gw[j]);
+    o[j] = pack(g0 / (1.0f + __expf(-g0)) * lo(uw[j]), g1 / (1.0f + __expf(-g1)) * hi(uw[j]));
+  }
+  out[i] = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+int launched() { return hipGetLastError() == hipSuccess ? CP_OK : CP_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int cpl_rmsnorm(const void* x, const void* w, void* out, int32_t n_rows, int32_t width,
+                float eps, void* stream) {
+  if (n_rows < 0 || width < 8 || width > 32768 || width % 8 != 0 || !(eps > 0.f))
+    return CP_ERR_INVALID_ARG;
+  if (n_rows == 0) return CP_OK;
+  if (!x || !w || !out || !aligned16(x) || !aligned16(w) || !aligned16(out))
+    return CP_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(n_rows), dim3(kThreads), 0, (hipStream_t)stream,
+                     (const uint4*)x, (const uint4*)w, (uint4*)out, width / 8, 1.0f / width, eps);
+  return launched();
+}
+
+int cpl_qkv_rope(const void* qkv, const void* q_norm_w, const void* k_norm_w,
+                 const int32_t* positions, int32_t n_tokens, int32_t hq, int32_t hkv,
+                 int32_t head_dim, double theta, float eps, void* q, void* k, void* v,
+                 void* stream) {
+  if (head_dim != 64 && head_dim != 128) return CP_ERR_UNSUPPORTED;
+  if (n_tokens < 0 || hq < 1 || hkv < 1 || hq > 1024 || hkv > 1024 || !(theta > 1.0) ||
+      !(eps > 0.f))
+    return CP_ERR_INVALID_ARG;
+  if (n_tokens == 0) return CP_OK;
+  if (!qkv || !q_norm_w || !k_norm_w || !positions || !q || !k || !v) return CP_ERR_INVALID_ARG;
+  const int64_t waves = (int64_t)n_tokens * (hq + 2 * hkv);
+  const int64_t blocks = (waves + kThreads / 64 - 1) / (kThreads / 64);
+  if (blocks > 0x7fffffff) return CP_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)blocks), dim3(kThreads), 0,
+                     (hipStream_t)stream, (const uint16_t*)qkv, (const uint16_t*)q_norm_w,
+                     (const uint16_t*)k_norm_w, positions, n_tokens, hq, hkv, head_dim,
+                     log2(theta), eps, (uint16_t*)q, (uint16_t*)k, (uint16_t*)v);
+  return launched();
+}
+
+int cpl_swiglu(const void* gu, void* out, int32_t n_tokens, int32_t inter, void* stream) {
+  if (n_tokens < 0 || inter < 8 || inter % 8 != 0) return CP_ERR_INVALID_ARG;
+  if (n_tokens == 0) return CP_OK;
+  if (!gu || !out || !aligned16(gu) || !aligned16(out)) return CP_ERR_INVALID_ARG;
+  const int64_t n = (int64_t)n_tokens * (inter / 8);
+  const int64_t blocks = (n + kThreads - 1) / kThreads;
+  if (blocks > 0x7fffffff) return CP_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)blocks), dim3(kThreads), 0,
+                     (hipStream_t)stream, (const uint4*)gu, (uint4*)out, inter / 8, n);
+  return launched();
+}
+
+}  // extern "C"

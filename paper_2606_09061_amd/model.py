@@ -1,0 +1,256 @@
+"""A Qwen3-style decoder stack around the attention step, on one GPU.
+
+The paper's predictor and target latency T* refer to a whole model iteration
+(Sec. 3.2.1; Sec. 4.4 uses Qwen3-8B with T* = 105 ms), so this module runs the
+scheduler's batch through every layer of such a model with synthetic weights:
+
+    embedding -> L x [RMSNorm -> QKV GEMM -> cpl_qkv_rope -> cp_kv_append ->
+    cp_attn_mixed -> O GEMM (+ residual) -> RMSNorm -> gate/up GEMM ->
+    cpl_swiglu -> down GEMM (+ residual)] -> RMSNorm -> LM head on each row's
+    last token -> argmax
+
+The GEMMs are plain library GEMMs (torch.mm / addmm, i.e. hipBLASLt); every
+other step runs in this package's HIP kernels (libcplayer.so for the
+element-wise parts, libcpattn.so for append and attention).  Each layer has
+its own paged KV pool; all layers share one block table, whose row s maps
+slot s's logical blocks to physical blocks (a random permutation, so pages
+are scattered).  Weights are N(0, 0.02) in bf16, norms 1.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import binding as cp
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcplayer.so")
+
+_lib = None
+
+
+def load():
+    """Loads libcplayer.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it first "
+                           "(python -m paper_2606_09061_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, F, D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_double
+    lib.cpl_rmsnorm.argtypes = [P, P, P, I32, I32, F, P]
+    lib.cpl_qkv_rope.argtypes = [P, P, P, P, I32, I32, I32, I32, D, F, P, P, P, P]
+    lib.cpl_swiglu.argtypes = [P, P, I32, I32, P]
+    for f in (lib.cpl_rmsnorm, lib.cpl_qkv_rope, lib.cpl_swiglu):
+        f.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def exported_symbols():
+    return ["cpl_rmsnorm", "cpl_qkv_rope", "cpl_swiglu"]
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise cp.CpError(rc, what)
+
+
+def _s(stream):
+    return cp._stream(stream)
+
+
+def _dense(*ts):
+    for t in ts:
+        if not t.is_contiguous():
+            raise cp.CpError(cp.CP_ERR_INVALID_ARG, "layer kernels take dense tensors")
+
+
+def rmsnorm(x, w, out, eps, stream=None):
+    """out = RMSNorm(x) * w over the last axis (bf16 tensors; out may be x)."""
+    _dense(x, w, out)
+    n, width = x.shape[0], x.shape[-1]
+    _check(load().cpl_rmsnorm(x.data_ptr(), w.data_ptr(), out.data_ptr(), n, width, eps,
+                              _s(stream)), "cpl_rmsnorm")
+
+
+def qkv_rope(qkv, q_norm_w, k_norm_w, positions, hq, hkv, head_dim, theta, eps, q, k, v,
+             stream=None):
+    """Splits qkv [T, (hq+2hkv)*D] into q [T, hq, D], k, v [T, hkv, D] with
+    per-head RMSNorm and rotary embedding of q and k (positions: int32 [T])."""
+    _dense(qkv, q_norm_w, k_norm_w, positions, q, k, v)
+    _check(load().cpl_qkv_rope(qkv.data_ptr(), q_norm_w.data_ptr(), k_norm_w.data_ptr(),
+                               positions.data_ptr(), qkv.shape[0], hq, hkv, head_dim,
+                               float(theta), eps, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                               _s(stream)), "cpl_qkv_rope")
+
+
+def swiglu(gu, out, stream=None):
+    """out [T, I] = silu(gu[:, :I]) * gu[:, I:]."""
+    _dense(gu, out)
+    _check(load().cpl_swiglu(gu.data_ptr(), out.data_ptr(), gu.shape[0], out.shape[-1],
+                             _s(stream)), "cpl_swiglu")
+
+
+@dataclass
+class ModelConfig:
+    hidden: int = 4096
+    layers: int = 36
+    hq: int = 32
+    hkv: int = 8
+    head_dim: int = 128
+    inter: int = 12288
+    vocab: int = 151936
+    eps: float = 1e-6
+    theta: float = 1e6
+    block_size: int = 16
+
+
+QWEN3_8B = ModelConfig()
+
+
+def positions_of(rows) -> np.ndarray:
+    """Absolute position of every scheduled token, in row order."""
+    rows = np.asarray(rows).reshape(-1, 4)
+    lens = rows[:, 2].astype(np.int64)
+    if lens.sum() == 0:
+        return np.zeros(0, np.int32)
+    base = np.repeat(rows[:, 1].astype(np.int64) - np.concatenate([[0], np.cumsum(lens)[:-1]]),
+                     lens)
+    return (base + np.arange(lens.sum())).astype(np.int32)
+
+
+class Model:
+    """Synthetic-weight decoder stack with per-layer paged KV pools."""
+
+    def __init__(self, cfg: ModelConfig = QWEN3_8B, max_seqs=128, max_seq_len=4096,
+                 max_tokens=2048, seed=0, device=None, lm_head=True, fill_caches=False):
+        import torch
+        from workloads.tensors import _randn_bf16
+
+        self.cfg = c = cfg
+        self.dev = device or torch.device("cuda", 0)
+        self.max_tokens = max_tokens
+        gen = torch.Generator(device=self.dev)
+        gen.manual_seed(seed)
+
+        def w(*shape):
+            t = _randn_bf16(shape, gen, self.dev)
+            return t.mul_(0.02)
+
+        def ones(n):
+            return torch.ones(n, dtype=torch.bfloat16, device=self.dev)
+
+        H, D = c.hidden, c.head_dim
+        nqkv = (c.hq + 2 * c.hkv) * D
+        self.layers = [dict(in_norm=ones(H), qkv=w(nqkv, H), q_norm=ones(D), k_norm=ones(D),
+                            o=w(H, c.hq * D), post_norm=ones(H), gate_up=w(2 * c.inter, H),
+                            down=w(H, c.inter)) for _ in range(c.layers)]
+        self.embed = w(c.vocab, H)
+        self.final_norm = ones(H)
+        self.lm_head = w(c.vocab, H) if lm_head else None
+        mbr = -(-max_seq_len // c.block_size)
+        nb = max_seqs * mbr
+        rng = np.random.default_rng(seed)
+        self.bt = torch.from_numpy(rng.permutation(nb).astype(np.int32).reshape(max_seqs, mbr)
+                                   ).to(self.dev)
+        # Serving writes every position before attention reads it, so pools may
+        # start unwritten; fill_caches draws N(0,1) contents for benchmarks
+        # that attend to context they never appended.
+        if fill_caches:
+            self.kc = [_randn_bf16((nb, c.hkv, c.block_size, D), gen, self.dev)
+                       for _ in range(c.layers)]
+            self.vc = [_randn_bf16((nb, c.hkv, D, c.block_size), gen, self.dev)
+                       for _ in range(c.layers)]
+        else:
+            self.kc = [torch.empty(nb, c.hkv, c.block_size, D, dtype=torch.bfloat16,
+                                   device=self.dev) for _ in range(c.layers)]
+            self.vc = [torch.empty(nb, c.hkv, D, c.block_size, dtype=torch.bfloat16,
+                                   device=self.dev) for _ in range(c.layers)]
+        self.desc = cp.make_desc(c.hq, c.hkv, D, c.block_size, nb, mbr, max_seqs,
+                                 1.0 / math.sqrt(D))
+        T = max_tokens
+
+        def buf(*shape):
+            return torch.empty(*shape, dtype=torch.bfloat16, device=self.dev)
+
+        self.x, self.h = buf(T, H), buf(T, H)
+        self.qkv = buf(T, nqkv)
+        self.q, self.k, self.v = buf(T, c.hq, D), buf(T, c.hkv, D), buf(T, c.hkv, D)
+        self.attn = buf(T, c.hq, D)
+        self.gu, self.act = buf(T, 2 * c.inter), buf(T, c.inter)
+        self.pos_host = torch.zeros(T, dtype=torch.int32).pin_memory()
+        self.pos = torch.zeros(T, dtype=torch.int32, device=self.dev)
+        self.tokens = torch.randint(0, c.vocab, (T,), generator=gen, device=self.dev)
+        self.ws = torch.empty(64 << 20, dtype=torch.uint8, device=self.dev)
+
+    def forward(self, rows, stream=None):
+        """Runs one iteration for the batch ``rows`` [(slot, start, len, ctx)];
+        returns the greedy next token of every row (device int64 [n_rows]), or
+        None when the model has no LM head."""
+        import torch
+        c = self.cfg
+        rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int32).reshape(-1, 4))
+        T = int(rows[:, 2].sum())
+        if T == 0:
+            return None
+        if T > self.max_tokens:
+            raise ValueError(f"batch of {T} tokens exceeds the model's {self.max_tokens}")
+        s = stream or torch.cuda.current_stream(self.dev)
+        need = cp.workspace_bytes(self.desc, rows)
+        if need > self.ws.numel():
+            self.ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
+        pos = positions_of(rows)
+        self.pos_host[:T].numpy()[:] = pos
+        with torch.cuda.stream(s):
+            self.pos[:T].copy_(self.pos_host[:T], non_blocking=True)
+            x, h = self.x[:T], self.h[:T]
+            torch.index_select(self.embed, 0, self.tokens[:T], out=x)
+            qkv, q, k, v, attn = self.qkv[:T], self.q[:T], self.k[:T], self.v[:T], self.attn[:T]
+            gu, act = self.gu[:T], self.act[:T]
+            for L, kc, vc in zip(self.layers, self.kc, self.vc):
+                rmsnorm(x, L["in_norm"], h, c.eps, s)
+                torch.mm(h, L["qkv"].t(), out=qkv)
+                qkv_rope(qkv, L["q_norm"], L["k_norm"], self.pos, c.hq, c.hkv, c.head_dim,
+                         c.theta, c.eps, q, k, v, s)
+                cp.kv_append(self.desc, k, v, kc, vc, self.bt, rows, self.ws, stream=s)
+                cp.attn_mixed(self.desc, q, kc, vc, self.bt, rows, attn, self.ws, stream=s)
+                x.addmm_(attn.view(T, c.hq * c.head_dim), L["o"].t())
+                rmsnorm(x, L["post_norm"], h, c.eps, s)
+                torch.mm(h, L["gate_up"].t(), out=gu)
+                swiglu(gu, act, s)
+                x.addmm_(act, L["down"].t())
+            if self.lm_head is None:
+                return None
+            last = torch.from_numpy(np.cumsum(rows[:, 2]).astype(np.int64) - 1)
+            last = last[rows[:, 2] > 0].to(self.dev, non_blocking=True)
+            hl = torch.empty(len(last), c.hidden, dtype=torch.bfloat16, device=self.dev)
+            rmsnorm(x.index_select(0, last), self.final_norm, hl, c.eps, s)
+            return torch.argmax(hl @ self.lm_head.t(), dim=-1)
+
+
+class ModelEngine:
+    """StepEngine-compatible wrapper: one scheduler round = one model iteration."""
+
+    def __init__(self, model: Model):
+        import torch
+        self.model = model
+        self.max_tokens = model.max_tokens
+        self.stream = torch.cuda.current_stream(model.dev)
+        self.ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def step(self, rows) -> float:
+        rows = np.asarray(rows, dtype=np.int32).reshape(-1, 4)
+        if int(rows[:, 2].sum()) == 0:
+            return 0.0
+        self.ev[0].record(self.stream)
+        self.model.forward(rows, self.stream)
+        self.ev[1].record(self.stream)
+        self.ev[1].synchronize()
+        return self.ev[0].elapsed_time(self.ev[1]) * 1e3

@@ -1,0 +1,168 @@
+"""The decoder-layer kernels (libcplayer.so) and the layer around the
+attention step against the fp64 reference of oracle/layer.py, on the GPU.
+
+Tolerances.  Each kernel computes in fp32 (the rotation angle is reduced in
+fp64 before an fp32 sine and cosine) and
+rounds its output once to bf16, so its error is at most half a bf16 ulp of
+the result (2^-9 relative) plus fp32 noise: the tests allow 2^-8 relative
+plus a small absolute term.  The whole layer rounds to bf16 at every kernel
+and GEMM boundary (about eight roundings on the longest path, each 2^-9
+relative, accumulated through fp32 GEMMs): the test bounds the error by 4 %
+of the output's RMS at the maximum and 0.6 % on average."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import layer as ref
+from paper_2606_09061_amd import model as M
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda", 0)
+
+
+def _bf16(shape, seed, scale=1.0):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    return (torch.randn(*shape, generator=g) * scale).to(torch.bfloat16)
+
+
+def _f64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _close(got, want, rel=2.0 ** -8, abs_=1e-5):
+    err = np.abs(got - want)
+    bound = rel * np.abs(want) + abs_
+    assert np.all(err <= bound), f"max excess {np.max(err - bound):.3e}, max err {err.max():.3e}"
+
+
+@pytest.mark.parametrize("n,width", [(1, 8), (37, 4096), (5, 12288), (3, 520)])
+def test_rmsnorm_matches_reference(n, width):
+    print(f"rmsnorm n={n} width={width}", flush=True)
+    x = _bf16((n, width), 1, 3.0)
+    w = _bf16((width,), 2)
+    out = torch.empty_like(x, device=DEV)
+    M.rmsnorm(x.to(DEV), w.to(DEV), out, 1e-6)
+    torch.cuda.synchronize()
+    _close(_f64(out), ref.rmsnorm(_f64(x), _f64(w), 1e-6))
+
+
+def test_rmsnorm_in_place():
+    x = _bf16((9, 1024), 3).to(DEV)
+    w = _bf16((1024,), 4).to(DEV)
+    want = ref.rmsnorm(_f64(x), _f64(w), 1e-6)
+    M.rmsnorm(x, w, x, 1e-6)
+    torch.cuda.synchronize()
+    _close(_f64(x), want)
+
+
+@pytest.mark.parametrize("T,hq,hkv,D", [(1, 4, 2, 128), (50, 32, 8, 128), (7, 8, 1, 64)])
+def test_qkv_rope_matches_reference(T, hq, hkv, D):
+    print(f"qkv_rope T={T} hq={hq} hkv={hkv} D={D}", flush=True)
+    qkv = _bf16((T, (hq + 2 * hkv) * D), 5)
+    qw, kw = _bf16((D,), 6), _bf16((D,), 7)
+    pos = torch.from_numpy(np.random.default_rng(8).integers(0, 32768, T).astype(np.int32))
+    q = torch.empty(T, hq, D, dtype=torch.bfloat16, device=DEV)
+    k = torch.empty(T, hkv, D, dtype=torch.bfloat16, device=DEV)
+    v = torch.empty(T, hkv, D, dtype=torch.bfloat16, device=DEV)
+    M.qkv_rope(qkv.to(DEV), qw.to(DEV), kw.to(DEV), pos.to(DEV), hq, hkv, D, 1e6, 1e-6, q, k, v)
+    torch.cuda.synchronize()
+    rq, rk, rv = ref.qkv_rope(_f64(qkv), _f64(qw), _f64(kw), pos.numpy(), hq, hkv, D, 1e6, 1e-6)
+    _close(_f64(q), rq, abs_=1e-4)
+    _close(_f64(k), rk, abs_=1e-4)
+    assert torch.equal(v.cpu(), qkv.view(T, hq + 2 * hkv, D)[:, hq + hkv:])  # bit copy
+
+
+@pytest.mark.parametrize("T,inter", [(1, 8), (33, 12288), (4, 1000)])
+def test_swiglu_matches_reference(T, inter):
+    gu = _bf16((T, 2 * inter), 9, 4.0)
+    out = torch.empty(T, inter, dtype=torch.bfloat16, device=DEV)
+    M.swiglu(gu.to(DEV), out)
+    torch.cuda.synchronize()
+    _close(_f64(out), ref.swiglu(_f64(gu)), abs_=1e-6)
+
+
+def test_bad_arguments_are_rejected():
+    x = torch.zeros(4, 16, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(Exception):
+        M.rmsnorm(x[:, 1:9], x[0, :8], x[:, :8], 1e-6)   # strided view
+    lib = M.load()
+    p = x.data_ptr()
+    assert lib.cpl_rmsnorm(p + 2, p, p, 1, 8, 1e-6, None) != 0   # misaligned: nothing launched
+    assert lib.cpl_rmsnorm(p, p, p, 1, 12, 1e-6, None) != 0      # width not a multiple of 8
+    assert lib.cpl_qkv_rope(1, 1, 1, 1, 1, 1, 1, 96, 1e6, 1e-6, 1, 1, 1, None) != 0
+    assert lib.cpl_swiglu(1, 1, 1, 12, None) != 0
+
+
+def _small_model():
+    cfg = M.ModelConfig(hidden=256, layers=1, hq=4, hkv=2, head_dim=64, inter=512, vocab=1000,
+                        theta=1e4)
+    return M.Model(cfg, max_seqs=4, max_seq_len=256, max_tokens=256, seed=3, lm_head=True)
+
+
+def test_decoder_layer_matches_reference():
+    m = _small_model()
+    c = m.cfg
+    # prior context of slots 1 and 2 already in the pool; slot 0 starts fresh
+    rows = np.array([[1, 40, 1, 41], [0, 0, 70, 70], [2, 100, 33, 133], [3, 0, 1, 1]], np.int32)
+    bt = m.bt.cpu().numpy()
+    B = c.block_size
+    g = torch.Generator(device="cpu").manual_seed(11)
+    prior_k, prior_v = {}, {}
+    kc, vc = m.kc[0], m.vc[0]
+    kc.fill_(float("nan"))
+    vc.fill_(float("nan"))
+    for slot, start, _, _ in rows.tolist():
+        pk = torch.randn(start, c.hkv, c.head_dim, generator=g).to(torch.bfloat16)
+        pv = torch.randn(start, c.hkv, c.head_dim, generator=g).to(torch.bfloat16)
+        for p in range(start):
+            blk = int(bt[slot, p // B])
+            kc[blk, :, p % B, :] = pk[p].to(DEV)
+            vc[blk, :, :, p % B] = pv[p].to(DEV)
+        prior_k[slot], prior_v[slot] = _f64(pk), _f64(pv)
+    T = int(rows[:, 2].sum())
+    x0 = _f64(m.embed[m.tokens[:T]])
+    L = m.layers[0]
+    wts = {k: _f64(v) for k, v in L.items()}
+    want, want_k, want_v = ref.decoder_layer(x0, wts, rows.tolist(), prior_k, prior_v, c.hq,
+                                             c.hkv, c.head_dim, c.theta, c.eps,
+                                             1.0 / math.sqrt(c.head_dim))
+    m.forward(rows)
+    torch.cuda.synchronize()
+    got = _f64(m.x[:T])
+    rms = float(np.sqrt((want ** 2).mean()))
+    err = np.abs(got - want)
+    print(f"layer: rms {rms:.3e} max err {err.max():.3e} mean err {err.mean():.3e}", flush=True)
+    assert np.isfinite(got).all()
+    assert err.max() <= 0.04 * rms and err.mean() <= 0.006 * rms
+    # the new keys and values landed in the pool at their positions (same
+    # rounding chain as the output: RMSNorm, GEMM, per-head norm and rotation)
+    got_k, got_v = [], []
+    for slot, start, length, _ in rows.tolist():
+        for j in range(length):
+            p = start + j
+            blk = int(bt[slot, p // B])
+            got_k.append(_f64(kc[blk, :, p % B, :]))
+            got_v.append(_f64(vc[blk, :, :, p % B]))
+    for got_kv, want_kv in ((np.array(got_k), want_k), (np.array(got_v), want_v)):
+        rms_kv = float(np.sqrt((want_kv ** 2).mean()))
+        e = np.abs(got_kv - want_kv)
+        assert e.max() <= 0.04 * rms_kv and e.mean() <= 0.006 * rms_kv
+
+
+def test_model_forward_is_deterministic_and_finite():
+    cfg = M.ModelConfig(hidden=256, layers=3, hq=4, hkv=2, head_dim=64, inter=512, vocab=1000)
+    m = M.Model(cfg, max_seqs=4, max_seq_len=256, max_tokens=256, seed=5)
+    rows1 = np.array([[0, 0, 20, 20], [1, 0, 5, 5]], np.int32)
+    t1 = m.forward(rows1)
+    rows2 = np.array([[0, 20, 1, 21], [1, 5, 1, 6]], np.int32)
+    t2 = m.forward(rows2)
+    x2 = m.x[:2].clone()
+    m.forward(rows1)          # same prefix again, then the same decode step
+    t2b = m.forward(rows2)
+    torch.cuda.synchronize()
+    assert t1.shape == (2,) and t2.shape == (2,)
+    assert torch.equal(t2, t2b) and torch.equal(x2, m.x[:2])
+    assert torch.isfinite(m.x[:2].float()).all()
