@@ -365,11 +365,45 @@ def copy_calibration(mib, reps):
 
 
 def measured_peaks(reps=20):
-    """Achieved rates of plain library operations on this GPU, beside the
-    datasheet peaks: a large bf16 GEMM (torch.matmul), a device copy and a
-    read-only reduction."""
+    """Practical peaks of this GPU beside the datasheet ones: the device
+    attributes behind the datasheet figures, a register-only bf16 MFMA loop
+    (constant and random operands) and a streaming non-temporal read
+    (libcppeaks.so), then plain library operations: a large bf16 GEMM
+    (torch.matmul), a device copy and a read-only reduction."""
     import torch
+    from paper_2606_09061_amd import peaks
     dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    info = peaks.device_info(0)
+    # datasheet-style peak from the attributes: 4 SIMD x 512 bf16 flop per clock per CU
+    info["bf16_tflops_at_attr_clock"] = info["compute_units"] * info["clock_khz"] * 1e3 * 2048 * 2 / 1e12
+
+    def timed_ms(fn, n=reps):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        b.synchronize()
+        return a.elapsed_time(b) / n
+
+    ops = torch.randn(1 << 24, device=dev, dtype=torch.float32).to(torch.bfloat16)  # 32 MiB
+    blocks, threads, iters = 4 * info["compute_units"], 256, 2000
+    out = torch.empty(blocks * threads, device=dev, dtype=torch.float32)
+    mfma = {}
+    for rnd in (0, 1):
+        ms = timed_ms(lambda: peaks.mfma_loop(ops, out, blocks, threads, iters, rnd, stream), 5)
+        flops = 32768.0 * 16 * iters * (threads // 64) * blocks
+        mfma["random" if rnd else "constant"] = flops / (ms * 1e-3) / 1e12
+    del ops, out
+    big = torch.empty(1 << 31, device=dev, dtype=torch.uint8).fill_(1)
+    rblocks = 8 * info["compute_units"]
+    rout = torch.empty(rblocks * 256, device=dev, dtype=torch.int32)
+    t_rs = timed_ms(lambda: peaks.read_stream(big, rout, rblocks, stream)) * 1e-3
+    del big, rout
 
     def timed(fn):
         for _ in range(3):
@@ -396,6 +430,9 @@ def measured_peaks(reps=20):
     f = src.view(torch.float32)
     t_rd = timed(lambda: f.sum())
     return {"measured_peaks": {
+        "device": info,
+        "mfma_loop_bf16_tflops": mfma,
+        "read_stream_2gib_gbs": (1 << 31) / t_rs / 1e9,
         "bf16_gemm_8192_tflops": 2 * n ** 3 / t_mm / 1e12,
         "copy_2gib_gbs_read_plus_write": 2 * m / t_cp / 1e9,
         "sum_2gib_read_gbs": m / t_rd / 1e9,

@@ -1,6 +1,7 @@
 """Builds, in-tree, libcpattn.so (the attention step: HIP kernels + C ABI,
 gfx950, hipcc), libcplayer.so (the element-wise kernels of the decoder layer
-around it, gfx950) and libcpsched.so (the host scheduler, plain C++17, g++)."""
+around it, gfx950), libcppeaks.so (peak-rate microbenchmarks, gfx950) and
+libcpsched.so (the host scheduler, plain C++17, g++)."""
 
 from __future__ import annotations
 
@@ -17,6 +18,8 @@ LIB = os.path.join(PKG, "libcpattn.so")
 SCHED_LIB = os.path.join(PKG, "libcpsched.so")
 LAYER_LIB = os.path.join(PKG, "libcplayer.so")
 LAYER_SOURCES = ["layer.hip"]
+PEAKS_LIB = os.path.join(PKG, "libcppeaks.so")
+PEAKS_SOURCES = ["peaks.hip"]
 CXX = os.environ.get("CXX", "g++")
 SOURCES = ["api.hip", "plan.cpp", "append.hip", "decode.hip", "prefill.hip", "merge.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -43,9 +46,11 @@ def _compile(src: str) -> str:
 def build(jobs: int = 8) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(_compile, SOURCES + LAYER_SOURCES))
-    _link(objs[:len(SOURCES)], LIB)
-    _link(objs[len(SOURCES):], LAYER_LIB)
+        objs = list(ex.map(_compile, SOURCES + LAYER_SOURCES + PEAKS_SOURCES))
+    n1, n2 = len(SOURCES), len(SOURCES) + len(LAYER_SOURCES)
+    _link(objs[:n1], LIB)
+    _link(objs[n1:n2], LAYER_LIB)
+    _link(objs[n2:], PEAKS_LIB)
     build_sched()
     return LIB
 

@@ -187,6 +187,8 @@ class LatencyPredictor:
                 print(f"epoch {ep}: loss {cur:.5f}")
             if progress is not None and (ep + 1) % 25 == 0:
                 progress(ep + 1, cur)
+        if best_state is None:
+            raise RuntimeError("predictor training diverged: every epoch's loss was NaN")
         with torch.no_grad():
             for p, b in zip(net.parameters(), best_state):
                 p.copy_(b)
