@@ -177,6 +177,8 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_PREFILL_TARGET_ITEMS")) t.prefill_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_MIN_SPLIT")) t.prefill_min_split = std::max(1, atoi(s));
   if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::max(1, atoi(s));
+  if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_ROWS"))
+    t.prefill_wide_min_rows = std::max<int64_t>(1, atoll(s));
   return t;
 }
 
@@ -286,7 +288,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len < t.prefill_min_len) continue;
-    const bool wide = (int64_t)m.chunk_len * G > kPrefillRows;
+    const bool wide = (int64_t)m.chunk_len * G >= t.prefill_wide_min_rows;
     const int32_t tt = wide ? kPrefillRowsWide / G : tile_tok;
     detail::Chunk ch{(int32_t)tiles.size(), 0, 0, wide};
     for (int32_t j = 0; j < m.chunk_len; j += tt) {
