@@ -925,7 +925,7 @@ def main():
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the attention step is "
               "measured on a single MI355X; a multi-GPU run would shard heads across GPUs with "
-              "no collective inside the step and is not part of this build.", file=sys.stderr)
+              "no collective inside the step and is not implemented here.", file=sys.stderr)
         sys.exit(2)
     cfgs = [1, 2, 3, 4, 5] if args.all else [args.config]
     for c in cfgs:
