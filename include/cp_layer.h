@@ -10,8 +10,8 @@
  *        cp_attn_mixed -> O projection (+ x) -> RMSNorm -> gate/up
  *        projection -> cpl_swiglu -> down projection (+ residual)
  *
- * The projections are plain GEMMs and run in the platform BLAS; these three
- * kernels are the rest.  The paper does not describe the model; the layer
+ * The projections are plain GEMMs: the platform BLAS runs them, except for
+ * decode-sized batches, where cpl_gemm_skinny streams the weights itself.  The paper does not describe the model; the layer
  * follows the published Qwen3 architecture (RMSNorm, per-head RMSNorm on
  * queries and keys before rotary embedding, SwiGLU feed-forward).
  *
@@ -57,6 +57,15 @@ int cpl_qkv_rope(const void* qkv, const void* q_norm_w, const void* k_norm_w,
 /* SwiGLU: out[t][i] = silu(gu[t][i]) * gu[t][inter + i], silu(g) = g / (1 + e^-g);
  * gu [T][2*inter], out [T][inter]; inter % 8 == 0. */
 int cpl_swiglu(const void* gu, void* out, int32_t n_tokens, int32_t inter, void* stream);
+
+/* Projection of a small batch: c[M][N] = a[M][K] . w[N][K]^T (+ r[M][N]), bf16 in and
+ * out, fp32 accumulation, for the decode-sized batches where a library GEMM
+ * cannot stream the weights at memory speed.  1 <= M <= 128, N % 32 == 0,
+ * K % 256 == 0; r may be NULL or equal to c (in-place residual add); a must
+ * not alias c.  w is read once; a is re-read from cache by every 32-column
+ * slice of the output. */
+int cpl_gemm_skinny(const void* a, const void* w, const void* r, void* c, int32_t m, int32_t n,
+                    int32_t k, void* stream);
 
 #ifdef __cplusplus
 }

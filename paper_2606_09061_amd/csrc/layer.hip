@@ -130,6 +130,84 @@ __global__ __launch_bounds__(kThreads) void swiglu_kernel(const uint4* __restric
   out[i] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+
+// Skinny GEMM C[M][N] = A[M][K] * W[N][K]^T (+ R), M <= 32 * MB: every weight
+// byte is streamed from HBM once while the activations stay in L2.  A
+// workgroup owns 32 output columns; its four waves take a quarter of K
+// each, with v_mfma_f32_32x32x16_bf16 on W rows (the 32 "m" rows) against
+// activation rows (the 32 "n" columns), then add their partial sums through
+// LDS.  Each lane's operands are 16 contiguous bytes of a W or A row.
+template <int MB>
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint4* __restrict__ A,
+                                                          const uint4* __restrict__ W,
+                                                          const uint16_t* R, uint16_t* C, int M,
+                                                          int N, int K) {
+  typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+  typedef float f32x16_t __attribute__((ext_vector_type(16)));
+  constexpr int kRowPad = 33;  // floats per reduction row (bank spread)
+  __shared__ float red[4][32 * MB][kRowPad];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * 32;
+  const int kq = K / 4, kb = wave * kq;
+  const int K8 = K / 8;  // uint4 per row
+  const int lr = lane & 31, lg = lane >> 5;
+  const uint4* wrow = W + (int64_t)(n0 + lr) * K8 + (kb >> 3) + lg;
+  const uint4* arow[MB];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+    arow[rb] = A + (int64_t)min(rb * 32 + lr, M - 1) * K8 + (kb >> 3) + lg;
+  f32x16_t acc[MB];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[rb][r] = 0.f;
+  constexpr int U = 4;  // k-steps of 16 per batch of loads
+  uint4 wf[U], af[U][MB];
+  auto load = [&](int s) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      wf[u] = wrow[(s + u) * 2];
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) af[u][rb] = arow[rb][(s + u) * 2];
+    }
+  };
+  const int steps = kq / 16;  // multiple of U
+  load(0);
+  for (int s = 0; s < steps; s += U) {
+    uint4 wc[U], ac[U][MB];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      wc[u] = wf[u];
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) ac[u][rb] = af[u][rb];
+    }
+    if (s + U < steps) load(s + U);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb)
+        acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, wc[u]), __builtin_bit_cast(bf16x8_t, ac[u][rb]),
+            acc[rb], 0, 0, 0);
+  }
+  // D[i][j] = sum_k W[n0 + i][k] A[32 rb + j][k]: lane holds j = lane % 32,
+  // register r holds i = 8 (r / 4) + 4 (lane / 32) + r % 4
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      red[wave][rb * 32 + lr][8 * (r >> 2) + 4 * lg + (r & 3)] = acc[rb][r];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 32 * MB * 32; idx += 256) {
+    const int j = idx >> 5, i = idx & 31;
+    if (j >= M) break;  // rows are visited in increasing order
+    float v = red[0][j][i] + red[1][j][i] + red[2][j][i] + red[3][j][i];
+    const int64_t o = (int64_t)j * N + n0 + i;
+    if (R) v += bf16_to_f32(R[o]);
+    C[o] = f32_to_bf16(v);
+  }
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 int launched() { return hipGetLastError() == hipSuccess ? CP_OK : CP_ERR_HIP; }
@@ -182,6 +260,27 @@ int cpl_swiglu(const void* gu, void* out, int32_t n_tokens, int32_t inter, void*
   (void)hipGetLastError();
   hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)blocks), dim3(kThreads), 0,
                      (hipStream_t)stream, (const uint4*)gu, (uint4*)out, inter / 8, n);
+  return launched();
+}
+
+int cpl_gemm_skinny(const void* a, const void* w, const void* r, void* c, int32_t m, int32_t n,
+                    int32_t k, void* stream) {
+  if (m < 1 || m > 128 || n < 32 || n % 32 != 0 || k < 256 || k % 256 != 0 || k > (1 << 20))
+    return CP_ERR_INVALID_ARG;
+  if (!a || !w || !c || !aligned16(a) || !aligned16(w) || a == c) return CP_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  const dim3 grid(n / 32), block(256);
+  hipStream_t s = (hipStream_t)stream;
+  const uint4* A = (const uint4*)a;
+  const uint4* W = (const uint4*)w;
+  const uint16_t* R = (const uint16_t*)r;
+  uint16_t* C = (uint16_t*)c;
+  if (m <= 32)
+    hipLaunchKernelGGL(gemm_skinny_kernel<1>, grid, block, 0, s, A, W, R, C, m, n, k);
+  else if (m <= 64)
+    hipLaunchKernelGGL(gemm_skinny_kernel<2>, grid, block, 0, s, A, W, R, C, m, n, k);
+  else
+    hipLaunchKernelGGL(gemm_skinny_kernel<4>, grid, block, 0, s, A, W, R, C, m, n, k);
   return launched();
 }
 

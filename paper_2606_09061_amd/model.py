@@ -9,9 +9,11 @@ scheduler's batch through every layer of such a model with synthetic weights:
     cpl_swiglu -> down GEMM (+ residual)] -> RMSNorm -> LM head on each row's
     last token -> argmax
 
-The GEMMs are plain library GEMMs (torch.mm / addmm, i.e. hipBLASLt); every
-other step runs in this package's HIP kernels (libcplayer.so for the
-element-wise parts, libcpattn.so for append and attention).  Each layer has
+Projections of small batches (<= 32 tokens, QKV and O) run in this
+package's skinny GEMM kernel, the rest as library GEMMs (torch.mm / addmm,
+i.e. hipBLASLt); every other step runs in this package's HIP kernels
+(libcplayer.so for the element-wise parts, libcpattn.so for append and
+attention).  Each layer has
 its own paged KV pool; all layers share one block table, whose row s maps
 slot s's logical blocks to physical blocks (a random permutation, so pages
 are scattered).  Weights are N(0, 0.02) in bf16, norms 1.
@@ -47,14 +49,15 @@ def load():
     lib.cpl_rmsnorm.argtypes = [P, P, P, I32, I32, F, P]
     lib.cpl_qkv_rope.argtypes = [P, P, P, P, I32, I32, I32, I32, D, F, P, P, P, P]
     lib.cpl_swiglu.argtypes = [P, P, I32, I32, P]
-    for f in (lib.cpl_rmsnorm, lib.cpl_qkv_rope, lib.cpl_swiglu):
+    lib.cpl_gemm_skinny.argtypes = [P, P, P, P, I32, I32, I32, P]
+    for f in (lib.cpl_rmsnorm, lib.cpl_qkv_rope, lib.cpl_swiglu, lib.cpl_gemm_skinny):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
 
 
 def exported_symbols():
-    return ["cpl_rmsnorm", "cpl_qkv_rope", "cpl_swiglu"]
+    return ["cpl_rmsnorm", "cpl_qkv_rope", "cpl_swiglu", "cpl_gemm_skinny"]
 
 
 def _check(rc, what):
@@ -96,6 +99,43 @@ def swiglu(gu, out, stream=None):
     _dense(gu, out)
     _check(load().cpl_swiglu(gu.data_ptr(), out.data_ptr(), gu.shape[0], out.shape[-1],
                              _s(stream)), "cpl_swiglu")
+
+
+# Where the skinny kernel beats the library GEMM on MI355X (measured, per
+# launch): batches of at most 32 rows on projections of K <= 4096 inputs and
+# N <= 8192 outputs (QKV: 20.5 -> 17.1 us at 32 rows, 22.6 -> 11.7 us at one
+# row; O: 19.7 -> 16.9, 21.1 -> 11.4).  Larger batches re-read the
+# activations from cache for every 32-column slice and lose to the library.
+SKINNY_MAX_M, SKINNY_MAX_K, SKINNY_MAX_N = 32, 4096, 8192
+
+
+def gemm_skinny(a, w, out, residual=None, stream=None):
+    """out [M, N] = a [M, K] @ w [N, K]^T (+ residual, which may be out itself)."""
+    _dense(a, w, out)
+    if residual is not None:
+        _dense(residual)
+    M, K = a.shape
+    N = w.shape[0]
+    _check(load().cpl_gemm_skinny(a.data_ptr(), w.data_ptr(),
+                                  residual.data_ptr() if residual is not None else None,
+                                  out.data_ptr(), M, N, K, _s(stream)), "cpl_gemm_skinny")
+
+
+def project(a, w, out, residual=None, stream=None):
+    """a @ w^T into out (+ residual): the skinny kernel where it is faster
+    (small batches, moderate projections), the platform BLAS otherwise."""
+    import torch
+    M, K = a.shape
+    N = w.shape[0]
+    if (M <= SKINNY_MAX_M and K <= SKINNY_MAX_K and N <= SKINNY_MAX_N and N % 32 == 0
+            and K % 256 == 0):
+        gemm_skinny(a, w, out, residual, stream)
+    elif residual is None:
+        torch.mm(a, w.t(), out=out)
+    elif residual is out:
+        out.addmm_(a, w.t())
+    else:
+        torch.addmm(residual, a, w.t(), out=out)
 
 
 @dataclass
@@ -216,16 +256,16 @@ class Model:
             gu, act = self.gu[:T], self.act[:T]
             for L, kc, vc in zip(self.layers, self.kc, self.vc):
                 rmsnorm(x, L["in_norm"], h, c.eps, s)
-                torch.mm(h, L["qkv"].t(), out=qkv)
+                project(h, L["qkv"], qkv, None, s)
                 qkv_rope(qkv, L["q_norm"], L["k_norm"], self.pos, c.hq, c.hkv, c.head_dim,
                          c.theta, c.eps, q, k, v, s)
                 cp.kv_append(self.desc, k, v, kc, vc, self.bt, rows, self.ws, stream=s)
                 cp.attn_mixed(self.desc, q, kc, vc, self.bt, rows, attn, self.ws, stream=s)
-                x.addmm_(attn.view(T, c.hq * c.head_dim), L["o"].t())
+                project(attn.view(T, c.hq * c.head_dim), L["o"], x, x, s)
                 rmsnorm(x, L["post_norm"], h, c.eps, s)
-                torch.mm(h, L["gate_up"].t(), out=gu)
+                project(h, L["gate_up"], gu, None, s)
                 swiglu(gu, act, s)
-                x.addmm_(act, L["down"].t())
+                project(act, L["down"], x, x, s)
             if self.lm_head is None:
                 return None
             last = torch.from_numpy(np.cumsum(rows[:, 2]).astype(np.int64) - 1)

@@ -96,17 +96,34 @@ def test_bad_arguments_are_rejected():
     assert lib.cpl_swiglu(1, 1, 1, 12, None) != 0
 
 
+def test_project_matches_library_and_reference():
+    from paper_2606_09061_amd import model as MM
+    for m_rows in (1, 32, 33):          # skinny kernel, then the library GEMM
+        a = _bf16((m_rows, 512), 31).to(DEV)
+        w = _bf16((256, 512), 32, 0.05).to(DEV)
+        x = _bf16((m_rows, 256), 33).to(DEV)
+        want = _f64(x) + _f64(a) @ _f64(w).T
+        MM.project(a, w, x, x)
+        torch.cuda.synchronize()
+        err = np.abs(_f64(x) - want)
+        assert err.max() <= 2e-2 * max(1.0, float(np.abs(want).max()))
+
+
 def _small_model():
     cfg = M.ModelConfig(hidden=256, layers=1, hq=4, hkv=2, head_dim=64, inter=512, vocab=1000,
                         theta=1e4)
     return M.Model(cfg, max_seqs=4, max_seq_len=256, max_tokens=256, seed=3, lm_head=True)
 
 
-def test_decoder_layer_matches_reference():
+@pytest.mark.parametrize("rows", [
+    [[1, 40, 1, 41], [0, 0, 70, 70], [2, 100, 33, 133], [3, 0, 1, 1]],   # 105 tokens: library GEMMs
+    [[1, 40, 1, 41], [0, 0, 20, 20], [2, 100, 5, 105], [3, 0, 1, 1]],    # 27 tokens: skinny kernel
+])
+def test_decoder_layer_matches_reference(rows):
     m = _small_model()
     c = m.cfg
     # prior context of slots 1 and 2 already in the pool; slot 0 starts fresh
-    rows = np.array([[1, 40, 1, 41], [0, 0, 70, 70], [2, 100, 33, 133], [3, 0, 1, 1]], np.int32)
+    rows = np.array(rows, np.int32)
     bt = m.bt.cpu().numpy()
     B = c.block_size
     g = torch.Generator(device="cpu").manual_seed(11)
@@ -166,3 +183,33 @@ def test_model_forward_is_deterministic_and_finite():
     assert t1.shape == (2,) and t2.shape == (2,)
     assert torch.equal(t2, t2b) and torch.equal(x2, m.x[:2])
     assert torch.isfinite(m.x[:2].float()).all()
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 32, 256), (17, 96, 512), (32, 4096, 4096), (33, 64, 256),
+                                   (64, 6144, 4096), (100, 4096, 12288), (128, 1024, 1024)])
+@pytest.mark.parametrize("residual", [False, True])
+def test_gemm_skinny_matches_reference(M, N, K, residual):
+    print(f"gemm_skinny M={M} N={N} K={K} residual={residual}", flush=True)
+    a = _bf16((M, K), 21)
+    w = _bf16((N, K), 22, 0.05)
+    r = _bf16((M, N), 23) if residual else None
+    out = (r.clone() if residual else torch.empty(M, N, dtype=torch.bfloat16)).to(DEV)
+    ad, wd = a.to(DEV), w.to(DEV)
+    from paper_2606_09061_amd import model as MM
+    MM.gemm_skinny(ad, wd, out, out if residual else None)
+    torch.cuda.synchronize()
+    want = _f64(a) @ _f64(w).T + (_f64(r) if residual else 0.0)
+    # fp32 accumulation over K terms, then one bf16 rounding
+    slack = 2.0 ** -20 * (np.abs(_f64(a)) @ np.abs(_f64(w)).T)
+    err = np.abs(_f64(out) - want)
+    assert np.all(err <= 2.0 ** -8 * np.abs(want) + slack + 1e-6), f"max err {err.max():.3e}"
+
+
+def test_gemm_skinny_rejects_unsupported_shapes():
+    lib = M.load()
+    x = torch.zeros(256, 256, dtype=torch.bfloat16, device=DEV)
+    p = x.data_ptr()
+    assert lib.cpl_gemm_skinny(p, p + 16 * 256 * 2, None, p + 64 * 256 * 2, 129, 32, 256, None) != 0
+    assert lib.cpl_gemm_skinny(p, p, None, p + 1024, 8, 48, 256, None) != 0     # N % 32
+    assert lib.cpl_gemm_skinny(p, p, None, p + 1024, 8, 32, 320, None) != 0    # K % 256
+    assert lib.cpl_gemm_skinny(p, p, None, p, 8, 32, 256, None) != 0           # a aliases c
