@@ -671,7 +671,7 @@ def sched_experiment(out_dir, engine="step", epochs=300, parts=("lprs", "aging",
     serve.serve(cfg(), wl.uniform_stream(30, HIGH, seed=99), eng)  # warm-up
     log("[sched] warm-up done")
 
-    need_model = "lprs" in parts or "apc" in parts
+    need_model = "lprs" in parts or "apc" in parts or "lprs_sweep" in parts
     # 1. samples
     X, Y, runs = [], [], []
     plan = [(b, HIGH, "uniform") for b in (256, 512, 1024, 2048)]
@@ -697,6 +697,8 @@ def sched_experiment(out_dir, engine="step", epochs=300, parts=("lprs", "aging",
         _aging_runs(out, P, cfg, strip, eng)
     if "apc" in parts:
         _apc_runs(out, P, cfg, strip, eng, model)
+    if "lprs_sweep" in parts:
+        _lprs_sweep(out, P, cfg, strip, eng, model)
     with open(os.path.join(out_dir, "sched_results.json"), "w") as fh:
         json.dump(out, fh, indent=1)
     return out
@@ -776,6 +778,28 @@ def _lprs_runs(out, P, cfg, strip, eng, model):
     cmp["regular"] = row
     log("[sched] LPRS vs token budget at regular load done")
     out["lprs_vs_token_budget"] = cmp
+
+
+def _lprs_sweep(out, P, cfg, strip, eng, model):
+    """Sensitivity of LPRS + APC at high load to the constants the paper
+    leaves open: the overflow penalty lambda_o (lambda_u = 1) and the search
+    granularity delta, at T* = the token budget's 90th-percentile round."""
+    import numpy as np
+    import workloads as wl
+    from paper_2606_09061_amd import sched, serve
+    reqs = wl.uniform_stream(P["n_req"], P["high"], seed=1000)
+    tb = serve.serve(cfg(max_tokens=1024), reqs, eng, record=True)
+    t = float(np.percentile(tb["_step_us"], 90))
+    res = {"target_us": t, "token_budget_1024": _vs_target(strip(tb), tb["_step_us"], t)}
+    for lo in (1.0, 2.0, 4.0, 8.0):
+        for delta in (32, 128):
+            for bmax in (1024, 2048):
+                r = serve.serve(cfg(max_tokens=bmax, chunking=sched.CHUNK_LPRS, target_us=t,
+                                    apc=True, lambda_o=lo, delta=delta), reqs, eng,
+                                predictor=model)
+                res[f"lo{lo:g}_d{delta}_B{bmax}"] = strip(r)
+        log(f"[sched] LPRS sweep lambda_o={lo} done")
+    out["lprs_sweep"] = res
 
 
 def _aging_runs(out, P, cfg, strip, eng):
@@ -906,7 +930,7 @@ def main():
     ap.add_argument("--sched-engine", choices=["step", "model"], default="step",
                     help="with --sched: the attention step alone or the whole 36-layer model")
     ap.add_argument("--sched-parts", default="lprs,aging,apc",
-                    help="with --sched: comma-separated subset of lprs, aging, apc")
+                    help="with --sched: comma-separated subset of lprs, aging, apc, lprs_sweep")
     ap.add_argument("--model", action="store_true",
                     help="only time whole iterations of the synthetic Qwen3-8B stack")
     ap.add_argument("--model-case", action="append", default=None,
