@@ -132,6 +132,35 @@ int cp_attn_mixed(const cp_attn_desc *desc, const void *q, const void *k_cache,
                   const void *v_cache, const int32_t *block_tables, const cp_row_meta *rows,
                   int32_t n_rows, void *out, void *ws, size_t ws_bytes, void *stream);
 
+/* A batch's attention plan, made once and run several times: the layers of
+ * one model iteration share rows, block tables and plan, and only q, the
+ * caches and out change.  Plain data filled by cp_attn_prepare and owned by
+ * the caller; the work lists it describes live in the workspace it was
+ * prepared in, so it stays valid while nothing but cp_attn_run writes that
+ * workspace (give cp_kv_append its own). */
+typedef struct {
+    cp_attn_desc desc;            /* the geometry it was made for             */
+    int64_t tokens;               /* scheduled tokens T of the batch          */
+    int64_t ws_bytes;             /* workspace bytes it occupies              */
+    int32_t n_prefill_slots, n_prefill_wide_slots, n_decode, n_merge;
+    int64_t off_prefill, off_prefill_slots, off_prefill_wide, off_prefill_wide_slots;
+    int64_t off_decode, off_merge, off_part_o, off_part_lse;  /* byte offsets in ws */
+} cp_attn_plan;
+
+/* Validates the batch, plans it and uploads the plan into ws (asynchronous on
+ * stream); fills *plan.  Same checks and codes as cp_attn_mixed.  An empty
+ * batch gives a plan whose runs do nothing. */
+int cp_attn_prepare(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows,
+                    void *ws, size_t ws_bytes, void *stream, cp_attn_plan *plan);
+
+/* cp_attn_mixed for a prepared batch: the same kernels on the same plan, so
+ * the output equals cp_attn_mixed's bit for bit.  ws must be the workspace
+ * the plan was prepared in (ws_bytes >= plan->ws_bytes); stream order must put
+ * the prepare before the run. */
+int cp_attn_run(const cp_attn_plan *plan, const void *q, const void *k_cache,
+                const void *v_cache, const int32_t *block_tables, void *out, void *ws,
+                size_t ws_bytes, void *stream);
+
 /* Plan summary for diagnostics and tests (host only, enqueues nothing).
  * counts[0..5] receive: prefill work items, decode work items, merge groups,
  * partial rows, workspace bytes, decode blocks per split. */

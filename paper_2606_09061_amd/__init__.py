@@ -8,9 +8,12 @@ scheduling iteration's attention step on torch tensors.
 """
 
 from .binding import (  # noqa: F401
+    AttnPlan,
     CpError,
     Desc,
     attn_mixed,
+    attn_prepare,
+    attn_run,
     check_batch,
     desc_for,
     kv_append,

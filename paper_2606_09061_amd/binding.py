@@ -45,6 +45,17 @@ class Desc(ctypes.Structure):
     ]
 
 
+class AttnPlan(ctypes.Structure):
+    """cp_attn_plan: a batch's attention plan, prepared once, run per layer."""
+
+    _fields_ = [("desc", Desc), ("tokens", ctypes.c_int64), ("ws_bytes", ctypes.c_int64),
+                ("n_prefill_slots", ctypes.c_int32), ("n_prefill_wide_slots", ctypes.c_int32),
+                ("n_decode", ctypes.c_int32), ("n_merge", ctypes.c_int32)] + [
+        (n, ctypes.c_int64) for n in ("off_prefill", "off_prefill_slots", "off_prefill_wide",
+                                      "off_prefill_wide_slots", "off_decode", "off_merge",
+                                      "off_part_o", "off_part_lse")]
+
+
 _lib = None
 
 
@@ -68,6 +79,10 @@ def load():
     lib.cp_kv_append.restype = ctypes.c_int
     lib.cp_attn_mixed.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp]
     lib.cp_attn_mixed.restype = ctypes.c_int
+    lib.cp_attn_prepare.argtypes = [dp, vp, i32, vp, sz, vp, vp]
+    lib.cp_attn_prepare.restype = ctypes.c_int
+    lib.cp_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.cp_attn_run.restype = ctypes.c_int
     lib.cp_plan_summary.argtypes = [dp, vp, i32, vp]
     lib.cp_plan_summary.restype = ctypes.c_int
     lib.cp_plan_items.argtypes = [dp, vp, i32, vp, i64]
@@ -80,8 +95,8 @@ def load():
 
 def exported_symbols():
     return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch", "cp_kv_append",
-            "cp_attn_mixed", "cp_plan_summary", "cp_plan_items", "cp_profile_begin",
-            "cp_profile_end"]
+            "cp_attn_mixed", "cp_attn_prepare", "cp_attn_run", "cp_plan_summary", "cp_plan_items",
+            "cp_profile_begin", "cp_profile_end"]
 
 
 def strerror(code: int) -> str:
@@ -164,6 +179,28 @@ def attn_mixed(desc: Desc, q, k_cache, v_cache, block_tables, rows, out, ws, ws_
                               nbytes, _stream(stream))
     if rc != CP_OK:
         raise CpError(rc, "cp_attn_mixed")
+
+
+def attn_prepare(desc: Desc, rows, ws, ws_bytes=None, stream=None) -> AttnPlan:
+    """Plans the batch once and uploads the plan into ws (cp_attn_prepare)."""
+    r = _rows(rows)
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    plan = AttnPlan()
+    rc = load().cp_attn_prepare(ctypes.byref(desc), r.ctypes.data, r.shape[0], _ptr(ws), nbytes,
+                                _stream(stream), ctypes.byref(plan))
+    if rc != CP_OK:
+        raise CpError(rc, "cp_attn_prepare")
+    return plan
+
+
+def attn_run(plan: AttnPlan, q, k_cache, v_cache, block_tables, out, ws, ws_bytes=None,
+             stream=None) -> None:
+    """cp_attn_mixed for a batch prepared by attn_prepare in the same workspace."""
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    rc = load().cp_attn_run(ctypes.byref(plan), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                            _ptr(block_tables), _ptr(out), _ptr(ws), nbytes, _stream(stream))
+    if rc != CP_OK:
+        raise CpError(rc, "cp_attn_run")
 
 
 def plan_summary(desc: Desc, rows) -> dict:

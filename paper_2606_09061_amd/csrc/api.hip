@@ -318,6 +318,119 @@ int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new,
   }
 }
 
+int cp_attn_prepare(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows, void* ws,
+                    size_t ws_bytes, void* stream, cp_attn_plan* plan) {
+  if (!plan) return CP_ERR_INVALID_ARG;
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  cp_attn_plan pl{};
+  pl.desc = *desc;
+  pl.tokens = total_tokens(rows, n_rows);
+  if (pl.tokens == 0) {
+    *plan = pl;
+    return CP_OK;
+  }
+  if (!ws || !aligned(ws, 256)) return CP_ERR_INVALID_ARG;
+  try {
+    Plan& p = thread_plan();
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
+    thread_local std::vector<uint8_t> buf;
+    serialize(p, buf);
+    const int rc = upload(ws, buf.data(), buf.size(), reinterpret_cast<hipStream_t>(stream));
+    if (rc != CP_OK) return rc;
+    pl.ws_bytes = (int64_t)p.ws_bytes;
+    pl.n_prefill_slots = (int32_t)p.prefill_slots.size();
+    pl.n_prefill_wide_slots = (int32_t)p.prefill_wide_slots.size();
+    pl.n_decode = (int32_t)p.decode.size();
+    pl.n_merge = (int32_t)p.merge.size();
+    pl.off_prefill = (int64_t)p.off_prefill;
+    pl.off_prefill_slots = (int64_t)p.off_prefill_slots;
+    pl.off_prefill_wide = (int64_t)p.off_prefill_wide;
+    pl.off_prefill_wide_slots = (int64_t)p.off_prefill_wide_slots;
+    pl.off_decode = (int64_t)p.off_decode;
+    pl.off_merge = (int64_t)p.off_merge;
+    pl.off_part_o = (int64_t)p.off_part_o;
+    pl.off_part_lse = (int64_t)p.off_part_lse;
+    *plan = pl;
+    return CP_OK;
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
+}
+
+int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, const void* v_cache,
+                const int32_t* block_tables, void* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!plan) return CP_ERR_INVALID_ARG;
+  const cp_attn_desc* desc = &plan->desc;
+  const int vd = validate(desc, nullptr, 0);
+  if (vd != CP_OK) return vd;
+  if (plan->tokens == 0) return CP_OK;
+  if (plan->ws_bytes <= 0 || plan->n_prefill_slots < 0 || plan->n_prefill_wide_slots < 0 ||
+      plan->n_decode < 0 || plan->n_merge < 0)
+    return CP_ERR_INVALID_ARG;
+  if ((size_t)plan->ws_bytes > ws_bytes) return CP_ERR_WORKSPACE;
+  if (!q || !k_cache || !v_cache || !block_tables || !out || !ws) return CP_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
+      !aligned(ws, 256) || !aligned(block_tables, 4))
+    return CP_ERR_INVALID_ARG;
+  const int64_t offs[8] = {plan->off_prefill,  plan->off_prefill_slots, plan->off_prefill_wide,
+                           plan->off_prefill_wide_slots, plan->off_decode, plan->off_merge,
+                           plan->off_part_o, plan->off_part_lse};
+  for (int64_t o : offs)
+    if (o < 0 || o > plan->ws_bytes) return CP_ERR_INVALID_ARG;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  AttnArgs a;
+  a.prefill = reinterpret_cast<const PrefillItem*>(base + plan->off_prefill);
+  a.prefill_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_slots);
+  a.n_prefill_slots = plan->n_prefill_slots;
+  a.prefill_wide = reinterpret_cast<const PrefillItem*>(base + plan->off_prefill_wide);
+  a.prefill_wide_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_wide_slots);
+  a.n_prefill_wide_slots = plan->n_prefill_wide_slots;
+  a.decode = reinterpret_cast<const DecodeItem*>(base + plan->off_decode);
+  a.n_decode = plan->n_decode;
+  a.merge = reinterpret_cast<const MergeGroup*>(base + plan->off_merge);
+  a.n_merge = plan->n_merge;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_cache = static_cast<const uint16_t*>(k_cache);
+  a.v_cache = static_cast<const uint16_t*>(v_cache);
+  a.bt = block_tables;
+  a.out = static_cast<uint16_t*>(out);
+  a.part_o = reinterpret_cast<float*>(base + plan->off_part_o);
+  a.part_lse = reinterpret_cast<float*>(base + plan->off_part_lse);
+  a.hq = desc->num_q_heads;
+  a.hkv = desc->num_kv_heads;
+  a.block_size = desc->block_size;
+  a.mbr = desc->max_blocks_per_req;
+  a.scale_log2 = desc->sm_scale * 1.4426950408889634f;
+  const int D = desc->head_dim;
+  const int G = desc->num_q_heads / desc->num_kv_heads;
+  int rc = CP_OK;
+  if (a.n_prefill_slots > 0 || a.n_prefill_wide_slots > 0) {
+    const long pi = prof_open(1, s);
+    const hipError_t e = launch_prefill(D, G, a, s);
+    prof_close(pi, s);
+    rc = finish(e, s);
+    if (rc != CP_OK) return rc;
+  }
+  if (a.n_decode > 0) {
+    const long pi = prof_open(2, s);
+    const hipError_t e = launch_decode(D, desc->block_size, G, a, s);
+    prof_close(pi, s);
+    rc = finish(e, s);
+    if (rc != CP_OK) return rc;
+  }
+  if (a.n_merge > 0) {
+    const long pi = prof_open(3, s);
+    const hipError_t e = launch_merge(D, G, a, s);
+    prof_close(pi, s);
+    rc = finish(e, s);
+    if (rc != CP_OK) return rc;
+  }
+  return CP_OK;
+}
+
 int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
                   const void* v_cache, const int32_t* block_tables, const cp_row_meta* rows,
                   int32_t n_rows, void* out, void* ws, size_t ws_bytes, void* stream) {
@@ -328,67 +441,10 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
       !aligned(ws, 256) || !aligned(block_tables, 4))
     return CP_ERR_INVALID_ARG;
-  try {
-    Plan& p = thread_plan();
-    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
-    if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
-    thread_local std::vector<uint8_t> buf;
-    serialize(p, buf);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    int rc = upload(ws, buf.data(), buf.size(), s);
-    if (rc != CP_OK) return rc;
-    uint8_t* base = static_cast<uint8_t*>(ws);
-    AttnArgs a;
-    a.prefill = reinterpret_cast<const PrefillItem*>(base + p.off_prefill);
-    a.prefill_slots = reinterpret_cast<const int32_t*>(base + p.off_prefill_slots);
-    a.n_prefill_slots = (int)p.prefill_slots.size();
-    a.prefill_wide = reinterpret_cast<const PrefillItem*>(base + p.off_prefill_wide);
-    a.prefill_wide_slots = reinterpret_cast<const int32_t*>(base + p.off_prefill_wide_slots);
-    a.n_prefill_wide_slots = (int)p.prefill_wide_slots.size();
-    a.decode = reinterpret_cast<const DecodeItem*>(base + p.off_decode);
-    a.n_decode = (int)p.decode.size();
-    a.merge = reinterpret_cast<const MergeGroup*>(base + p.off_merge);
-    a.n_merge = (int)p.merge.size();
-    a.q = static_cast<const uint16_t*>(q);
-    a.k_cache = static_cast<const uint16_t*>(k_cache);
-    a.v_cache = static_cast<const uint16_t*>(v_cache);
-    a.bt = block_tables;
-    a.out = static_cast<uint16_t*>(out);
-    a.part_o = reinterpret_cast<float*>(base + p.off_part_o);
-    a.part_lse = reinterpret_cast<float*>(base + p.off_part_lse);
-    a.hq = desc->num_q_heads;
-    a.hkv = desc->num_kv_heads;
-    a.block_size = desc->block_size;
-    a.mbr = desc->max_blocks_per_req;
-    a.scale_log2 = desc->sm_scale * 1.4426950408889634f;
-    const int D = desc->head_dim;
-    const int G = desc->num_q_heads / desc->num_kv_heads;
-    const bool has_pf = a.n_prefill_slots > 0 || a.n_prefill_wide_slots > 0;
-    if (has_pf) {
-      const long pi = prof_open(1, s);
-      const hipError_t e = launch_prefill(D, G, a, s);
-      prof_close(pi, s);
-      rc = finish(e, s);
-      if (rc != CP_OK) return rc;
-    }
-    if (a.n_decode > 0) {
-      const long pi = prof_open(2, s);
-      const hipError_t e = launch_decode(D, desc->block_size, G, a, s);
-      prof_close(pi, s);
-      rc = finish(e, s);
-      if (rc != CP_OK) return rc;
-    }
-    if (a.n_merge > 0) {
-      const long pi = prof_open(3, s);
-      const hipError_t e = launch_merge(D, G, a, s);
-      prof_close(pi, s);
-      rc = finish(e, s);
-      if (rc != CP_OK) return rc;
-    }
-    return CP_OK;
-  } catch (...) {
-    return CP_ERR_INVALID_ARG;
-  }
+  cp_attn_plan plan;
+  const int rc = cp_attn_prepare(desc, rows, n_rows, ws, ws_bytes, stream, &plan);
+  if (rc != CP_OK) return rc;
+  return cp_attn_run(&plan, q, k_cache, v_cache, block_tables, out, ws, ws_bytes, stream);
 }
 
 int cp_profile_begin(void) {

@@ -228,7 +228,8 @@ class Model:
         self.pos_host = torch.zeros(T, dtype=torch.int32).pin_memory()
         self.pos = torch.zeros(T, dtype=torch.int32, device=self.dev)
         self.tokens = torch.randint(0, c.vocab, (T,), generator=gen, device=self.dev)
-        self.ws = torch.empty(64 << 20, dtype=torch.uint8, device=self.dev)
+        self.ws = torch.empty(64 << 20, dtype=torch.uint8, device=self.dev)      # attention plan
+        self.ws_append = torch.empty(1 << 20, dtype=torch.uint8, device=self.dev)
 
     def forward(self, rows, stream=None):
         """Runs one iteration for the batch ``rows`` [(slot, start, len, ctx)];
@@ -246,6 +247,8 @@ class Model:
         need = cp.workspace_bytes(self.desc, rows)
         if need > self.ws.numel():
             self.ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
+        if need > self.ws_append.numel():
+            self.ws_append = torch.empty(need, dtype=torch.uint8, device=self.dev)
         pos = positions_of(rows)
         self.pos_host[:T].numpy()[:] = pos
         with torch.cuda.stream(s):
@@ -254,13 +257,15 @@ class Model:
             torch.index_select(self.embed, 0, self.tokens[:T], out=x)
             qkv, q, k, v, attn = self.qkv[:T], self.q[:T], self.k[:T], self.v[:T], self.attn[:T]
             gu, act = self.gu[:T], self.act[:T]
+            # every layer attends with the same rows: plan once, run per layer
+            plan = cp.attn_prepare(self.desc, rows, self.ws, stream=s)
             for L, kc, vc in zip(self.layers, self.kc, self.vc):
                 rmsnorm(x, L["in_norm"], h, c.eps, s)
                 project(h, L["qkv"], qkv, None, s)
                 qkv_rope(qkv, L["q_norm"], L["k_norm"], self.pos, c.hq, c.hkv, c.head_dim,
                          c.theta, c.eps, q, k, v, s)
-                cp.kv_append(self.desc, k, v, kc, vc, self.bt, rows, self.ws, stream=s)
-                cp.attn_mixed(self.desc, q, kc, vc, self.bt, rows, attn, self.ws, stream=s)
+                cp.kv_append(self.desc, k, v, kc, vc, self.bt, rows, self.ws_append, stream=s)
+                cp.attn_run(plan, q, kc, vc, self.bt, attn, self.ws, stream=s)
                 project(attn.view(T, c.hq * c.head_dim), L["o"], x, x, s)
                 rmsnorm(x, L["post_norm"], h, c.eps, s)
                 project(h, L["gate_up"], gu, None, s)

@@ -186,3 +186,35 @@ def test_plan_summary_counts_consistent():
     assert s["prefill_items"] + s["decode_items"] == len(items)
     assert s["workspace_bytes"] == cp.workspace_bytes(cp.desc_for(b), b.rows)
     assert s["workspace_bytes"] >= s["partial_rows"] * (b.head_dim + 1) * 4
+
+
+def test_attn_prepare_and_run_reject_bad_input():
+    lib = binding.load()
+    plan = binding.AttnPlan()
+    bad = _desc(head_dim=96)
+    r = np.ascontiguousarray(GOOD_ROWS)
+    assert lib.cp_attn_prepare(ctypes.byref(bad), r.ctypes.data, 2, None, 0, None,
+                               ctypes.byref(plan)) == binding.CP_ERR_UNSUPPORTED
+    d = _desc()
+    assert lib.cp_attn_prepare(ctypes.byref(d), r.ctypes.data, 2, None, 0, None,
+                               None) == binding.CP_ERR_INVALID_ARG
+    # an empty batch prepares without a workspace, and its plan runs as a no-op
+    empty = np.zeros((1, 4), np.int32)
+    assert lib.cp_attn_prepare(ctypes.byref(d), empty.ctypes.data, 1, None, 0, None,
+                               ctypes.byref(plan)) == binding.CP_OK
+    assert plan.tokens == 0
+    assert lib.cp_attn_run(ctypes.byref(plan), None, None, None, None, None, None, 0,
+                           None) == binding.CP_OK
+    # a plan with work: missing buffers, a short workspace and offsets outside it are refused
+    # before anything is launched
+    plan.tokens, plan.ws_bytes, plan.n_decode = 5, 1 << 20, 1
+    assert lib.cp_attn_run(ctypes.byref(plan), None, None, None, None, None, None, 1 << 20,
+                           None) == binding.CP_ERR_INVALID_ARG
+    assert lib.cp_attn_run(ctypes.byref(plan), 256, 256, 256, 256, 256, 256, 1024,
+                           None) == binding.CP_ERR_WORKSPACE
+    plan.off_decode = 2 << 20
+    assert lib.cp_attn_run(ctypes.byref(plan), 256, 256, 256, 256, 256, 256, 1 << 20,
+                           None) == binding.CP_ERR_INVALID_ARG
+    plan.off_decode, plan.n_merge = 0, -1
+    assert lib.cp_attn_run(ctypes.byref(plan), 256, 256, 256, 256, 256, 256, 1 << 20,
+                           None) == binding.CP_ERR_INVALID_ARG

@@ -71,3 +71,36 @@ def test_single_token_chunks_and_tiny_prefill():
     rows = [(100, c) for c in (1, 2, 3, 5, 8)] + [(0, 2), (17, 3)]
     batch = make_batch("tiny-chunks", 32, 8, 128, 16, rows, rng)
     _full_check(batch, 3003, "tiny chunks")
+
+
+def test_prepared_plan_runs_match_attn_mixed_bit_for_bit():
+    # Prefill chunks long enough to be split and merged, plus decode rows with
+    # split contexts: one plan, run for two "layers" (different q and pools).
+    import paper_2606_09061_amd as cp
+    rng = np.random.default_rng(17)
+    rows = [(3000, 96), (0, 130), (8000, 1), (5000, 1), (300, 1), (12000, 40)]
+    batch = make_batch("plan", 32, 8, 128, 16, rows, rng)
+    d = cp.desc_for(batch)
+    say(f"[gpu] prepared plan: rows={batch.n_rows} T={batch.num_tokens}")
+    layers = [to_dev(make_tensors(batch, seed=s)) for s in (5101, 5102)]
+    ws_a = torch.empty(cp.workspace_bytes(d, batch.rows), dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty_like(ws_a)
+    outs_ref, outs_plan = [], []
+    for t in layers:
+        cp.kv_append(d, t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["block_tables"],
+                     batch.rows, ws_a)
+        o = torch.empty(batch.num_tokens, 32, 128, dtype=torch.bfloat16, device="cuda")
+        cp.attn_mixed(d, t["q"], t["k_cache"], t["v_cache"], t["block_tables"], batch.rows, o, ws_a)
+        outs_ref.append(o)
+    plan = cp.attn_prepare(d, batch.rows, ws_b)
+    assert plan.tokens == batch.num_tokens and plan.n_merge > 0
+    for t in layers:
+        o = torch.empty(batch.num_tokens, 32, 128, dtype=torch.bfloat16, device="cuda")
+        cp.attn_run(plan, t["q"], t["k_cache"], t["v_cache"], t["block_tables"], o, ws_b)
+        outs_plan.append(o)
+    torch.cuda.synchronize()
+    for a, b in zip(outs_ref, outs_plan):
+        assert torch.equal(a, b)
+    with pytest.raises(cp.CpError):   # a workspace smaller than the plan's
+        cp.attn_run(plan, layers[0]["q"], layers[0]["k_cache"], layers[0]["v_cache"],
+                    layers[0]["block_tables"], outs_plan[0], ws_b[:256])
