@@ -16,9 +16,9 @@
  * queries and keys before rotary embedding, SwiGLU feed-forward).
  *
  * Conventions: bf16 tensors are dense and row-major with 16-byte aligned
- * rows; arithmetic is fp32 (the rotation angle is formed and reduced to
- * [-pi, pi] in fp64 before its fp32 sine and cosine) and results are rounded
- * to bf16 (nearest even).  All pointers are device pointers owned by the
+ * rows; arithmetic is fp32 (the rotation angle is formed in turns and
+ * reduced to [-1/2, 1/2] turn in fp64 before the hardware's fp32 sine and
+ * cosine) and results are rounded to bf16 (nearest even).  All pointers are device pointers owned by the
  * caller; nothing is allocated.  Calls are asynchronous on `stream`.  Return
  * CP_OK or CP_ERR_INVALID_ARG (null pointer, misaligned buffer, size out of
  * range), CP_ERR_UNSUPPORTED (head_dim), CP_ERR_HIP (launch failure);

@@ -1,8 +1,8 @@
 // Element-wise kernels around the attention step of one decoder layer
 // (include/cp_layer.h): RMSNorm, the QKV split with per-head RMSNorm and
 // rotary embedding, and SwiGLU.  All three are bound by HBM traffic: each
-// reads its input once and writes its output once with 16-byte (or, for the
-// per-head kernel, 128-byte-per-wave) coalesced accesses.
+// reads its input once and writes its output once with 16-byte coalesced
+// accesses.
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -70,47 +70,83 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const uint4* x, const
   }
 }
 
-// One wave per (token, head) of the fused projection; lane l < D/2 owns the
-// rotation pair (l, l + D/2).  Heads [0, hq) are queries, [hq, hq + hkv) keys,
+// One wave per (token, group of 64 / (D/8) heads) of the fused projection.
+// A head is D/8 consecutive lanes of 8 elements each (16-byte loads and
+// stores); lane j < D/16 of a head holds elements of the first half and lane
+// j + D/16 their rotation partners, and the two swap their raw words with
+// one cross-lane exchange.  Heads [0, hq) are queries, [hq, hq + hkv) keys,
 // the rest values.
+template <int D>
 __global__ __launch_bounds__(kThreads) void qkv_rope_kernel(
-    const uint16_t* __restrict qkv, const uint16_t* __restrict qw, const uint16_t* __restrict kw,
-    const int32_t* __restrict positions, int n_tokens, int hq, int hkv, int D, double log2_theta,
-    float eps, uint16_t* __restrict q, uint16_t* __restrict k, uint16_t* __restrict v) {
+    const uint4* __restrict qkv, const uint4* __restrict qw, const uint4* __restrict kw,
+    const int32_t* __restrict positions, int n_tokens, int hq, int hkv, double step,
+    double step8, float eps, uint4* __restrict q, uint4* __restrict k, uint4* __restrict v) {
+  constexpr int L = D / 8, HPW = 64 / L, HALF = L / 2;
   const int nh = hq + 2 * hkv;
+  const int groups = (nh + HPW - 1) / HPW;
   const int64_t g = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  if (g >= (int64_t)n_tokens * nh) return;  // whole wave
-  const int t = (int)(g / nh), hh = (int)(g % nh), lane = threadIdx.x & 63, half = D >> 1;
-  const bool on = lane < half;
-  const uint16_t* in = qkv + ((size_t)t * nh + hh) * D;
-  const float e0 = on ? bf16_to_f32(in[lane]) : 0.f;
-  const float e1 = on ? bf16_to_f32(in[lane + half]) : 0.f;
+  if (g >= (int64_t)n_tokens * groups) return;  // whole wave
+  const int t = (int)(g / groups), h0 = (int)(g % groups) * HPW;
+  const int lane = threadIdx.x & 63, sub = lane % L, hh = h0 + lane / L;
+  const bool live = hh < nh;
+  const uint4 a = live ? qkv[((size_t)t * nh + hh) * L + sub] : make_uint4(0, 0, 0, 0);
+  if (h0 >= hq + hkv) {  // values only (wave-uniform)
+    if (live) v[((size_t)t * hkv + (hh - hq - hkv)) * L + sub] = a;
+    return;
+  }
+  uint4 b;  // the partner lane's raw words
+  b.x = __shfl_xor(a.x, HALF, 64);
+  b.y = __shfl_xor(a.y, HALF, 64);
+  b.z = __shfl_xor(a.z, HALF, 64);
+  b.w = __shfl_xor(a.w, HALF, 64);
+  float ss = sumsq8(a);
+#pragma unroll
+  for (int m = 1; m < L; m <<= 1) ss += __shfl_xor(ss, m, 64);
+  const float scale = 1.0f / sqrtf(ss / (float)D + eps);
+  if (!live) return;
   if (hh >= hq + hkv) {
-    if (on) {
-      uint16_t* o = v + ((size_t)t * hkv + (hh - hq - hkv)) * D;
-      o[lane] = in[lane];
-      o[lane + half] = in[lane + half];
-    }
+    v[((size_t)t * hkv + (hh - hq - hkv)) * L + sub] = a;
     return;
   }
   const bool is_q = hh < hq;
-  const float ss = wave_sum(e0 * e0 + e1 * e1);
-  const float scale = 1.0f / sqrtf(ss / (float)D + eps);
-  if (!on) return;
-  const uint16_t* wn = is_q ? qw : kw;
-  const float y0 = e0 * scale * bf16_to_f32(wn[lane]);
-  const float y1 = e1 * scale * bf16_to_f32(wn[lane + half]);
-  // angle = pos * theta^(-2 lane / D), formed and reduced to [-pi, pi] in
-  // double (long positions keep their fraction), then sine and cosine in fp32
-  const double inv_freq = exp2(-(2.0 * lane / D) * log2_theta);
-  const double angle = (double)positions[t] * inv_freq;
-  const double two_pi = 6.283185307179586476925286766559;
-  const float r = (float)(angle - two_pi * rint(angle * (1.0 / two_pi)));
-  float sf, cf;
-  sincosf(r, &sf, &cf);
-  uint16_t* o = is_q ? q + ((size_t)t * hq + hh) * D : k + ((size_t)t * hkv + (hh - hq)) * D;
-  o[lane] = f32_to_bf16(y0 * cf - y1 * sf);
-  o[lane + half] = f32_to_bf16(y1 * cf + y0 * sf);
+  const uint4* w = is_q ? qw : kw;
+  const uint4 wo = w[sub], wp = w[sub ^ HALF];
+  // frequency of element e in turns per position:
+  // theta^(-2 (8 (sub mod D/16) + e) / D) / (2 pi) = step8^(sub mod D/16) * step^e / (2 pi),
+  // by fp64 products; the angle is reduced to [-1/2, 1/2] turn in fp64 and its
+  // sine and cosine taken by the hardware's turn-based instructions
+  const int mlo = sub % HALF;
+  double f = 0.15915494309189533576888376337251, p = step8;
+#pragma unroll
+  for (int bit = 0; bit < 3; ++bit) {
+    if (mlo & (1 << bit)) f *= p;
+    p *= p;
+  }
+  const double pos = (double)positions[t];
+  const float sgn = sub < HALF ? -1.f : 1.f;
+  const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+  const uint32_t wow[4] = {wo.x, wo.y, wo.z, wo.w}, wpw[4] = {wp.x, wp.y, wp.z, wp.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float r2[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const double turns = pos * f;
+      f *= step;
+      const float r = (float)(turns - rint(turns));
+      const float sn = __builtin_amdgcn_sinf(r), cs = __builtin_amdgcn_cosf(r);
+      const float xo = (h ? hi(aw[i]) : lo(aw[i])) * scale * (h ? hi(wow[i]) : lo(wow[i]));
+      const float xp = (h ? hi(bw[i]) : lo(bw[i])) * scale * (h ? hi(wpw[i]) : lo(wpw[i]));
+      r2[h] = xo * cs + sgn * (xp * sn);
+    }
+    o[i] = pack(r2[0], r2[1]);
+  }
+  const uint4 out = make_uint4(o[0], o[1], o[2], o[3]);
+  if (is_q)
+    q[((size_t)t * hq + hh) * L + sub] = out;
+  else
+    k[((size_t)t * hkv + (hh - hq)) * L + sub] = out;
 }
 
 __global__ __launch_bounds__(kThreads) void swiglu_kernel(const uint4* __restrict gu,
@@ -239,14 +275,22 @@ int cpl_qkv_rope(const void* qkv, const void* q_norm_w, const void* k_norm_w,
     return CP_ERR_INVALID_ARG;
   if (n_tokens == 0) return CP_OK;
   if (!qkv || !q_norm_w || !k_norm_w || !positions || !q || !k || !v) return CP_ERR_INVALID_ARG;
-  const int64_t waves = (int64_t)n_tokens * (hq + 2 * hkv);
+  if (!aligned16(qkv) || !aligned16(q_norm_w) || !aligned16(k_norm_w) || !aligned16(q) ||
+      !aligned16(k) || !aligned16(v))
+    return CP_ERR_INVALID_ARG;
+  const int64_t hpw = 64 / (head_dim / 8);
+  const int64_t groups = (hq + 2 * hkv + hpw - 1) / hpw;
+  const int64_t waves = (int64_t)n_tokens * groups;
   const int64_t blocks = (waves + kThreads / 64 - 1) / (kThreads / 64);
   if (blocks > 0x7fffffff) return CP_ERR_INVALID_ARG;
+  // ratio of consecutive frequencies theta^(-2/D), and its eighth power
+  const double step = exp2(-2.0 / head_dim * log2(theta));
+  const double step8 = exp2(-16.0 / head_dim * log2(theta));
   (void)hipGetLastError();
-  hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)blocks), dim3(kThreads), 0,
-                     (hipStream_t)stream, (const uint16_t*)qkv, (const uint16_t*)q_norm_w,
-                     (const uint16_t*)k_norm_w, positions, n_tokens, hq, hkv, head_dim,
-                     log2(theta), eps, (uint16_t*)q, (uint16_t*)k, (uint16_t*)v);
+  auto kern = head_dim == 128 ? qkv_rope_kernel<128> : qkv_rope_kernel<64>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), 0, (hipStream_t)stream,
+                     (const uint4*)qkv, (const uint4*)q_norm_w, (const uint4*)k_norm_w, positions,
+                     n_tokens, hq, hkv, step, step8, eps, (uint4*)q, (uint4*)k, (uint4*)v);
   return launched();
 }
 

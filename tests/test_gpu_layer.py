@@ -58,7 +58,8 @@ def test_rmsnorm_in_place():
     _close(_f64(x), want)
 
 
-@pytest.mark.parametrize("T,hq,hkv,D", [(1, 4, 2, 128), (50, 32, 8, 128), (7, 8, 1, 64)])
+@pytest.mark.parametrize("T,hq,hkv,D", [(1, 4, 2, 128), (50, 32, 8, 128), (7, 8, 1, 64),
+                                        (3, 5, 3, 128), (5, 3, 2, 64)])
 def test_qkv_rope_matches_reference(T, hq, hkv, D):
     print(f"qkv_rope T={T} hq={hq} hkv={hkv} D={D}", flush=True)
     qkv = _bf16((T, (hq + 2 * hkv) * D), 5)
@@ -93,6 +94,8 @@ def test_bad_arguments_are_rejected():
     assert lib.cpl_rmsnorm(p + 2, p, p, 1, 8, 1e-6, None) != 0   # misaligned: nothing launched
     assert lib.cpl_rmsnorm(p, p, p, 1, 12, 1e-6, None) != 0      # width not a multiple of 8
     assert lib.cpl_qkv_rope(1, 1, 1, 1, 1, 1, 1, 96, 1e6, 1e-6, 1, 1, 1, None) != 0
+    y = torch.zeros(64, dtype=torch.int32, device=DEV).data_ptr()
+    assert lib.cpl_qkv_rope(p + 2, p, p, y, 1, 1, 1, 64, 1e6, 1e-6, p, p, p, None) != 0  # misaligned
     assert lib.cpl_swiglu(1, 1, 1, 12, None) != 0
 
 
