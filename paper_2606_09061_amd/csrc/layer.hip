@@ -14,6 +14,8 @@ namespace {
 
 constexpr int kThreads = 256;
 
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 __device__ __forceinline__ uint16_t f32_to_bf16(float a) {
@@ -172,22 +174,39 @@ __global__ __launch_bounds__(kThreads) void swiglu_kernel(const uint4* __restric
 // workgroup owns 32 output columns; its four waves take a quarter of K
 // each, with v_mfma_f32_32x32x16_bf16 on W rows (the 32 "m" rows) against
 // activation rows (the 32 "n" columns), then add their partial sums through
-// LDS.  Each lane's operands are 16 contiguous bytes of a W or A row.
-template <int MB>
+// LDS.
+//
+// The matrix core wants lane l to hold 16 bytes of W row l % 32, so loading
+// its operands straight from memory touches 32 rows with 32-byte pieces per
+// instruction.  Instead each wave reads a batch of U k-steps as whole
+// 32U-byte row segments (2U lanes per row, 32 / U rows per instruction) with
+// non-temporal loads, parks them in its own slice of LDS and reads its MFMA
+// operands from there: the weight stream then moves in runs of 2-4 full
+// cache lines per row, which is what lets it approach the HBM rate.  Only the
+// wave that writes a slice reads it, so no barrier is needed until the final
+// reduction.  Activations are read directly (they are small and cached).
+template <int MB, int U>
 __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint4* __restrict__ A,
                                                           const uint4* __restrict__ W,
                                                           const uint16_t* R, uint16_t* C, int M,
                                                           int N, int K) {
   typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
   typedef float f32x16_t __attribute__((ext_vector_type(16)));
-  constexpr int kRowPad = 33;  // floats per reduction row (bank spread)
-  __shared__ float red[4][32 * MB][kRowPad];
+  constexpr int kRowPad = 33;           // floats per reduction row (bank spread)
+  constexpr int kPitch = 2 * U + 1;     // uint4 per staged row (bank spread)
+  constexpr int kLanesPerRow = 2 * U, kRowsPerLoad = 64 / kLanesPerRow;
+  constexpr int kStage = 4 * 32 * kPitch * 16, kRed = 4 * 32 * MB * kRowPad * 4;
+  __shared__ __align__(16) char smem[kStage > kRed ? kStage : kRed];
+  uint4* stage = reinterpret_cast<uint4*>(smem) + (threadIdx.x >> 6) * 32 * kPitch;
+  auto red = reinterpret_cast<float(*)[32 * MB][kRowPad]>(smem);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * 32;
   const int kq = K / 4, kb = wave * kq;
   const int K8 = K / 8;  // uint4 per row
   const int lr = lane & 31, lg = lane >> 5;
-  const uint4* wrow = W + (int64_t)(n0 + lr) * K8 + (kb >> 3) + lg;
+  const int rin = lane / kLanesPerRow, col = lane % kLanesPerRow;
+  const u32x4_t* wsrc =
+      reinterpret_cast<const u32x4_t*>(W + (int64_t)(n0 + rin) * K8 + (kb >> 3) + col);
   const uint4* arow[MB];
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb)
@@ -197,27 +216,26 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint4* __restric
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[rb][r] = 0.f;
-  constexpr int U = 4;  // k-steps of 16 per batch of loads
-  uint4 wf[U], af[U][MB];
-  auto load = [&](int s) {
+  u32x4_t wr[U];  // the next batch, rows rin + kRowsPerLoad * i
+  auto load = [&](int b) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      wf[u] = wrow[(s + u) * 2];
-#pragma unroll
-      for (int rb = 0; rb < MB; ++rb) af[u][rb] = arow[rb][(s + u) * 2];
-    }
+    for (int i = 0; i < U; ++i)
+      wr[i] = __builtin_nontemporal_load(wsrc + (int64_t)kRowsPerLoad * i * K8 + b * 2 * U);
   };
-  const int steps = kq / 16;  // multiple of U
+  const int batches = kq / (16 * U);
   load(0);
-  for (int s = 0; s < steps; s += U) {
+  for (int b = 0; b < batches; ++b) {
+#pragma unroll
+    for (int i = 0; i < U; ++i)
+      stage[(kRowsPerLoad * i + rin) * kPitch + col] = make_uint4(wr[i][0], wr[i][1], wr[i][2], wr[i][3]);
     uint4 wc[U], ac[U][MB];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      wc[u] = wf[u];
+      wc[u] = stage[lr * kPitch + 2 * u + lg];
 #pragma unroll
-      for (int rb = 0; rb < MB; ++rb) ac[u][rb] = af[u][rb];
+      for (int rb = 0; rb < MB; ++rb) ac[u][rb] = arow[rb][b * 2 * U + 2 * u];
     }
-    if (s + U < steps) load(s + U);
+    if (b + 1 < batches) load(b + 1);
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -226,6 +244,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint4* __restric
             __builtin_bit_cast(bf16x8_t, wc[u]), __builtin_bit_cast(bf16x8_t, ac[u][rb]),
             acc[rb], 0, 0, 0);
   }
+  __syncthreads();  // every wave is done with its staging slice
   // D[i][j] = sum_k W[n0 + i][k] A[32 rb + j][k]: lane holds j = lane % 32,
   // register r holds i = 8 (r / 4) + 4 (lane / 32) + r % 4
 #pragma unroll
@@ -319,12 +338,18 @@ int cpl_gemm_skinny(const void* a, const void* w, const void* r, void* c, int32_
   const uint4* W = (const uint4*)w;
   const uint16_t* R = (const uint16_t*)r;
   uint16_t* C = (uint16_t*)c;
+  // batches of 8 k-steps (256-byte row segments) where each wave's quarter
+  // of K holds whole batches, else of 4
+  const bool u8 = k % 512 == 0;
+  using Kernel = void (*)(const uint4*, const uint4*, const uint16_t*, uint16_t*, int, int, int);
+  Kernel kern;
   if (m <= 32)
-    hipLaunchKernelGGL(gemm_skinny_kernel<1>, grid, block, 0, s, A, W, R, C, m, n, k);
+    kern = u8 ? gemm_skinny_kernel<1, 8> : gemm_skinny_kernel<1, 4>;
   else if (m <= 64)
-    hipLaunchKernelGGL(gemm_skinny_kernel<2>, grid, block, 0, s, A, W, R, C, m, n, k);
+    kern = u8 ? gemm_skinny_kernel<2, 8> : gemm_skinny_kernel<2, 4>;
   else
-    hipLaunchKernelGGL(gemm_skinny_kernel<4>, grid, block, 0, s, A, W, R, C, m, n, k);
+    kern = u8 ? gemm_skinny_kernel<4, 8> : gemm_skinny_kernel<4, 4>;
+  hipLaunchKernelGGL(kern, grid, block, 0, s, A, W, R, C, m, n, k);
   return launched();
 }
 

@@ -101,12 +101,21 @@ def swiglu(gu, out, stream=None):
                              _s(stream)), "cpl_swiglu")
 
 
-# Where the skinny kernel beats the library GEMM on MI355X (measured, per
-# launch): batches of at most 32 rows on projections of K <= 4096 inputs and
-# N <= 8192 outputs (QKV: 20.5 -> 17.1 us at 32 rows, 22.6 -> 11.7 us at one
-# row; O: 19.7 -> 16.9, 21.1 -> 11.4).  Larger batches re-read the
-# activations from cache for every 32-column slice and lose to the library.
-SKINNY_MAX_M, SKINNY_MAX_K, SKINNY_MAX_N = 32, 4096, 8192
+# Where the skinny kernel beats the library GEMM on MI355X.  Per launch, with
+# the weights evicted from the caches beforehand (a model iteration streams
+# 15 GB of weights): at 1-16 rows on every projection of the model (QKV
+# 24.0 -> 14.4 us, O 21.2 -> 13.9, gate/up 78.7 -> 34.1, down 39.8 -> 29.1,
+# LM head 286 -> 178 at one row) and at 32 rows where K <= 4096 (gate/up 2.0x,
+# QKV 1.23x, O 1.13x; down 0.98x).  A whole 36-layer decode iteration with
+# this dispatch against the library alone: 1.20x at 1 row, 1.15x at 8, 1.10x
+# at 16, 1.03x at 32, and 0.96x / 0.93x at 48 / 64 rows (each 32-column
+# slice re-reads the activations), hence no skinny kernel above 32 rows.
+def skinny_faster(m, n, k):
+    if n % 32 or k % 256 or m < 1:
+        return False
+    if m <= 16:
+        return True
+    return m <= 32 and k <= 4096
 
 
 def gemm_skinny(a, w, out, residual=None, stream=None):
@@ -127,8 +136,7 @@ def project(a, w, out, residual=None, stream=None):
     import torch
     M, K = a.shape
     N = w.shape[0]
-    if (M <= SKINNY_MAX_M and K <= SKINNY_MAX_K and N <= SKINNY_MAX_N and N % 32 == 0
-            and K % 256 == 0):
+    if skinny_faster(M, N, K):
         gemm_skinny(a, w, out, residual, stream)
     elif residual is None:
         torch.mm(a, w.t(), out=out)
@@ -277,7 +285,9 @@ class Model:
             last = last[rows[:, 2] > 0].to(self.dev, non_blocking=True)
             hl = torch.empty(len(last), c.hidden, dtype=torch.bfloat16, device=self.dev)
             rmsnorm(x.index_select(0, last), self.final_norm, hl, c.eps, s)
-            return torch.argmax(hl @ self.lm_head.t(), dim=-1)
+            logits = torch.empty(len(last), c.vocab, dtype=torch.bfloat16, device=self.dev)
+            project(hl, self.lm_head, logits, None, s)
+            return torch.argmax(logits, dim=-1)
 
 
 class ModelEngine:

@@ -121,3 +121,13 @@ def test_positions_of_rows():
     rows = np.array([[3, 7, 2, 9], [0, 0, 0, 0], [1, 199, 1, 200], [2, 0, 3, 3]])
     assert positions_of(rows).tolist() == [7, 8, 199, 0, 1, 2]
     assert positions_of(np.zeros((0, 4))).tolist() == []
+
+
+def test_skinny_dispatch_follows_measured_table():
+    from paper_2606_09061_amd.model import skinny_faster
+    qkv, o, gate_up, down = (6144, 4096), (4096, 4096), (24576, 4096), (4096, 12288)
+    for n, k in (qkv, o, gate_up, down):
+        assert skinny_faster(1, n, k) and skinny_faster(16, n, k)
+        assert not skinny_faster(33, n, k) and not skinny_faster(128, n, k)
+    assert skinny_faster(32, *qkv) and skinny_faster(32, *gate_up) and not skinny_faster(32, *down)
+    assert not skinny_faster(1, 1000, 256) and not skinny_faster(1, 64, 320)   # unsupported shapes
