@@ -9,9 +9,9 @@ scheduler's batch through every layer of such a model with synthetic weights:
     cpl_swiglu -> down GEMM (+ residual)] -> RMSNorm -> LM head on each row's
     last token -> argmax
 
-Projections of small batches (<= 32 tokens, QKV and O) run in this
-package's skinny GEMM kernel, the rest as library GEMMs (torch.mm / addmm,
-i.e. hipBLASLt); every other step runs in this package's HIP kernels
+Projections of small batches (up to 16 tokens, or 32 where K <= 4096) run
+in this package's skinny GEMM kernel, the rest as library GEMMs (torch.mm /
+addmm, i.e. hipBLASLt); every other step runs in this package's HIP kernels
 (libcplayer.so for the element-wise parts, libcpattn.so for append and
 attention).  Each layer has
 its own paged KV pool; all layers share one block table, whose row s maps
@@ -234,6 +234,7 @@ class Model:
         self.attn = buf(T, c.hq, D)
         self.gu, self.act = buf(T, 2 * c.inter), buf(T, c.inter)
         self.pos_host = torch.zeros(T, dtype=torch.int32).pin_memory()
+        self.pos_copied = torch.cuda.Event()   # the last upload out of pos_host is done
         self.pos = torch.zeros(T, dtype=torch.int32, device=self.dev)
         self.tokens = torch.randint(0, c.vocab, (T,), generator=gen, device=self.dev)
         self.ws = torch.empty(64 << 20, dtype=torch.uint8, device=self.dev)      # attention plan
@@ -258,9 +259,11 @@ class Model:
         if need > self.ws_append.numel():
             self.ws_append = torch.empty(need, dtype=torch.uint8, device=self.dev)
         pos = positions_of(rows)
+        self.pos_copied.synchronize()   # the previous iteration's upload has left pos_host
         self.pos_host[:T].numpy()[:] = pos
         with torch.cuda.stream(s):
             self.pos[:T].copy_(self.pos_host[:T], non_blocking=True)
+            self.pos_copied.record(s)
             x, h = self.x[:T], self.h[:T]
             torch.index_select(self.embed, 0, self.tokens[:T], out=x)
             qkv, q, k, v, attn = self.qkv[:T], self.q[:T], self.k[:T], self.v[:T], self.attn[:T]
