@@ -63,7 +63,8 @@ int cpl_swiglu(const void* gu, void* out, int32_t n_tokens, int32_t inter, void*
  * cannot stream the weights at memory speed.  1 <= M <= 128, N % 32 == 0,
  * K % 256 == 0; r may be NULL or equal to c (in-place residual add); a must
  * not alias c.  w is read once; a is re-read from cache by every 32-column
- * slice of the output. */
+ * slice of the output (16-column slices when N <= 4096, M <= 32 and
+ * K % 512 == 0, so that narrow projections occupy every CU). */
 int cpl_gemm_skinny(const void* a, const void* w, const void* r, void* c, int32_t m, int32_t n,
                     int32_t k, void* stream);
 

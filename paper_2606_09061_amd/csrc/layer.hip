@@ -263,6 +263,89 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint4* __restric
   }
 }
 
+// The same product with 16 output columns per workgroup
+// (v_mfma_f32_16x16x32_bf16), for projections whose N / 32 column slices
+// would leave CUs idle; M <= 16 * MB.  A wave's batch is 4 k-steps of 32: 16
+// rows of 256 bytes (4 rows per load instruction), staged in its LDS slice
+// as above.  Lane l holds W row l % 16, k-chunk l / 16 of each step, and
+// activation row l % 16 of the same chunk.
+template <int MB>
+__global__ __launch_bounds__(256) void gemm_skinny16_kernel(const uint4* __restrict__ A,
+                                                            const uint4* __restrict__ W,
+                                                            const uint16_t* R, uint16_t* C, int M,
+                                                            int N, int K) {
+  typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+  typedef float f32x4_t __attribute__((ext_vector_type(4)));
+  constexpr int U = 4;                 // k-steps of 32 per batch
+  constexpr int kPitch = 4 * U + 1;    // uint4 per staged row (256 bytes + pad)
+  constexpr int kRowPad = 17;          // floats per reduction row
+  constexpr int kStage = 4 * 16 * kPitch * 16, kRed = 4 * 16 * MB * kRowPad * 4;
+  __shared__ __align__(16) char smem[kStage > kRed ? kStage : kRed];
+  uint4* stage = reinterpret_cast<uint4*>(smem) + (threadIdx.x >> 6) * 16 * kPitch;
+  auto red = reinterpret_cast<float(*)[16 * MB][kRowPad]>(smem);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * 16;
+  const int kq = K / 4, kb = wave * kq;
+  const int K8 = K / 8;
+  const int lr = lane & 15, lg = lane >> 4;        // MFMA row, k-chunk
+  const int rin = lane >> 4, col = lane & 15;      // staging: row within a load, 16-byte column
+  const u32x4_t* wsrc =
+      reinterpret_cast<const u32x4_t*>(W + (int64_t)(n0 + rin) * K8 + (kb >> 3) + col);
+  const uint4* arow[MB];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+    arow[rb] = A + (int64_t)min(rb * 16 + lr, M - 1) * K8 + (kb >> 3) + lg;
+  f32x4_t acc[MB];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[rb][r] = 0.f;
+  u32x4_t wr[4];  // the next batch, rows rin + 4 i
+  auto load = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      wr[i] = __builtin_nontemporal_load(wsrc + (int64_t)4 * i * K8 + b * 4 * U);
+  };
+  const int batches = kq / (32 * U);
+  load(0);
+  for (int b = 0; b < batches; ++b) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      stage[(4 * i + rin) * kPitch + col] = make_uint4(wr[i][0], wr[i][1], wr[i][2], wr[i][3]);
+    uint4 wc[U], ac[U][MB];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      wc[u] = stage[lr * kPitch + 4 * u + lg];
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) ac[u][rb] = arow[rb][b * 4 * U + 4 * u];
+    }
+    if (b + 1 < batches) load(b + 1);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb)
+        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8_t, wc[u]), __builtin_bit_cast(bf16x8_t, ac[u][rb]),
+            acc[rb], 0, 0, 0);
+  }
+  __syncthreads();  // every wave is done with its staging slice
+  // D[i][j] = sum_k W[n0 + i][k] A[16 rb + j][k]: lane holds j = lane % 16,
+  // register r holds i = 4 (lane / 16) + r
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][rb * 16 + lr][4 * lg + r] = acc[rb][r];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 16 * MB * 16; idx += 256) {
+    const int j = idx >> 4, i = idx & 15;
+    if (j >= M) break;  // rows are visited in increasing order
+    float v = red[0][j][i] + red[1][j][i] + red[2][j][i] + red[3][j][i];
+    const int64_t o = (int64_t)j * N + n0 + i;
+    if (R) v += bf16_to_f32(R[o]);
+    C[o] = f32_to_bf16(v);
+  }
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 int launched() { return hipGetLastError() == hipSuccess ? CP_OK : CP_ERR_HIP; }
@@ -343,6 +426,13 @@ int cpl_gemm_skinny(const void* a, const void* w, const void* r, void* c, int32_
   const bool u8 = k % 512 == 0;
   using Kernel = void (*)(const uint4*, const uint4*, const uint16_t*, uint16_t*, int, int, int);
   Kernel kern;
+  // narrow projections (32-column slices would leave half the CUs idle):
+  // 16-column slices, so that every CU gets one
+  if (m <= 32 && u8 && n / 32 <= 128) {
+    kern = m <= 16 ? gemm_skinny16_kernel<1> : gemm_skinny16_kernel<2>;
+    hipLaunchKernelGGL(kern, dim3(n / 16), block, 0, s, A, W, R, C, m, n, k);
+    return launched();
+  }
   if (m <= 32)
     kern = u8 ? gemm_skinny_kernel<1, 8> : gemm_skinny_kernel<1, 4>;
   else if (m <= 64)

@@ -9,9 +9,9 @@ scheduler's batch through every layer of such a model with synthetic weights:
     cpl_swiglu -> down GEMM (+ residual)] -> RMSNorm -> LM head on each row's
     last token -> argmax
 
-Projections of small batches (up to 16 tokens, or 32 where K <= 4096) run
-in this package's skinny GEMM kernel, the rest as library GEMMs (torch.mm /
-addmm, i.e. hipBLASLt); every other step runs in this package's HIP kernels
+Projections of small batches (up to 32 tokens) run in this package's skinny
+GEMM kernel, the rest as library GEMMs (torch.mm / addmm, i.e. hipBLASLt);
+every other step runs in this package's HIP kernels
 (libcplayer.so for the element-wise parts, libcpattn.so for append and
 attention).  Each layer has
 its own paged KV pool; all layers share one block table, whose row s maps
@@ -103,19 +103,16 @@ def swiglu(gu, out, stream=None):
 
 # Where the skinny kernel beats the library GEMM on MI355X.  Per launch, with
 # the weights evicted from the caches beforehand (a model iteration streams
-# 15 GB of weights): at 1-16 rows on every projection of the model (QKV
-# 24.0 -> 14.4 us, O 21.2 -> 13.9, gate/up 78.7 -> 34.1, down 39.8 -> 29.1,
-# LM head 286 -> 178 at one row) and at 32 rows where K <= 4096 (gate/up 2.0x,
-# QKV 1.23x, O 1.13x; down 0.98x).  A whole 36-layer decode iteration with
-# this dispatch against the library alone: 1.20x at 1 row, 1.15x at 8, 1.10x
-# at 16, 1.03x at 32, and 0.96x / 0.93x at 48 / 64 rows (each 32-column
-# slice re-reads the activations), hence no skinny kernel above 32 rows.
+# 15 GB of weights), at one row: QKV 24.0 -> 14.2 us, O 21.0 -> 11.1, gate/up
+# 79.3 -> 34.0, down 40.8 -> 23.5, LM head 288 -> 178; at 32 rows still
+# 1.19-1.97x on all five.  A whole 36-layer decode iteration with this
+# dispatch against the library alone: 1.29x at 1 row, 1.23x at 8, 1.18x at
+# 16, 1.08x at 24, 1.03x at 32, even at 40 rows (each 32-column slice
+# re-reads the activations), hence no skinny kernel above 32 rows.
 def skinny_faster(m, n, k):
     if n % 32 or k % 256 or m < 1:
         return False
-    if m <= 16:
-        return True
-    return m <= 32 and k <= 4096
+    return m <= 32
 
 
 def gemm_skinny(a, w, out, residual=None, stream=None):

@@ -190,7 +190,8 @@ def test_model_forward_is_deterministic_and_finite():
 
 @pytest.mark.parametrize("M,N,K", [(1, 32, 256), (17, 96, 512), (32, 4096, 4096), (33, 64, 256),
                                    (64, 6144, 4096), (100, 4096, 12288), (128, 1024, 1024),
-                                   (70, 64, 768), (5, 160, 1280)])
+                                   (70, 64, 768), (5, 160, 1280), (9, 4096, 12288),
+                                   (1, 1024, 512)])
 @pytest.mark.parametrize("residual", [False, True])
 def test_gemm_skinny_matches_reference(M, N, K, residual):
     print(f"gemm_skinny M={M} N={N} K={K} residual={residual}", flush=True)
