@@ -53,6 +53,8 @@ GOOD_ROWS = np.array([[0, 10, 5, 15], [1, 0, 1, 1]], np.int32)
     (dict(num_q_heads=12, num_kv_heads=8), binding.CP_ERR_BAD_META),
     (dict(sm_scale=float("nan")), binding.CP_ERR_BAD_META),
     (dict(sm_scale=-1.0), binding.CP_ERR_BAD_META),
+    (dict(sm_scale=0.0), binding.CP_ERR_BAD_META),
+    (dict(sm_scale=float("inf")), binding.CP_ERR_BAD_META),
     (dict(head_dim=96), binding.CP_ERR_UNSUPPORTED),
     (dict(block_size=8), binding.CP_ERR_UNSUPPORTED),
     (dict(num_q_heads=48, num_kv_heads=3), binding.CP_ERR_UNSUPPORTED),
