@@ -181,8 +181,9 @@ __global__ __launch_bounds__(kThreads) void swiglu_kernel(const uint4* __restric
 // instruction.  Instead each wave reads a batch of U k-steps as whole
 // 32U-byte row segments (2U lanes per row, 32 / U rows per instruction) with
 // non-temporal loads, parks them in its own slice of LDS and reads its MFMA
-// operands from there: the weight stream then moves in runs of 2-4 full
-// cache lines per row, which is what lets it approach the HBM rate.  Only the
+// operands from there: the weight stream then moves in whole 128-byte
+// (U = 4) or 256-byte (U = 8) runs per row, which is what lets it approach
+// the HBM rate.  Only the
 // wave that writes a slice reads it, so no barrier is needed until the final
 // reduction.  Activations are read directly (they are small and cached).
 template <int MB, int U>
