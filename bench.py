@@ -906,6 +906,66 @@ def model_bench(reps=5, max_seqs=128, only=None):
     return out
 
 
+def per_iteration(cfg, reps=7):
+    """Prefill and decode kernel time of every batch of mix ``cfg`` (the 20
+    iterations of the replay for mix 5), measured one batch at a time with the
+    library's per-kernel events after the batches have run once in order,
+    with each batch's algorithmic work and the fractions of the peaks."""
+    import numpy as np
+    import torch
+    import paper_2606_09061_amd as cp
+    from paper_2606_09061_amd import binding
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    batches, steps, shared, _ = build_inputs(cfg, dev)
+    descs = [cp.desc_for(b) for b in batches]
+    tables = [torch.from_numpy(b.block_tables).to(dev) for b in batches]
+    ws = torch.empty(max(cp.workspace_bytes(d, b.rows) for d, b in zip(descs, batches)),
+                     dtype=torch.uint8, device=dev)
+    outs = [torch.empty(b.num_tokens, b.num_q_heads, b.head_dim, dtype=torch.bfloat16,
+                        device=dev) for b in batches]
+    s = torch.cuda.current_stream()
+
+    def step(j):
+        b, d, t = batches[j], descs[j], steps[j]
+        cp.kv_append(d, t["k_new"], t["v_new"], shared["k_cache"], shared["v_cache"], tables[j],
+                     b.rows, ws, stream=s)
+        cp.attn_mixed(d, t["q"], shared["k_cache"], shared["v_cache"], tables[j], b.rows,
+                      outs[j], ws, stream=s)
+
+    for j in range(len(batches)):       # every batch once, in order (fills the replay's pools)
+        step(j)
+    torch.cuda.synchronize()
+    times = [{"prefill": [], "decode": []} for _ in batches]
+    for rep in range(reps):
+        for j in range(len(batches)):
+            binding.profile_begin()
+            step(j)
+            torch.cuda.synchronize()
+            prof = binding.profile_end()
+            for k in ("prefill", "decode"):
+                times[j][k].append(prof[k][0] * 1e3)
+        log(f"[per-iteration] rep {rep + 1}/{reps}")
+    out = []
+    for j, b in enumerate(batches):
+        w = work_of(b)
+        pf = b.rows[b.rows[:, 2] >= 2]
+        t_pf = float(np.median(times[j]["prefill"][1:]))
+        t_dc = float(np.median(times[j]["decode"][1:]))
+        out.append({"iteration": j, "prefill_chunks": int(len(pf)),
+                    "prefill_tokens": int(pf[:, 2].sum()),
+                    "max_prior": int(pf[:, 1].max()) if len(pf) else 0,
+                    "decode_rows": int((b.rows[:, 2] == 1).sum()),
+                    "prefill_gflop": w["prefill_flops"] / 1e9, "prefill_us": t_pf,
+                    "prefill_frac_mfma": (w["prefill_flops"] / (t_pf * 1e-6) / (PEAK_BF16_TFLOPS * 1e12)
+                                          if t_pf > 0 else None),
+                    "decode_mb": w["decode_bytes"] / 1e6, "decode_us": t_dc,
+                    "decode_frac_hbm": (w["decode_bytes"] / (t_dc * 1e-6) / (PEAK_HBM_GBS * 1e9)
+                                        if t_dc > 0 else None)})
+    return {"mix": cfg, "reps": reps, "iterations": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -935,6 +995,9 @@ def main():
                     help="only time whole iterations of the synthetic Qwen3-8B stack")
     ap.add_argument("--model-case", action="append", default=None,
                     help="with --model: time only this batch (repeatable)")
+    ap.add_argument("--per-iteration", action="store_true",
+                    help="prefill / decode kernel time of every batch of --config (mix 5: its "
+                         "20 iterations) against its algorithmic work")
     ap.add_argument("--fit", default=None, metavar="CSV",
                     help="only fit a latency table written earlier (no GPU)")
     args = ap.parse_args()
@@ -953,6 +1016,9 @@ def main():
     if args.sched:
         print(json.dumps(sched_experiment(args.sched, engine=args.sched_engine,
                                           parts=tuple(args.sched_parts.split(",")))), flush=True)
+        return
+    if args.per_iteration:
+        print(json.dumps(per_iteration(args.config)), flush=True)
         return
     if args.model:
         print(json.dumps(model_bench(only=args.model_case)), flush=True)
