@@ -179,6 +179,8 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::max(1, atoi(s));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_ROWS"))
     t.prefill_wide_min_rows = std::max<int64_t>(1, atoll(s));
+  if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_KEYS"))
+    t.prefill_wide_min_keys = std::max<int64_t>(0, atoll(s));
   return t;
 }
 
@@ -285,10 +287,22 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   auto& chunks = sc.chunks;
   tiles.clear();
   chunks.clear();
+  // 256-row tiles halve the K/V reads per flop but leave a CU one workgroup,
+  // whose start-up and drain nothing overlaps: they pay only when the step's
+  // queries see long key ranges (token-weighted mean of chunk_start + len / 2).
+  // The choice is per step, so that all prefill tiles share one launch.
+  double pf_tok = 0, pf_keys = 0;
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len < t.prefill_min_len) continue;
-    const bool wide = (int64_t)m.chunk_len * G >= t.prefill_wide_min_rows;
+    pf_tok += m.chunk_len;
+    pf_keys += (double)m.chunk_len * ((double)m.chunk_start + 0.5 * m.chunk_len);
+  }
+  const bool long_keys = pf_tok > 0 && pf_keys >= (double)t.prefill_wide_min_keys * pf_tok;
+  for (int32_t r = 0; r < n_rows; ++r) {
+    const cp_row_meta& m = rows[r];
+    if (m.chunk_len < t.prefill_min_len) continue;
+    const bool wide = long_keys && (int64_t)m.chunk_len * G >= t.prefill_wide_min_rows;
     const int32_t tt = wide ? kPrefillRowsWide / G : tile_tok;
     detail::Chunk ch{(int32_t)tiles.size(), 0, 0, wide};
     for (int32_t j = 0; j < m.chunk_len; j += tt) {

@@ -79,7 +79,8 @@ struct Tuning {
   int prefill_min_split = 8;    // shortest prefill split, in kPrefillKeys steps
   int num_cus = 256;
   int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
-  int64_t prefill_wide_min_rows = 129;  // chunks with chunk_len * G >= this use 256-row tiles
+  int64_t prefill_wide_min_rows = 129;  // chunks with chunk_len * G >= this use 256-row tiles,
+  int64_t prefill_wide_min_keys = 1200; // ... when the step's mean key range per query is this
 };
 
 namespace detail {
