@@ -220,3 +220,18 @@ def test_attn_prepare_and_run_reject_bad_input():
     plan.off_decode, plan.n_merge = 0, -1
     assert lib.cp_attn_run(ctypes.byref(plan), 256, 256, 256, 256, 256, 256, 1 << 20,
                            None) == binding.CP_ERR_INVALID_ARG
+
+
+def test_prefill_tile_width_follows_the_step_key_range():
+    # 32/8 heads: a 256-row tile holds 64 tokens, a 128-row tile 32
+    d = _desc(num_blocks=4096, max_blocks_per_req=600, num_reqs_in_table=4)
+
+    def widest(rows):
+        items = cp.plan_items(d, np.array(rows, np.int32))
+        return int(items[items[:, 0] == 0][:, 2].max())
+
+    assert widest([[0, 0, 256, 256]]) == 32                 # mean key range 128: 128-row tiles
+    assert widest([[0, 8192, 256, 8448]]) == 64             # 8,320: 256-row tiles
+    # one width for the whole step: its token-weighted mean decides (here 4,224)
+    assert widest([[0, 0, 256, 256], [1, 8192, 256, 8448]]) == 64
+    assert widest([[0, 0, 2000, 2000], [1, 1200, 8, 1208]]) == 32   # (2000*1000 + 8*1204)/2008
