@@ -34,7 +34,9 @@
  * read or written only during the call.
  *
  * Errors: functions return CPS_OK (0) or a negative CPS_ERR_* code; a call
- * that fails changes no scheduler state.  No C++ exception crosses the ABI.
+ * that fails changes no scheduler state, except CPS_ERR_NO_MEMORY from
+ * cps_schedule, after which the scheduler may only be destroyed.  No C++
+ * exception crosses the ABI.
  */
 #ifndef CP_SCHED_H
 #define CP_SCHED_H
@@ -53,6 +55,7 @@ extern "C" {
 #define CPS_ERR_NO_PREDICTOR (-3) /* LPRS selected but no predictor loaded    */
 #define CPS_ERR_STATE (-4)       /* call out of order (complete before schedule,
                                     duplicate request id)                     */
+#define CPS_ERR_NO_MEMORY (-5)   /* a host allocation failed                  */
 
 #define CPS_POLICY_FCFS 0        /* prefills in arrival order                 */
 #define CPS_POLICY_AGING 1       /* max-heap on K_i = -alpha*a_i + beta*r_i   */

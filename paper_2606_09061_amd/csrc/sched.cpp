@@ -255,6 +255,23 @@ int32_t select_chunk(const cps_config& cfg, const Mlp& mlp, const double* mem,
   return c_star;
 }
 
+// Runs an entry point's body; a failed host allocation becomes an error code
+// instead of an exception crossing the C ABI.
+template <class F>
+int guarded(F&& body) {
+  try {
+    return body();
+  } catch (...) {
+    return CPS_ERR_NO_MEMORY;
+  }
+}
+
+// Room for `extra` more elements without a reallocation later (amortised growth).
+template <class V>
+void make_room(V& v, size_t extra) {
+  if (v.capacity() - v.size() < extra) v.reserve(std::max(v.size() + extra, 2 * v.capacity()));
+}
+
 }  // namespace
 
 struct cps_sched {
@@ -316,13 +333,19 @@ cps_sched* cps_create(const cps_config* cfg, int* err) {
     *err = CPS_ERR_INVALID_ARG;
     return nullptr;
   }
-  cps_sched* s = new (std::nothrow) cps_sched();
-  if (!s) {
-    *err = CPS_ERR_CAPACITY;
+  cps_sched* s = nullptr;
+  const int rc = guarded([&] {
+    s = new cps_sched();
+    s->cfg = *cfg;
+    s->free_slots.reserve(cfg->max_seqs);
+    for (int32_t i = cfg->max_seqs - 1; i >= 0; --i) s->free_slots.push_back(i);
+    return CPS_OK;
+  });
+  if (rc != CPS_OK) {
+    delete s;
+    *err = rc;
     return nullptr;
   }
-  s->cfg = *cfg;
-  for (int32_t i = cfg->max_seqs - 1; i >= 0; --i) s->free_slots.push_back(i);
   *err = CPS_OK;
   return s;
 }
@@ -344,6 +367,7 @@ int cps_set_predictor(cps_sched* s, int32_t n_layers, const int32_t* dims, const
   }
   for (int k = 0; k < NF; ++k)
     if (!(x_std[k] > 0.0) || !std::isfinite(x_mean[k])) return CPS_ERR_INVALID_ARG;
+  return guarded([&] {
   Mlp m;
   m.dims.assign(dims, dims + n_layers + 1);
   m.wt.resize(nw);
@@ -358,6 +382,7 @@ int cps_set_predictor(cps_sched* s, int32_t n_layers, const int32_t* dims, const
   m.y_scale = y_scale;
   s->mlp = std::move(m);
   return CPS_OK;
+  });
 }
 
 int cps_set_memory_state(cps_sched* s, const double mem_mb[4]) {
@@ -374,17 +399,22 @@ int cps_add_request(cps_sched* s, int64_t id, double arrival, int32_t prompt_len
       (int64_t)prompt_len + max_new_tokens > s->cfg.max_seq_len)
     return CPS_ERR_INVALID_ARG;
   if (s->by_id.count(id)) return CPS_ERR_STATE;
-  Request r;
-  r.id = id;
-  r.arrival = arrival;
-  r.prompt_len = prompt_len;
-  r.max_new = max_new_tokens;
-  r.remaining = prompt_len;
-  const int32_t idx = (int32_t)s->reqs.size();
-  s->reqs.push_back(r);
-  s->by_id.emplace(id, idx);
-  s->push(idx);
-  return CPS_OK;
+  return guarded([&] {
+    // every allocation happens before the first change of state
+    make_room(s->reqs, 1);
+    make_room(s->heap, 1);
+    const int32_t idx = (int32_t)s->reqs.size();
+    s->by_id.emplace(id, idx);
+    Request r;
+    r.id = id;
+    r.arrival = arrival;
+    r.prompt_len = prompt_len;
+    r.max_new = max_new_tokens;
+    r.remaining = prompt_len;
+    s->reqs.push_back(r);
+    s->push(idx);
+    return CPS_OK;
+  });
 }
 
 int cps_schedule(cps_sched* s, double now, cp_row_meta* rows, int64_t* ids, int32_t cap,
@@ -396,7 +426,10 @@ int cps_schedule(cps_sched* s, double now, cp_row_meta* rows, int64_t* ids, int3
   // Every row holds a distinct slot, so max_seqs rows always fit.
   if (cap < std::min<int64_t>(s->cfg.max_seqs, (int64_t)s->decoding.size() + (int64_t)s->heap.size()))
     return CPS_ERR_CAPACITY;
+  return guarded([&] {
   const cps_config& cfg = s->cfg;
+  make_room(s->batch_idx, (size_t)cap);
+  make_room(s->batch_len, (size_t)cap);
   int32_t n = 0;
   int64_t u = 0;
   s->batch_idx.clear();
@@ -417,6 +450,7 @@ int cps_schedule(cps_sched* s, double now, cp_row_meta* rows, int64_t* ids, int3
   int32_t n_active = 0;
   s->scratch.forget();
   std::vector<int32_t> popped;
+  popped.reserve(s->heap.size());
   while (!s->heap.empty() && u < cfg.max_tokens && n < cap) {
     if (cfg.apc && n_active > 0 && n_active >= activity_cap(cfg, n_decode, u)) {
       s->stats.apc_not_scored += (int64_t)s->heap.size();
@@ -471,14 +505,19 @@ int cps_schedule(cps_sched* s, double now, cp_row_meta* rows, int64_t* ids, int3
   *n_rows = n;
   *n_decode_out = n_decode;
   return CPS_OK;
+  });
 }
 
 int cps_complete(cps_sched* s, double now) {
   if (!s || !std::isfinite(now)) return CPS_ERR_INVALID_ARG;
   if (!s->pending_batch) return CPS_ERR_STATE;
+  return guarded([&] {
+  // every allocation happens before the first change of state
   std::vector<int32_t> still;
-  still.reserve(s->decoding.size());
+  still.reserve(s->decoding.size() + s->batch_idx.size());
   std::vector<char> done(s->reqs.size(), 0);
+  make_room(s->decoding, s->batch_idx.size());
+  make_room(s->free_slots, s->batch_idx.size());
   for (size_t k = 0; k < s->batch_idx.size(); ++k) {
     Request& r = s->reqs[s->batch_idx[k]];
     if (r.processed < r.prompt_len) {  // a prefill chunk
@@ -509,6 +548,7 @@ int cps_complete(cps_sched* s, double now) {
   std::sort(s->free_slots.begin(), s->free_slots.end(), std::greater<int32_t>());
   s->pending_batch = false;
   return CPS_OK;
+  });
 }
 
 int cps_get_stats(const cps_sched* s, cps_stats* out) {
@@ -535,15 +575,19 @@ int64_t cps_pending(const cps_sched* s) {
 int cps_batch_features(const cp_row_meta* rows, int32_t n_rows, const double mem_mb[4],
                        double* out) {
   if ((!rows && n_rows > 0) || n_rows < 0 || !mem_mb || !out) return CPS_ERR_INVALID_ARG;
-  features(rows, n_rows, mem_mb, out);
-  return CPS_OK;
+  return guarded([&] {
+    features(rows, n_rows, mem_mb, out);
+    return CPS_OK;
+  });
 }
 
 int cps_predict(const cps_sched* s, const double* x, int32_t n, double* out) {
   if (!s || (!x && n > 0) || (!out && n > 0) || n < 0) return CPS_ERR_INVALID_ARG;
   if (!s->mlp.loaded()) return CPS_ERR_NO_PREDICTOR;
-  s->mlp.forward(x, n, out);
-  return CPS_OK;
+  return guarded([&] {
+    s->mlp.forward(x, n, out);
+    return CPS_OK;
+  });
 }
 
 int cps_select_chunk(const cps_sched* s, const cp_row_meta* committed, int32_t n_committed,
@@ -554,11 +598,13 @@ int cps_select_chunk(const cps_sched* s, const cp_row_meta* committed, int32_t n
     return CPS_ERR_INVALID_ARG;
   if (!s->mlp.loaded()) return CPS_ERR_NO_PREDICTOR;
   // Own scratch and counter: the scheduler's state is left unchanged.
-  SelectScratch sc;
-  int64_t scored = 0;
-  *chunk = select_chunk(s->cfg, s->mlp, s->mem, committed, n_committed, slot, processed,
-                        remaining, sc, predicted, &scored);
-  return CPS_OK;
+  return guarded([&] {
+    SelectScratch sc;
+    int64_t scored = 0;
+    *chunk = select_chunk(s->cfg, s->mlp, s->mem, committed, n_committed, slot, processed,
+                          remaining, sc, predicted, &scored);
+    return CPS_OK;
+  });
 }
 
 int cps_apc_decide(const cps_config* cfg, int32_t c_star, int32_t h, int32_t remaining,

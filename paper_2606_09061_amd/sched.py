@@ -29,7 +29,7 @@ POLICY_FCFS, POLICY_AGING = 0, 1
 CHUNK_TOKEN_BUDGET, CHUNK_LPRS = 0, 1
 APC_REASONS = ("accepted", "warm_start", "blocked_cap", "blocked_min_chunk")
 _ERRORS = {-1: "invalid argument", -2: "capacity", -3: "no predictor loaded",
-           -4: "call out of order"}
+           -4: "call out of order", -5: "host allocation failed"}
 
 
 class SchedError(RuntimeError):
