@@ -3,9 +3,10 @@
 
 A step is cp_kv_append + cp_attn_mixed over one batch of synthetic input (the
 whole hot path: planner, append, prefill-MFMA, decode split-K, merge).  With
-no flags it runs the Llama-3-8B-shaped mix with a 512-token budget (32 q / 8
-kv heads, head_dim 128, block 16; 2 prefill chunks of 192 tokens + 128
-decode rows) on one GPU and prints one JSON line.
+no flags it runs the 70B-shaped mix (64 q / 8 kv heads, head_dim 128, block
+32, token budget 4096): a 20-iteration replay of an aging/APC schedule over
+64 requests, one iteration per step, cycling, on one GPU, and prints one JSON
+line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--config N] [--all]
                   [--sub prefill|decode] [--cold N] [--no-cpu]
@@ -13,8 +14,8 @@ decode rows) on one GPU and prints one JSON line.
   python bench.py --latency-table out.csv
   python bench.py --fit out.csv
 
-``--config 5`` replays the 20-iteration 70B-shaped schedule (a step is one
-iteration, iterations cycle).  ``--all`` prints one line per mix.  ``--sub``
+``--config N`` picks another mix (1 tiny, 2 Llama-3-8B budget 512, 3 prefill-
+heavy, 4 decode-dominated).  ``--all`` prints one line per mix.  ``--sub``
 times only the prefill rows or only the decode rows of the mix (same pools);
 ``--cold`` adds steps timed after flushing the caches.
 """
@@ -100,30 +101,56 @@ def traffic_for(kernel, workload):
 
 # --------------------------------------------------------------------------- cpu baseline
 
-def cpu_baseline(batches, host_caches, tensors_host, budget_s=10.0, seed=0):
-    """The fp64 oracle on a uniform random sample of (token, q head) outputs of
-    the first batch, timed on all host cores; tokens/s scaled from the sample."""
+def cpu_baseline(batches, pools0, steps_host, budget_s=10.0, seed=0):
+    """The fp64 oracle timed on all host cores over a uniform random sample of
+    the (token, q head) outputs of every batch, in order.  Each batch's pools
+    are rebuilt on the host by the oracle's own append, batch after batch, in
+    ``pools0`` (written in place), so every sampled output reads the context
+    it reads on the GPU.
+    Each output is drawn with one probability f, chosen from a pilot so that
+    the timed work is about ``budget_s``; only the attention calls are timed
+    (the append is a bit copy, under 0.1 % of the oracle's work).  Tokens/s is
+    sampled outputs / Hq over the timed seconds."""
     import numpy as np
     import oracle
 
-    batch = batches[0]
-    kc0, vc0 = host_caches
-    kc, vc = oracle.kv_append(batch, tensors_host["k_new"], tensors_host["v_new"], kc0, vc0)
-    total = batch.num_tokens * batch.num_q_heads
     rng = np.random.default_rng(seed)
-    pilot = rng.choice(total, size=min(total, 64), replace=False)
-    t0 = time.perf_counter()
-    oracle.attn(batch, tensors_host["q"], kc, vc, sel=pilot)
-    per = (time.perf_counter() - t0) / len(pilot)
-    n = int(min(total, max(len(pilot), budget_s / max(per, 1e-9))))
-    sel = rng.choice(total, size=n, replace=False)
-    t0 = time.perf_counter()
-    oracle.attn(batch, tensors_host["q"], kc, vc, sel=sel)
-    dt = time.perf_counter() - t0
-    tok = n / batch.num_q_heads
-    return {"value": tok / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{n} of {total} (token, q head) outputs drawn uniformly "
-                      f"({100.0 * n / total:.1f}%), fp64, {dt:.2f} s"}
+    Hq = batches[0].num_q_heads
+
+    def keys_per_output(b):  # keys each (token, head) output reads, flat t*Hq+h order
+        pos = np.concatenate([np.arange(s_, s_ + c_) for _, s_, c_, _ in b.rows.tolist()] or
+                             [np.zeros(0, np.int64)])
+        return np.repeat(pos + 1, Hq)
+
+    total_keys = sum(int(keys_per_output(b).sum()) for b in batches)
+    kc, vc = pools0
+    f, timed, n_out, n_all = None, 0.0, 0, 0
+    for i, b in enumerate(batches):
+        kc, vc = oracle.kv_append(b, steps_host[i]["k_new"], steps_host[i]["v_new"], kc, vc,
+                                  inplace=True)
+        kpo = keys_per_output(b)
+        n_all += kpo.size
+        if kpo.size == 0:
+            continue
+        if f is None:  # pilot: seconds per key read, on the first batch
+            pilot = rng.choice(kpo.size, size=min(kpo.size, 64), replace=False)
+            t0 = time.perf_counter()
+            oracle.attn(b, steps_host[i]["q"], kc, vc, sel=pilot)
+            per_key = (time.perf_counter() - t0) / max(1, int(kpo[pilot].sum()))
+            f = min(1.0, budget_s / max(per_key * total_keys, 1e-9))
+        sel = np.nonzero(rng.random(kpo.size) < f)[0]
+        if sel.size == 0:
+            continue
+        t0 = time.perf_counter()
+        oracle.attn(b, steps_host[i]["q"], kc, vc, sel=sel)
+        timed += time.perf_counter() - t0
+        n_out += sel.size
+    tok = n_out / Hq
+    return {"value": tok / timed if timed > 0 else None, "unit": "tokens/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{n_out} of {n_all} (token, q head) outputs over all {len(batches)} "
+                      f"batch(es), each drawn with probability {f:.4f}, fp64 attention only, "
+                      f"{timed:.2f} s"}
 
 
 # --------------------------------------------------------------------------- gpu run
@@ -202,10 +229,19 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
                                       dtype=torch.bfloat16, device=dev), ws, stream=stream)
     torch.cuda.synchronize()
     host = None
-    if with_cpu:  # the pools as the first timed step finds them, for the oracle
-        host = ((shared["k_cache"].cpu().view(torch.int16).numpy().view(np.uint16),
-                 shared["v_cache"].cpu().view(torch.int16).numpy().view(np.uint16)),
-                {k: v.cpu() for k, v in steps[0].items()})
+    if with_cpu and sub is None:
+        if prime:
+            # the replay starts from empty (all-NaN) pools; the oracle rebuilds
+            # each iteration's pools from them with the iterations' own K/V
+            shape_k, shape_v = shared["k_cache"].shape, shared["v_cache"].shape
+            pools0 = (np.full(tuple(shape_k), 0x7FC0, np.uint16),
+                      np.full(tuple(shape_v), 0x7FC0, np.uint16))
+            host = ([b for b, _ in prime], pools0,
+                    [{k: v.cpu() for k, v in t.items()} for _, t in prime])
+        else:  # the pools as the first timed step finds them
+            host = (batches, (shared["k_cache"].cpu().view(torch.int16).numpy().view(np.uint16),
+                              shared["v_cache"].cpu().view(torch.int16).numpy().view(np.uint16)),
+                    [{k: v.cpu() for k, v in steps[0].items()}])
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
@@ -330,15 +366,15 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
                                   "p10": float(np.percentile(cold_ms, 10)),
                                   "p90": float(np.percentile(cold_ms, 90)), "reps": cold}
         del flush
-    if with_cpu:
+    if host is not None:
         log("[bench] timing the fp64 oracle on a host sample")
-        res["cpu_baseline"] = cpu_baseline([batches[0]], host[0], host[1], budget_s=cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(host[0], host[1], host[2], budget_s=cpu_budget)
         if cfg in (1, 2):
             import oracle
             n_all = oracle.num_threads()
             oracle.set_threads(1)
             try:
-                res["cpu_baseline_1thread"] = cpu_baseline([batches[0]], host[0], host[1],
+                res["cpu_baseline_1thread"] = cpu_baseline(host[0], host[1], host[2],
                                                            budget_s=cpu_budget / 3)
             finally:
                 oracle.set_threads(n_all)
@@ -969,9 +1005,9 @@ def per_iteration(cfg, reps=7):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--all", action="store_true", help="one JSON line per mix")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)

@@ -47,8 +47,13 @@
  * Errors: functions return CP_OK (0) or a negative CP_ERR_* code.  All
  * validation happens before anything is enqueued: a call that fails enqueues
  * no work and writes nothing.  No C++ exception crosses this interface.
- * Block-table entries live on the device and are not inspected on the host;
- * entries a batch reads must be in [0, num_blocks).
+ * Block-table entries live on the device and are normally not inspected on
+ * the host; entries a batch reads must be in [0, num_blocks).  With the
+ * environment variable CP_DEBUG=1, cp_kv_append and cp_attn_mixed first wait
+ * for the stream, copy the entries the batch reads to the host, check them
+ * (cp_check_block_tables) and return CP_ERR_BAD_META without enqueueing
+ * anything if one is out of range; every launch is then followed by a stream
+ * synchronisation so a kernel error surfaces at the call that caused it.
  *
  * Asynchrony: both compute calls are asynchronous on `stream` (a hipStream_t;
  * NULL is the legacy default stream).  cp_attn_mixed reads only the caches:
@@ -105,6 +110,15 @@ int cp_version(void);
 /* Static string for a CP_* code ("unknown error" for anything else). */
 const char *cp_strerror(int code);
 
+/* Host-only check of the block-table entries a batch reads: for every row,
+ * entries [0, ceil(ctx_len / block_size)) of row req_id of block_tables_host
+ * (a host copy of the int32 [num_reqs_in_table][max_blocks_per_req] table)
+ * must lie in [0, num_blocks).  Returns CP_OK, the code cp_check_batch would
+ * return for desc/rows, CP_ERR_INVALID_ARG for a null table, or
+ * CP_ERR_BAD_META for an entry out of range.  Reads nothing else. */
+int cp_check_block_tables(const cp_attn_desc *desc, const int32_t *block_tables_host,
+                          const cp_row_meta *rows, int32_t n_rows);
+
 /* Workspace bytes cp_attn_mixed and cp_kv_append need for this batch, or 0 if
  * desc/rows are invalid (call cp_check_batch for the reason).  Depends only
  * on desc and the rows' metadata, never on tensor contents. */
@@ -125,9 +139,12 @@ int cp_kv_append(const cp_attn_desc *desc, const void *k_new, const void *v_new,
 
 /* Mixed prefill/decode causal attention over the paged cache (definition in
  * the file header).  Writes out[T][Hq][D]; reads q, the caches and the
- * tables.  Rows with chunk_len >= 2 run on the bf16-MFMA chunk kernel, one-
- * token rows on the split-K decode kernel; long key ranges are split and
- * merged by a log-sum-exp pass. */
+ * tables.  Rows with chunk_len >= L run on the bf16-MFMA chunk kernel, and
+ * shorter rows on the split-K decode kernel, one query token at a time, each
+ * over keys [0, its position]; L is 2 unless the environment variable
+ * CP_PREFILL_MIN_LEN sets it (clamped to [2, 64], read on every call; every
+ * value gives the same definition).  Long key ranges are split and merged by
+ * a log-sum-exp pass. */
 int cp_attn_mixed(const cp_attn_desc *desc, const void *q, const void *k_cache,
                   const void *v_cache, const int32_t *block_tables, const cp_row_meta *rows,
                   int32_t n_rows, void *out, void *ws, size_t ws_bytes, void *stream);
@@ -145,6 +162,8 @@ typedef struct {
     int32_t n_prefill_slots, n_prefill_wide_slots, n_decode, n_merge;
     int64_t off_prefill, off_prefill_slots, off_prefill_wide, off_prefill_wide_slots;
     int64_t off_decode, off_merge, off_part_o, off_part_lse;  /* byte offsets in ws */
+    int32_t n_prefill_items, n_prefill_wide_items;  /* items the slots index   */
+    int64_t partial_rows;         /* fp32 partial rows of split key ranges    */
 } cp_attn_plan;
 
 /* Validates the batch, plans it and uploads the plan into ws (asynchronous on
@@ -156,7 +175,10 @@ int cp_attn_prepare(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n
 /* cp_attn_mixed for a prepared batch: the same kernels on the same plan, so
  * the output equals cp_attn_mixed's bit for bit.  ws must be the workspace
  * the plan was prepared in (ws_bytes >= plan->ws_bytes); stream order must put
- * the prepare before the run. */
+ * the prepare before the run.  Every list the plan names (its offset plus
+ * its length times the item size) must lie inside plan->ws_bytes, else
+ * CP_ERR_INVALID_ARG and nothing is enqueued; the kernels skip any prefill
+ * slot that does not index an item of the plan. */
 int cp_attn_run(const cp_attn_plan *plan, const void *q, const void *k_cache,
                 const void *v_cache, const int32_t *block_tables, void *out, void *ws,
                 size_t ws_bytes, void *stream);

@@ -75,11 +75,19 @@ def _ptr(a):
     return a.ctypes.data_as(ctypes.c_void_p)
 
 
-def kv_append(batch, k_new, v_new, k_cache, v_cache, lib=None):
-    """Returns new (k_cache, v_cache) uint16 arrays with the step's tokens written."""
+def kv_append(batch, k_new, v_new, k_cache, v_cache, lib=None, inplace=False):
+    """Returns (k_cache, v_cache) uint16 arrays with the step's tokens written:
+    new copies, or with ``inplace`` the given C-contiguous uint16 numpy arrays
+    themselves (no copy of the pools)."""
     lib = lib or load()
     kn, vn = _u16(k_new), _u16(v_new)
-    kc, vc = _u16(k_cache).copy(), _u16(v_cache).copy()
+    if inplace:
+        for a in (k_cache, v_cache):
+            if not (isinstance(a, np.ndarray) and a.dtype == np.uint16 and a.flags.c_contiguous):
+                raise TypeError("inplace append needs C-contiguous uint16 numpy pools")
+        kc, vc = k_cache, v_cache
+    else:
+        kc, vc = _u16(k_cache).copy(), _u16(v_cache).copy()
     bt = np.ascontiguousarray(batch.block_tables, dtype=np.int32)
     rows = np.ascontiguousarray(batch.rows, dtype=np.int32)
     rc = lib.oracle_kv_append(batch.num_kv_heads, batch.head_dim, batch.block_size,

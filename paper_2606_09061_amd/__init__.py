@@ -3,8 +3,9 @@
 The HIP library (libcpattn.so, built from csrc/ for gfx950) holds the whole
 path: the varlen planner, the paged KV append, the bf16-MFMA prefill-chunk
 kernel, the split-K decode kernel and the merge pass.  ``binding`` is the
-ctypes layer over its C ABI (include/cp_attn.h); ``step`` drives one
-scheduling iteration's attention step on torch tensors.
+ctypes layer over its C ABI (include/cp_attn.h), re-exported here; the
+scheduler (``sched``, ``lprs``, ``serve``) and the decoder layer around the
+step (``model``) sit on top of it.
 """
 
 from .binding import (  # noqa: F401
@@ -15,6 +16,7 @@ from .binding import (  # noqa: F401
     attn_prepare,
     attn_run,
     check_batch,
+    check_block_tables,
     desc_for,
     kv_append,
     make_desc,

@@ -53,7 +53,9 @@ class AttnPlan(ctypes.Structure):
                 ("n_decode", ctypes.c_int32), ("n_merge", ctypes.c_int32)] + [
         (n, ctypes.c_int64) for n in ("off_prefill", "off_prefill_slots", "off_prefill_wide",
                                       "off_prefill_wide_slots", "off_decode", "off_merge",
-                                      "off_part_o", "off_part_lse")]
+                                      "off_part_o", "off_part_lse")] + [
+        ("n_prefill_items", ctypes.c_int32), ("n_prefill_wide_items", ctypes.c_int32),
+        ("partial_rows", ctypes.c_int64)]
 
 
 _lib = None
@@ -75,6 +77,8 @@ def load():
     lib.cp_strerror.argtypes, lib.cp_strerror.restype = [ctypes.c_int], ctypes.c_char_p
     lib.cp_workspace_bytes.argtypes, lib.cp_workspace_bytes.restype = [dp, vp, i32], sz
     lib.cp_check_batch.argtypes, lib.cp_check_batch.restype = [dp, vp, i32], ctypes.c_int
+    lib.cp_check_block_tables.argtypes = [dp, vp, vp, i32]
+    lib.cp_check_block_tables.restype = ctypes.c_int
     lib.cp_kv_append.argtypes = [dp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
     lib.cp_kv_append.restype = ctypes.c_int
     lib.cp_attn_mixed.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp, sz, vp]
@@ -94,7 +98,8 @@ def load():
 
 
 def exported_symbols():
-    return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch", "cp_kv_append",
+    return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch",
+            "cp_check_block_tables", "cp_kv_append",
             "cp_attn_mixed", "cp_attn_prepare", "cp_attn_run", "cp_plan_summary", "cp_plan_items",
             "cp_profile_begin", "cp_profile_end"]
 
@@ -149,6 +154,14 @@ def _stream(stream):
 def check_batch(desc: Desc, rows) -> int:
     r = _rows(rows)
     return load().cp_check_batch(ctypes.byref(desc), r.ctypes.data, r.shape[0])
+
+
+def check_block_tables(desc: Desc, block_tables_host, rows) -> int:
+    """cp_check_block_tables on a host copy of the table (numpy int32)."""
+    r = _rows(rows)
+    bt = np.ascontiguousarray(block_tables_host, dtype=np.int32)
+    return load().cp_check_block_tables(ctypes.byref(desc), bt.ctypes.data, r.ctypes.data,
+                                        r.shape[0])
 
 
 def workspace_bytes(desc: Desc, rows) -> int:

@@ -45,12 +45,41 @@ int num_cus_setting() {
   return n;
 }
 
-bool debug_sync() {
-  static const bool on = [] {
-    const char* s = std::getenv("CP_DEBUG");
-    return s && s[0] == '1';
-  }();
-  return on;
+// CP_DEBUG=1: check block-table entries on the host before enqueueing and
+// synchronise after every launch (read on every call).
+bool debug_mode() {
+  const char* s = std::getenv("CP_DEBUG");
+  return s && s[0] == '1';
+}
+
+int check_tables_host(const cp_attn_desc* d, const int32_t* bt, const cp_row_meta* rows,
+                      int32_t n_rows) {
+  const int64_t mbr = d->max_blocks_per_req;
+  for (int32_t r = 0; r < n_rows; ++r) {
+    const int64_t nb = ((int64_t)rows[r].ctx_len + d->block_size - 1) / d->block_size;
+    const int32_t* e = bt + (int64_t)rows[r].req_id * mbr;
+    for (int64_t i = 0; i < nb; ++i)
+      if (e[i] < 0 || e[i] >= d->num_blocks) return CP_ERR_BAD_META;
+  }
+  return CP_OK;
+}
+
+// Debug path: waits for the stream (earlier work may still write the table),
+// copies the entries the batch reads to the host and checks them.
+int debug_check_tables(const cp_attn_desc* d, const int32_t* bt_dev, const cp_row_meta* rows,
+                       int32_t n_rows, hipStream_t s) {
+  if (hipStreamSynchronize(s) != hipSuccess) return CP_ERR_HIP;
+  const int64_t mbr = d->max_blocks_per_req;
+  std::vector<int32_t> host((size_t)d->num_reqs_in_table * mbr, 0);
+  for (int32_t r = 0; r < n_rows; ++r) {
+    const int64_t nb = ((int64_t)rows[r].ctx_len + d->block_size - 1) / d->block_size;
+    if (nb == 0) continue;
+    const int64_t off = (int64_t)rows[r].req_id * mbr;
+    if (hipMemcpy(host.data() + off, bt_dev + off, (size_t)nb * sizeof(int32_t),
+                  hipMemcpyDefault) != hipSuccess)
+      return CP_ERR_HIP;
+  }
+  return check_tables_host(d, host.data(), rows, n_rows);
 }
 
 // Requires g_mu held.
@@ -137,7 +166,7 @@ void prof_close(long idx, hipStream_t s) {
 
 int finish(hipError_t e, hipStream_t s) {
   if (e != hipSuccess) return CP_ERR_HIP;
-  if (debug_sync()) {
+  if (debug_mode()) {
     if (hipStreamSynchronize(s) != hipSuccess) return CP_ERR_HIP;
     if (hipGetLastError() != hipSuccess) return CP_ERR_HIP;
   }
@@ -192,6 +221,14 @@ int cp_check_batch(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_
   return validate(desc, rows, n_rows);
 }
 
+int cp_check_block_tables(const cp_attn_desc* desc, const int32_t* block_tables_host,
+                          const cp_row_meta* rows, int32_t n_rows) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  if (!block_tables_host) return n_rows > 0 ? CP_ERR_INVALID_ARG : CP_OK;
+  return check_tables_host(desc, block_tables_host, rows, n_rows);
+}
+
 size_t cp_workspace_bytes(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows) {
   if (validate(desc, rows, n_rows) != CP_OK) return 0;
   try {
@@ -219,7 +256,9 @@ int cp_plan_summary(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
     counts[2] = (int64_t)p.merge.size() * hkv;
     counts[3] = p.partial_rows;
     counts[5] = p.decode_split_blocks;
-    counts[4] = (int64_t)cp_workspace_bytes(desc, rows, n_rows);  // rebuilds the plan
+    AppendPlan& a = thread_append_plan();
+    build_append_plan(*desc, rows, n_rows, a);
+    counts[4] = (int64_t)(p.ws_bytes > a.ws_bytes ? p.ws_bytes : a.ws_bytes);
   } catch (...) {
     return CP_ERR_INVALID_ARG;
   }
@@ -254,17 +293,15 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
         put_item(0, it.tok0, it.n_tok, it.pos0, it.req, slot % hkv, it.kv_begin, it.kv_end);
       }
     }
-    // position of a decode query: its row's chunk_start
+    // position of a decode query: chunk_start + its index inside the row
     std::vector<int32_t> pos_of_tok;
     {
       int64_t t = 0;
       for (int32_t r = 0; r < n_rows; ++r) t += rows[r].chunk_len;
       pos_of_tok.assign((size_t)t, -1);
       t = 0;
-      for (int32_t r = 0; r < n_rows; ++r) {
-        if (rows[r].chunk_len > 0) pos_of_tok[(size_t)t] = rows[r].chunk_start;
-        t += rows[r].chunk_len;
-      }
+      for (int32_t r = 0; r < n_rows; ++r)
+        for (int32_t j = 0; j < rows[r].chunk_len; ++j) pos_of_tok[(size_t)t++] = rows[r].chunk_start + j;
     }
     for (int32_t h = 0; h < hkv; ++h)
       for (const DecodeItem& it : p.decode)
@@ -290,6 +327,10 @@ int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new,
     build_append_plan(*desc, rows, n_rows, p);
     if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (debug_mode()) {
+      const int rc = debug_check_tables(desc, block_tables, rows, n_rows, s);
+      if (rc != CP_OK) return rc;
+    }
     AppendArgs a;
     a.items = reinterpret_cast<const AppendItem*>(ws);
     a.n_items = (int)p.items.size();
@@ -352,6 +393,9 @@ int cp_attn_prepare(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
     pl.off_merge = (int64_t)p.off_merge;
     pl.off_part_o = (int64_t)p.off_part_o;
     pl.off_part_lse = (int64_t)p.off_part_lse;
+    pl.n_prefill_items = (int32_t)p.prefill.size();
+    pl.n_prefill_wide_items = (int32_t)p.prefill_wide.size();
+    pl.partial_rows = p.partial_rows;
     *plan = pl;
     return CP_OK;
   } catch (...) {
@@ -367,7 +411,8 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   if (vd != CP_OK) return vd;
   if (plan->tokens == 0) return CP_OK;
   if (plan->ws_bytes <= 0 || plan->n_prefill_slots < 0 || plan->n_prefill_wide_slots < 0 ||
-      plan->n_decode < 0 || plan->n_merge < 0)
+      plan->n_decode < 0 || plan->n_merge < 0 || plan->n_prefill_items < 0 ||
+      plan->n_prefill_wide_items < 0 || plan->partial_rows < 0)
     return CP_ERR_INVALID_ARG;
   if ((size_t)plan->ws_bytes > ws_bytes) return CP_ERR_WORKSPACE;
   if (!q || !k_cache || !v_cache || !block_tables || !out || !ws) return CP_ERR_INVALID_ARG;
@@ -379,12 +424,27 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
                            plan->off_part_o, plan->off_part_lse};
   for (int64_t o : offs)
     if (o < 0 || o > plan->ws_bytes) return CP_ERR_INVALID_ARG;
+  // every list the kernels read lies inside the plan's workspace
+  const int64_t D64 = desc->head_dim;
+  const int64_t ends[8] = {
+      plan->off_prefill + (int64_t)plan->n_prefill_items * (int64_t)sizeof(PrefillItem),
+      plan->off_prefill_slots + (int64_t)plan->n_prefill_slots * 4,
+      plan->off_prefill_wide + (int64_t)plan->n_prefill_wide_items * (int64_t)sizeof(PrefillItem),
+      plan->off_prefill_wide_slots + (int64_t)plan->n_prefill_wide_slots * 4,
+      plan->off_decode + (int64_t)plan->n_decode * (int64_t)sizeof(DecodeItem),
+      plan->off_merge + (int64_t)plan->n_merge * (int64_t)sizeof(MergeGroup),
+      plan->off_part_o + plan->partial_rows * D64 * 4,
+      plan->off_part_lse + plan->partial_rows * 4};
+  for (int64_t e : ends)
+    if (e > plan->ws_bytes) return CP_ERR_INVALID_ARG;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* base = static_cast<uint8_t*>(ws);
   AttnArgs a;
   a.prefill = reinterpret_cast<const PrefillItem*>(base + plan->off_prefill);
   a.prefill_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_slots);
   a.n_prefill_slots = plan->n_prefill_slots;
+  a.n_prefill_items = plan->n_prefill_items;
+  a.n_prefill_wide_items = plan->n_prefill_wide_items;
   a.prefill_wide = reinterpret_cast<const PrefillItem*>(base + plan->off_prefill_wide);
   a.prefill_wide_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_wide_slots);
   a.n_prefill_wide_slots = plan->n_prefill_wide_slots;
@@ -441,6 +501,11 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
       !aligned(ws, 256) || !aligned(block_tables, 4))
     return CP_ERR_INVALID_ARG;
+  if (debug_mode()) {
+    const int rc = debug_check_tables(desc, block_tables, rows, n_rows,
+                                      reinterpret_cast<hipStream_t>(stream));
+    if (rc != CP_OK) return rc;
+  }
   cp_attn_plan plan;
   const int rc = cp_attn_prepare(desc, rows, n_rows, ws, ws_bytes, stream, &plan);
   if (rc != CP_OK) return rc;

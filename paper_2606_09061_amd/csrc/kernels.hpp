@@ -30,6 +30,7 @@ struct AttnArgs {
   const PrefillItem* prefill;       // 128-row tiles (4-wave kernel)
   const int32_t* prefill_slots;     // item * hkv + kv head, or -1
   int n_prefill_slots;
+  int n_prefill_items, n_prefill_wide_items;  // slots outside [0, items * hkv) are skipped
   const PrefillItem* prefill_wide;  // 256-row tiles (8-wave kernel)
   const int32_t* prefill_wide_slots;
   int n_prefill_wide_slots;

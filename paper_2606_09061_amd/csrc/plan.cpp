@@ -172,7 +172,10 @@ int validate(const cp_attn_desc* d, const cp_row_meta* rows, int32_t n_rows) {
 Tuning tuning_from_env(int num_cus) {
   Tuning t;
   t.num_cus = num_cus > 0 ? num_cus : 256;
-  if (const char* s = std::getenv("CP_PREFILL_MIN_LEN")) t.prefill_min_len = std::max(2, atoi(s));
+  // Rows shorter than this run on the decode kernel, token by token (any
+  // value >= 2 is exact; 2 sends every multi-token chunk to the MFMA kernel).
+  if (const char* s = std::getenv("CP_PREFILL_MIN_LEN"))
+    t.prefill_min_len = std::min(kMaxPrefillMinLen, std::max(2, atoi(s)));
   if (const char* s = std::getenv("CP_DECODE_TARGET_ITEMS")) t.decode_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_TARGET_ITEMS")) t.prefill_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_MIN_SPLIT")) t.prefill_min_split = std::max(1, atoi(s));
@@ -365,12 +368,23 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   order_for_xcds(true, sc.item_cost[1], Hkv, t.num_xcds, sc, p.prefill_wide_slots);
 
   // ---- decode ranges --------------------------------------------------
+  // Rows shorter than prefill_min_len run on the split-K decode kernel, one
+  // item list per query token: token j of a row sits at position
+  // chunk_start + j and sees keys [0, chunk_start + j + 1), so each token is
+  // its own "decode row" with its own causal limit (a one-token row is the
+  // usual case; few-token chunks read their request's K/V once per token).
+  auto each_decode_token = [&](auto&& f) {
+    for (int32_t r = 0; r < n_rows; ++r) {
+      const cp_row_meta& m = rows[r];
+      if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
+      for (int32_t j = 0; j < m.chunk_len; ++j)
+        f(m, (int32_t)(off[r] + j), m.chunk_start + j + 1);
+    }
+  };
   int64_t dec_blocks = 0;
-  for (int32_t r = 0; r < n_rows; ++r) {
-    const cp_row_meta& m = rows[r];
-    if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
-    dec_blocks += ceil_div(m.ctx_len, B) * Hkv;
-  }
+  each_decode_token([&](const cp_row_meta&, int32_t, int32_t kv_end) {
+    dec_blocks += ceil_div(kv_end, B) * Hkv;
+  });
   if (dec_blocks > 0) {
     // Items per CU grow with the decode bytes: ~3 per CU (the kernel keeps
     // three workgroups resident) for small loads, where every extra item costs
@@ -390,13 +404,11 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     // count, which is at most sb): first count, then place.
     auto& count = sc.count;
     count.assign((size_t)sb + 2, 0);
-    for (int32_t r = 0; r < n_rows; ++r) {
-      const cp_row_meta& m = rows[r];
-      if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
-      const int64_t nb = ceil_div(m.ctx_len, B);
+    each_decode_token([&](const cp_row_meta&, int32_t, int32_t kv_end) {
+      const int64_t nb = ceil_div(kv_end, B);
       const int64_t ns = std::max<int64_t>(1, ceil_div(nb, sb));
       for (int64_t s = 0; s < ns; ++s) ++count[nb * (s + 1) / ns - nb * s / ns];
-    }
+    });
     int64_t n_items = 0;
     for (int64_t c = sb + 1; c >= 0; --c) {  // count[c] becomes the first slot of cost c
       const int64_t k = count[c];
@@ -404,29 +416,27 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
       n_items += k;
     }
     p.decode.resize((size_t)n_items);
-    for (int32_t r = 0; r < n_rows; ++r) {
-      const cp_row_meta& m = rows[r];
-      if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
-      const int64_t nb = ceil_div(m.ctx_len, B);
+    each_decode_token([&](const cp_row_meta& m, int32_t tok, int32_t kv_end) {
+      const int64_t nb = ceil_div(kv_end, B);
       const int64_t ns = std::max<int64_t>(1, ceil_div(nb, sb));
       int32_t part0 = -1;
       if (ns > 1) {
         part0 = (int32_t)p.partial_rows;
         p.partial_rows += (int64_t)Hkv * ns * G;
-        add_merge(p, (int32_t)off[r], 1, (int32_t)ns, part0, G, d.head_dim);
+        add_merge(p, tok, 1, (int32_t)ns, part0, G, d.head_dim);
       }
       for (int64_t s = 0; s < ns; ++s) {
         const int64_t b0 = nb * s / ns, b1 = nb * (s + 1) / ns;
         DecodeItem& it = p.decode[(size_t)count[b1 - b0]++];
-        it.tok = (int32_t)off[r];
+        it.tok = tok;
         it.req = m.req_id;
         it.kv_begin = (int32_t)(b0 * B);
-        it.kv_end = (int32_t)std::min<int64_t>(b1 * B, m.ctx_len);
+        it.kv_end = (int32_t)std::min<int64_t>(b1 * B, kv_end);
         it.part = ns > 1 ? part0 + (int32_t)(s * G) : -1;
         it.part_kvh_stride = ns > 1 ? (int32_t)(ns * G) : 0;
         it.pad0 = it.pad1 = 0;
       }
-    }
+    });
   }
 
   // ---- workspace layout ------------------------------------------------

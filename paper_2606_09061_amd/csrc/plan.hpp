@@ -27,6 +27,9 @@ constexpr int kPrefillRowsWide = 256;
 constexpr int kPrefillKeys = 64;
 // Waves per decode workgroup (each wave walks every kDecodeWaves-th block).
 constexpr int kDecodeWaves = 4;
+// Upper bound of Tuning::prefill_min_len: rows shorter than it become one
+// decode item list per token, which only pays for few-token chunks.
+constexpr int kMaxPrefillMinLen = 64;
 
 // One item describes the work of every kv head.  Decode and merge kernels run
 // on a grid of (items, num_kv_heads).  Prefill workgroups take a slot each:
@@ -73,7 +76,8 @@ struct AppendItem {   // 16 bytes: one request's new tokens inside one block
 };
 
 struct Tuning {
-  int prefill_min_len = 2;      // rows with chunk_len >= this go to the MFMA kernel
+  int prefill_min_len = 2;      // rows with chunk_len >= this go to the MFMA kernel, shorter
+                                // rows to the decode kernel token by token (2..kMaxPrefillMinLen)
   int decode_target_items = 0;  // 0: derived from the CU count and the decode bytes
   int prefill_target_items = 0; // 0: split length chosen by the run-time estimate
   int prefill_min_split = 8;    // shortest prefill split, in kPrefillKeys steps

@@ -153,7 +153,7 @@ using namespace prefill_impl;
 
 template <int D, int B, int G, int NW, int RG>
 __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
-    const PrefillItem* __restrict__ items, const int32_t* __restrict__ slots,
+    const PrefillItem* __restrict__ items, const int32_t* __restrict__ slots, int n_items,
     const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
@@ -171,7 +171,8 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
   __shared__ __attribute__((aligned(1024))) uint8_t vb1[C::TILE_BYTES];
 
   const int slot = slots[blockIdx.x];
-  if (slot < 0) return;  // idle slot of the XCD-interleaved order
+  // idle slot of the XCD-interleaved order (-1), or one naming no item
+  if (slot < 0 || slot >= n_items * hkv) return;
   const int item = slot / hkv;
   const int kvh = slot - item * hkv;
   const PrefillItem it = items[item];
@@ -661,32 +662,32 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
 
 template <int D, int B, int G, int NW>
 static hipError_t launch_prefill_t(const PrefillItem* items, const int32_t* slots, int n,
-                                   const AttnArgs& a, hipStream_t s) {
+                                   int n_items, const AttnArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((prefill_kernel<D, B, G, NW, kPrefillRG>), dim3(n), dim3(NW * 64), 0, s, items, slots,
-                     a.q, a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv,
+                     n_items, a.q, a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv,
                      a.mbr, a.scale_log2);
   return hipGetLastError();
 }
 
 template <int D, int B, int NW>
 static hipError_t launch_prefill_g(int G, const PrefillItem* items, const int32_t* slots, int n,
-                                   const AttnArgs& a, hipStream_t s) {
+                                   int ni, const AttnArgs& a, hipStream_t s) {
   switch (G) {
-    case 1: return launch_prefill_t<D, B, 1, NW>(items, slots, n, a, s);
-    case 2: return launch_prefill_t<D, B, 2, NW>(items, slots, n, a, s);
-    case 4: return launch_prefill_t<D, B, 4, NW>(items, slots, n, a, s);
-    case 8: return launch_prefill_t<D, B, 8, NW>(items, slots, n, a, s);
+    case 1: return launch_prefill_t<D, B, 1, NW>(items, slots, n, ni, a, s);
+    case 2: return launch_prefill_t<D, B, 2, NW>(items, slots, n, ni, a, s);
+    case 4: return launch_prefill_t<D, B, 4, NW>(items, slots, n, ni, a, s);
+    case 8: return launch_prefill_t<D, B, 8, NW>(items, slots, n, ni, a, s);
   }
   return hipErrorInvalidValue;
 }
 
 template <int NW>
 static hipError_t launch_prefill_w(int D, int G, const PrefillItem* items, const int32_t* slots,
-                                   int n, const AttnArgs& a, hipStream_t s) {
-  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, items, slots, n, a, s);
-  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, items, slots, n, a, s);
-  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, items, slots, n, a, s);
-  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, items, slots, n, a, s);
+                                   int n, int ni, const AttnArgs& a, hipStream_t s) {
+  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, items, slots, n, ni, a, s);
+  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, items, slots, n, ni, a, s);
+  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, items, slots, n, ni, a, s);
+  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, items, slots, n, ni, a, s);
   return hipErrorInvalidValue;
 }
 
@@ -696,9 +697,10 @@ hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s) {
   hipError_t e = hipSuccess;
   if (a.n_prefill_wide_slots > 0)
     e = launch_prefill_w<kWide>(D, G, a.prefill_wide, a.prefill_wide_slots, a.n_prefill_wide_slots,
-                                a, s);
+                                a.n_prefill_wide_items, a, s);
   if (e == hipSuccess && a.n_prefill_slots > 0)
-    e = launch_prefill_w<kNarrow>(D, G, a.prefill, a.prefill_slots, a.n_prefill_slots, a, s);
+    e = launch_prefill_w<kNarrow>(D, G, a.prefill, a.prefill_slots, a.n_prefill_slots,
+                                  a.n_prefill_items, a, s);
   return e;
 }
 

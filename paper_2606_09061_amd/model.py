@@ -235,7 +235,10 @@ class Model:
         self.pos = torch.zeros(T, dtype=torch.int32, device=self.dev)
         self.tokens = torch.randint(0, c.vocab, (T,), generator=gen, device=self.dev)
         self.ws = torch.empty(64 << 20, dtype=torch.uint8, device=self.dev)      # attention plan
-        self.ws_append = torch.empty(1 << 20, dtype=torch.uint8, device=self.dev)
+        # an append item covers one row's tokens inside one block: at most
+        # max_tokens + max_seqs items of 16 bytes, so the append never needs more
+        self.ws_append = torch.empty(16 * (max_tokens + max_seqs) + 256, dtype=torch.uint8,
+                                     device=self.dev)
 
     def forward(self, rows, stream=None):
         """Runs one iteration for the batch ``rows`` [(slot, start, len, ctx)];
@@ -250,11 +253,6 @@ class Model:
         if T > self.max_tokens:
             raise ValueError(f"batch of {T} tokens exceeds the model's {self.max_tokens}")
         s = stream or torch.cuda.current_stream(self.dev)
-        need = cp.workspace_bytes(self.desc, rows)
-        if need > self.ws.numel():
-            self.ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
-        if need > self.ws_append.numel():
-            self.ws_append = torch.empty(need, dtype=torch.uint8, device=self.dev)
         pos = positions_of(rows)
         self.pos_copied.synchronize()   # the previous iteration's upload has left pos_host
         self.pos_host[:T].numpy()[:] = pos
@@ -266,7 +264,16 @@ class Model:
             qkv, q, k, v, attn = self.qkv[:T], self.q[:T], self.k[:T], self.v[:T], self.attn[:T]
             gu, act = self.gu[:T], self.act[:T]
             # every layer attends with the same rows: plan once, run per layer
-            plan = cp.attn_prepare(self.desc, rows, self.ws, stream=s)
+            # (the plan is built once per iteration; only a workspace that is
+            # too small costs a second planning, to learn the size)
+            try:
+                plan = cp.attn_prepare(self.desc, rows, self.ws, stream=s)
+            except cp.CpError as e:
+                if e.code != cp.CP_ERR_WORKSPACE:
+                    raise
+                self.ws = torch.empty(cp.workspace_bytes(self.desc, rows), dtype=torch.uint8,
+                                      device=self.dev)
+                plan = cp.attn_prepare(self.desc, rows, self.ws, stream=s)
             for L, kc, vc in zip(self.layers, self.kc, self.vc):
                 rmsnorm(x, L["in_norm"], h, c.eps, s)
                 project(h, L["qkv"], qkv, None, s)

@@ -65,6 +65,17 @@ class StepEngine:
         self.stream = torch.cuda.current_stream(self.dev)
         self.ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
 
+    def _grow_on_demand(self, call, rows):
+        import torch
+        try:
+            call()
+        except cp.CpError as e:
+            if e.code != cp.CP_ERR_WORKSPACE:
+                raise
+            self.ws = torch.empty(cp.workspace_bytes(self.desc, rows), dtype=torch.uint8,
+                                  device=self.dev)
+            call()
+
     def step(self, rows) -> float:
         """Runs one batch; returns the GPU time of append + attention in us."""
         import torch
@@ -74,15 +85,16 @@ class StepEngine:
             return 0.0
         if T > self.max_tokens:
             raise ValueError(f"batch of {T} tokens exceeds the engine's {self.max_tokens}")
-        need = cp.workspace_bytes(self.desc, rows)
-        if need > self.ws.numel():
-            self.ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
         s = self.stream
         self.ev[0].record(s)
-        cp.kv_append(self.desc, self.kn[:T], self.vn[:T], self.kc, self.vc, self.bt, rows, self.ws,
-                     stream=s)
-        cp.attn_mixed(self.desc, self.q[:T], self.kc, self.vc, self.bt, rows, self.out[:T], self.ws,
-                      stream=s)
+        # Each call plans the batch once.  A workspace too small is reported
+        # before anything is enqueued; only then is the size asked for (a
+        # second planning) and the call repeated.
+        self._grow_on_demand(lambda: cp.kv_append(self.desc, self.kn[:T], self.vn[:T], self.kc,
+                                                  self.vc, self.bt, rows, self.ws, stream=s), rows)
+        self._grow_on_demand(lambda: cp.attn_mixed(self.desc, self.q[:T], self.kc, self.vc,
+                                                   self.bt, rows, self.out[:T], self.ws, stream=s),
+                             rows)
         self.ev[1].record(s)
         self.ev[1].synchronize()
         return self.ev[0].elapsed_time(self.ev[1]) * 1e3

@@ -125,7 +125,11 @@ def test_workspace_bytes_zero_for_invalid():
 
 # ----------------------------------------------------------------- planner coverage
 
-def _check_coverage(batch):
+def _check_coverage(batch, min_len=2):
+    """Every (token, kv head) of the batch is covered by items whose key ranges
+    partition [0, end) with the token's position p < end <= ctx.  Rows of at
+    least ``min_len`` tokens are prefill tiles; shorter rows are decode items,
+    one per token, each ending exactly at its own causal limit p + 1."""
     d = cp.desc_for(batch)
     items = cp.plan_items(d, batch.rows)
     G = batch.group
@@ -147,7 +151,7 @@ def _check_coverage(batch):
                 assert lst, f"token {t} head {kvh} not covered"
                 seen.add((t, kvh))
                 kinds = {x[0] for x in lst}
-                assert kinds == ({0} if c >= 2 else {1})
+                assert kinds == ({0} if c >= min_len else {1})
                 assert all(x[5] == req for x in lst)
                 ranges = sorted((x[1], x[2]) for x in lst)
                 # the ranges partition [0, end) with p < end <= ctx
@@ -159,8 +163,9 @@ def _check_coverage(batch):
                 # every split holds a key the token may see
                 for kb, ke in ranges:
                     assert kb <= p
-                if c == 1:
-                    assert end == ctx
+                if c < min_len:
+                    assert end == p + 1, f"decode token at {p} ends at {end}"
+                    assert all(x[3] == p and x[4] == 1 for x in lst)
     assert seen == set(cover), "items cover tokens outside the batch"
 
 
@@ -235,3 +240,101 @@ def test_prefill_tile_width_follows_the_step_key_range():
     # one width for the whole step: its token-weighted mean decides (here 4,224)
     assert widest([[0, 0, 256, 256], [1, 8192, 256, 8448]]) == 64
     assert widest([[0, 0, 2000, 2000], [1, 1200, 8, 1208]]) == 32   # (2000*1000 + 8*1204)/2008
+
+
+FEW_TOKEN_ROWS = [(0, 2), (5, 3), (100, 2), (4000, 7), (31, 15), (16, 16), (999, 1), (0, 1),
+                  (2047, 40), (3, 0)]
+
+
+@pytest.mark.parametrize("min_len", [2, 3, 8, 16, 64])
+def test_plan_routes_short_rows_to_decode_token_by_token(monkeypatch, min_len):
+    """CP_PREFILL_MIN_LEN sends rows shorter than it to the decode kernel with
+    one item list per token (its own causal limit); any value is exact."""
+    monkeypatch.setenv("CP_PREFILL_MIN_LEN", str(min_len))
+    rng = np.random.default_rng(min_len)
+    for hq, hkv, d, bs in ((32, 8, 128, 16), (64, 8, 128, 32), (8, 8, 64, 16), (16, 2, 64, 32)):
+        _check_coverage(make_batch("few", hq, hkv, d, bs, FEW_TOKEN_ROWS, rng), min_len)
+
+
+@pytest.mark.parametrize("value,effective", [("1", 2), ("0", 2), ("-5", 2), ("65", 64),
+                                             ("100000", 64), ("junk", 2)])
+def test_prefill_min_len_is_clamped(monkeypatch, value, effective):
+    monkeypatch.setenv("CP_PREFILL_MIN_LEN", value)
+    rng = np.random.default_rng(4)
+    rows = [(10, c) for c in (1, 2, 63, 64, 65)]
+    b = make_batch("clamp", 32, 8, 128, 16, [(10 * i, c) for i, (s, c) in enumerate(rows)], rng)
+    _check_coverage(b, effective)
+
+
+def test_attn_run_rejects_lists_past_the_workspace():
+    """Each list end (offset + length x item size) must lie inside the plan's
+    workspace; a stale or edited plan is refused before any launch."""
+    lib = binding.load()
+    d = _desc()
+
+    def run(**kw):
+        plan = binding.AttnPlan()
+        plan.desc = d
+        plan.tokens, plan.ws_bytes = 5, 4096
+        for k, v in kw.items():
+            setattr(plan, k, v)
+        return lib.cp_attn_run(ctypes.byref(plan), 256, 256, 256, 256, 256, 256, 4096, None)
+
+    big = 4096
+    assert run(off_decode=big - 64, n_decode=3) == binding.CP_ERR_INVALID_ARG     # 96 B past 4032
+    assert run(off_merge=big - 32, n_merge=2) == binding.CP_ERR_INVALID_ARG
+    assert run(off_prefill_slots=big - 4, n_prefill_slots=2) == binding.CP_ERR_INVALID_ARG
+    assert run(off_prefill_wide_slots=big - 8, n_prefill_wide_slots=3) == binding.CP_ERR_INVALID_ARG
+    assert run(off_prefill=big - 32, n_prefill_items=2) == binding.CP_ERR_INVALID_ARG
+    assert run(off_prefill_wide=0, n_prefill_wide_items=129) == binding.CP_ERR_INVALID_ARG
+    assert run(off_part_o=0, partial_rows=9) == binding.CP_ERR_INVALID_ARG        # 9 x 512 B
+    assert run(off_part_lse=big - 8, partial_rows=3) == binding.CP_ERR_INVALID_ARG
+    assert run(n_prefill_items=-1) == binding.CP_ERR_INVALID_ARG
+    assert run(partial_rows=-1) == binding.CP_ERR_INVALID_ARG
+
+
+def test_prepared_plan_lists_fit_its_workspace():
+    for n in (2, 3, 4):
+        b = make_config(n)
+        d = cp.desc_for(b)
+        s = cp.plan_summary(d, b.rows)
+        assert s["workspace_bytes"] == cp.workspace_bytes(d, b.rows)
+        assert s["workspace_bytes"] >= s["partial_rows"] * (b.head_dim + 1) * 4
+
+
+def test_check_block_tables_host():
+    b = make_config(2)
+    d = cp.desc_for(b)
+    bt = b.block_tables.copy()
+    assert cp.check_block_tables(d, bt, b.rows) == binding.CP_OK
+    # an entry past a row's context is never read: any value is accepted there
+    req, s, c, ctx = (int(x) for x in b.rows[0])
+    nb = -(-ctx // b.block_size)
+    if nb < bt.shape[1]:
+        bt2 = bt.copy()
+        bt2[req, nb] = -7
+        assert cp.check_block_tables(d, bt2, b.rows) == binding.CP_OK
+    for bad in (-1, b.num_blocks, 1 << 30):
+        bt2 = bt.copy()
+        bt2[req, nb - 1] = bad                      # the row's last block
+        assert cp.check_block_tables(d, bt2, b.rows) == binding.CP_ERR_BAD_META
+        bt2 = bt.copy()
+        bt2[req, 0] = bad
+        assert cp.check_block_tables(d, bt2, b.rows) == binding.CP_ERR_BAD_META
+    lib = binding.load()
+    r = np.ascontiguousarray(b.rows)
+    assert lib.cp_check_block_tables(ctypes.byref(d), None, r.ctypes.data,
+                                     r.shape[0]) == binding.CP_ERR_INVALID_ARG
+    assert cp.check_block_tables(_desc(head_dim=96), bt, b.rows) == binding.CP_ERR_UNSUPPORTED
+
+
+def test_compute_calls_reject_bad_tables_under_debug_only_after_validation(monkeypatch):
+    """With CP_DEBUG=1 a malformed batch is still refused by validation first
+    (no device access happens for it, so no GPU is needed here)."""
+    monkeypatch.setenv("CP_DEBUG", "1")
+    lib = binding.load()
+    d = _desc()
+    bad = np.array([[0, 10, 5, 16]], np.int32)
+    fake = 1 << 20
+    assert lib.cp_attn_mixed(ctypes.byref(d), fake, fake, fake, fake, bad.ctypes.data, 1, fake,
+                             fake, 1 << 30, None) == binding.CP_ERR_BAD_META

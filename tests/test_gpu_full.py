@@ -1,9 +1,9 @@
 """Full-size GPU parity: the benchmark's mixes in the benchmark's launch
 configuration (same C ABI calls, same plans), checked against the fp64
-oracle.  Whole K/V pools are compared bit for bit after the append; outputs
-are compared on sampled (token, q head) pairs the oracle computes one by
-one: every decode row, the first/last token of every chunk and of every
-prefill tile, and a uniform random sample.
+oracle.  Whole K/V pools are compared bit for bit after the append, and every
+output element (all T x Hq x D of each mix and of each of the replay's 20
+iterations) is compared with the oracle's; max and mean errors are printed
+per mix and per iteration.
 """
 
 import numpy as np
@@ -18,29 +18,10 @@ from workloads import replay_schedule
 pytestmark = pytest.mark.gpu
 
 
-def sample_pairs(batch, n_random=1500, seed=0):
-    Hq = batch.num_q_heads
-    tile = 128 // batch.group
-    off = batch.tok_offsets()
-    toks = set()
-    for r, (req, s, c, ctx) in enumerate(batch.rows.tolist()):
-        if c == 0:
-            continue
-        for j in (0, c - 1, tile - 1, tile, c // 2):
-            if 0 <= j < c:
-                toks.add(int(off[r] + j))
-    sel = {t * Hq + h for t in toks for h in range(Hq)}
-    rng = np.random.default_rng(seed)
-    total = batch.num_tokens * Hq
-    sel |= set(rng.choice(total, size=min(total, n_random), replace=False).tolist())
-    return np.array(sorted(sel), dtype=np.int64)
-
-
-def check_sampled(batch, out_gpu, q_host, kc_ref, vc_ref, what, seed=0):
-    sel = sample_pairs(batch, seed=seed)
-    ref = oracle.attn(batch, q_host, kc_ref, vc_ref, sel=sel)
-    got = out_gpu.reshape(-1, batch.head_dim)[torch.from_numpy(sel).to(out_gpu.device)]
-    return assert_close(got, ref, f"{what} ({len(sel)} sampled rows)")
+def check_all(batch, out_gpu, q_host, kc_ref, vc_ref, what):
+    """Every output element against the oracle's."""
+    ref = oracle.attn(batch, q_host, kc_ref, vc_ref)
+    return assert_close(out_gpu, ref, f"{what} (all {ref.size} elements)")
 
 
 @pytest.mark.parametrize("n", [2, 3, 4])
@@ -57,7 +38,7 @@ def test_full_size_mix(n):
     del kc0, vc0
     assert np.array_equal(words(t["k_cache"]).reshape(-1), kc_ref.reshape(-1)), "K pool differs"
     assert np.array_equal(words(t["v_cache"]).reshape(-1), vc_ref.reshape(-1)), "V pool differs"
-    check_sampled(batch, out, host["q"], kc_ref, vc_ref, f"mix {n}")
+    check_all(batch, out, host["q"], kc_ref, vc_ref, f"mix {n}")
 
 
 def test_replay_twenty_iterations_lockstep():
@@ -72,8 +53,8 @@ def test_replay_twenty_iterations_lockstep():
         say(f"[gpu] replay iteration {i}: rows={b.n_rows} T={b.num_tokens}")
         out = run_step(b, t)
         torch.cuda.synchronize()
-        kc_ref, vc_ref = oracle.kv_append(b, kn.cpu(), vn.cpu(), kc_ref, vc_ref)
-        check_sampled(b, out, q.cpu(), kc_ref, vc_ref, f"replay it {i}", seed=i)
+        kc_ref, vc_ref = oracle.kv_append(b, kn.cpu(), vn.cpu(), kc_ref, vc_ref, inplace=True)
+        check_all(b, out, q.cpu(), kc_ref, vc_ref, f"replay it {i}")
         if i in (0, 9, 19):
             assert np.array_equal(words(kc).reshape(-1), kc_ref.reshape(-1)), f"K pool it {i}"
             assert np.array_equal(words(vc).reshape(-1), vc_ref.reshape(-1)), f"V pool it {i}"
@@ -141,4 +122,4 @@ def test_long_context_prefill_unsplit(monkeypatch):
     del kc0, vc0
     assert np.array_equal(words(t["k_cache"]).reshape(-1), kc_ref.reshape(-1)), "K pool differs"
     assert np.array_equal(words(t["v_cache"]).reshape(-1), vc_ref.reshape(-1)), "V pool differs"
-    check_sampled(batch, out, host["q"], kc_ref, vc_ref, "long context", seed=3)
+    check_all(batch, out, host["q"], kc_ref, vc_ref, "long context")

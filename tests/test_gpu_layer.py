@@ -172,11 +172,18 @@ def test_decoder_layer_matches_reference(rows):
         assert e.max() <= 0.04 * rms_kv and e.mean() <= 0.006 * rms_kv
 
 
-def test_model_forward_is_deterministic_and_finite():
+def test_model_forward_is_deterministic_and_finite(monkeypatch):
     cfg = M.ModelConfig(hidden=256, layers=3, hq=4, hkv=2, head_dim=64, inter=512, vocab=1000)
     m = M.Model(cfg, max_seqs=4, max_seq_len=256, max_tokens=256, seed=5)
+    # an iteration plans its batch once: the size is asked for only when the
+    # workspace reported too small
+    sized = []
+    real = M.cp.workspace_bytes
+    monkeypatch.setattr(M.cp, "workspace_bytes", lambda d, r: sized.append(1) or real(d, r))
+    m.ws = torch.empty(256, dtype=torch.uint8, device=m.dev)
     rows1 = np.array([[0, 0, 20, 20], [1, 0, 5, 5]], np.int32)
     t1 = m.forward(rows1)
+    assert len(sized) == 1 and m.ws.numel() >= 256
     rows2 = np.array([[0, 20, 1, 21], [1, 5, 1, 6]], np.int32)
     t2 = m.forward(rows2)
     x2 = m.x[:2].clone()
@@ -184,6 +191,7 @@ def test_model_forward_is_deterministic_and_finite():
     t2b = m.forward(rows2)
     torch.cuda.synchronize()
     assert t1.shape == (2,) and t2.shape == (2,)
+    assert len(sized) == 1, "a later iteration planned twice"
     assert torch.equal(t2, t2b) and torch.equal(x2, m.x[:2])
     assert torch.isfinite(m.x[:2].float()).all()
 

@@ -42,8 +42,13 @@ GEOMS = [(hq, hkv, d, b) for d in (64, 128) for b in (16, 32)
          for hq, hkv in ((4, 4), (8, 4), (8, 2), (16, 2))]
 
 
+@pytest.mark.parametrize("tiles", ["planned", "wide"])
 @pytest.mark.parametrize("geom", GEOMS, ids=lambda g: "hq%d_hkv%d_d%d_b%d" % g)
-def test_geometry_grid(geom):
+def test_geometry_grid(monkeypatch, geom, tiles):
+    """Every supported (D, B, G); with tiles="wide" every chunk of more than
+    128 rows runs on the 256-row tiles whatever the step's key range."""
+    if tiles == "wide":
+        monkeypatch.setenv("CP_PREFILL_WIDE_MIN_KEYS", "0")
     hq, hkv, d, b = geom
     rng = np.random.default_rng(hash(geom) % (2 ** 31))
     # a multi-tile chunk with a ragged tail, a chunk over deep context, a
@@ -58,6 +63,20 @@ def test_rows_in_any_order_and_zero_length_rows():
     rows = [(10, 40), (0, 0), (63, 1), (200, 0), (128, 130), (31, 1)]
     batch = make_batch("zeros", 32, 8, 128, 16, rows, rng)
     _full_check(batch, 3001, "zero-length rows")
+
+
+@pytest.mark.parametrize("min_len", [4, 16, 64])
+def test_few_token_rows_on_the_decode_kernel(monkeypatch, min_len):
+    """Rows shorter than CP_PREFILL_MIN_LEN run on the decode kernel token by
+    token, each token over keys up to its own position; output and pools as
+    with the default routing (the oracle's)."""
+    monkeypatch.setenv("CP_PREFILL_MIN_LEN", str(min_len))
+    rng = np.random.default_rng(min_len)
+    rows = [(0, 2), (5, 3), (100, 2), (4000, 7), (31, 15), (16, 16), (999, 1), (0, 1),
+            (2047, 40), (3, 0), (1500, 63), (777, 64)]
+    for hq, hkv, d, b in ((32, 8, 128, 16), (64, 8, 128, 32), (8, 8, 64, 16)):
+        batch = make_batch("few", hq, hkv, d, b, rows, rng)
+        _full_check(batch, 3100 + min_len + hq, f"few-token rows min_len={min_len} {(hq, hkv, d, b)}")
 
 
 def test_empty_batch_is_noop():
@@ -104,3 +123,41 @@ def test_prepared_plan_runs_match_attn_mixed_bit_for_bit():
     with pytest.raises(cp.CpError):   # a workspace smaller than the plan's
         cp.attn_run(plan, layers[0]["q"], layers[0]["k_cache"], layers[0]["v_cache"],
                     layers[0]["block_tables"], outs_plan[0], ws_b[:256])
+
+
+def test_debug_mode_rejects_out_of_range_block_ids(monkeypatch):
+    """CP_DEBUG=1: a table entry outside [0, num_blocks) is found on the host
+    before anything is enqueued (the entry points at memory the pools do hold,
+    past the num_blocks the descriptor declares)."""
+    import paper_2606_09061_amd as cp
+    rng = np.random.default_rng(31)
+    batch = make_batch("debug", 8, 2, 64, 16, [(40, 24), (70, 1)], rng, n_spare=8)
+    tens = to_dev(make_tensors(batch, seed=3201))
+    d = cp.desc_for(batch)
+    d.num_blocks = batch.num_blocks - 4            # the pools hold 4 blocks more
+    req, s, c, ctx = (int(x) for x in batch.rows[0])
+    bt = tens["block_tables"].clone()
+    bt[req, 1] = batch.num_blocks - 2              # declared out of range, allocated
+    ws = torch.empty(cp.workspace_bytes(d, batch.rows), dtype=torch.uint8, device="cuda")
+    out = torch.zeros(batch.num_tokens, 8, 64, dtype=torch.bfloat16, device="cuda")
+    kc0, vc0 = tens["k_cache"].clone(), tens["v_cache"].clone()
+    monkeypatch.setenv("CP_DEBUG", "1")
+    say("[gpu] CP_DEBUG table check")
+    with pytest.raises(cp.CpError) as e:
+        cp.kv_append(d, tens["k_new"], tens["v_new"], tens["k_cache"], tens["v_cache"], bt,
+                     batch.rows, ws)
+    assert e.value.code == -2
+    with pytest.raises(cp.CpError) as e:
+        cp.attn_mixed(d, tens["q"], tens["k_cache"], tens["v_cache"], bt, batch.rows, out, ws)
+    assert e.value.code == -2
+    torch.cuda.synchronize()
+    assert torch.equal(out, torch.zeros_like(out)), "output written after a refused call"
+    assert np.array_equal(words(tens["k_cache"]), words(kc0)) and np.array_equal(
+        words(tens["v_cache"]), words(vc0)), "pools written after a refused call"
+    # the intact table passes the same checks and the step runs
+    cp.kv_append(d, tens["k_new"], tens["v_new"], tens["k_cache"], tens["v_cache"],
+                 tens["block_tables"], batch.rows, ws)
+    cp.attn_mixed(d, tens["q"], tens["k_cache"], tens["v_cache"], tens["block_tables"],
+                  batch.rows, out, ws)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all()

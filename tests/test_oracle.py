@@ -423,3 +423,18 @@ def test_planted_mistake_is_caught(name, tmp_path):
 
 def test_unmutated_oracle_passes_pin_subset():
     assert _pins_pass(oracle.load())
+
+
+def test_inplace_append_equals_copying_append():
+    """The in-place form of the oracle's append writes the same pools."""
+    import numpy as np
+    import oracle
+    from workloads import make_config, make_tensors
+    b = make_config(1)
+    t = make_tensors(b, seed=77)
+    kc, vc = oracle.kv_append(b, t["k_new"], t["v_new"], t["k_cache"], t["v_cache"])
+    k2 = t["k_cache"].view(__import__("torch").int16).numpy().view(np.uint16).copy()
+    v2 = t["v_cache"].view(__import__("torch").int16).numpy().view(np.uint16).copy()
+    k3, v3 = oracle.kv_append(b, t["k_new"], t["v_new"], k2, v2, inplace=True)
+    assert k3 is k2 and v3 is v2
+    assert np.array_equal(k2, kc) and np.array_equal(v2, vc)

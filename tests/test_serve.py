@@ -84,3 +84,37 @@ def test_apc_counts_interventions_and_enlarges_chunks():
     assert res[False]["apc_blocked_cap"] == 0 and res[False]["apc_blocked_min_chunk"] == 0
     assert res[True]["apc_blocked_cap"] + res[True]["apc_blocked_min_chunk"] > 0
     assert res[True]["avg_prefill_chunk"] > res[False]["avg_prefill_chunk"]
+
+
+def test_step_engine_plans_once_and_grows_workspace_on_demand(monkeypatch):
+    """The engine asks for the workspace size only after a call reported it
+    too small (CP_ERR_WORKSPACE, nothing enqueued), then repeats that call."""
+    import torch
+    from paper_2606_09061_amd import binding
+
+    eng = object.__new__(serve.StepEngine)
+    eng.dev = torch.device("cpu")
+    eng.desc = None
+    eng.ws = torch.empty(256, dtype=torch.uint8)
+    sizes = []
+    monkeypatch.setattr(binding, "workspace_bytes", lambda d, r: sizes.append(1) or 4096)
+    calls = []
+
+    def call():
+        calls.append(eng.ws.numel())
+        if eng.ws.numel() < 4096:
+            raise binding.CpError(binding.CP_ERR_WORKSPACE, "cp_attn_mixed")
+
+    eng._grow_on_demand(call, np.zeros((1, 4), np.int32))
+    assert calls == [256, 4096] and len(sizes) == 1 and eng.ws.numel() == 4096
+    calls.clear()
+    eng._grow_on_demand(call, np.zeros((1, 4), np.int32))   # big enough: no size query
+    assert calls == [4096] and len(sizes) == 1
+
+    def other():
+        raise binding.CpError(binding.CP_ERR_BAD_META, "cp_attn_mixed")
+    try:
+        eng._grow_on_demand(other, np.zeros((1, 4), np.int32))
+        raise AssertionError("error swallowed")
+    except binding.CpError as e:
+        assert e.code == binding.CP_ERR_BAD_META
