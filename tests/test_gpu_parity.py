@@ -127,17 +127,22 @@ def test_prepared_plan_runs_match_attn_mixed_bit_for_bit():
 
 def test_debug_mode_rejects_out_of_range_block_ids(monkeypatch):
     """CP_DEBUG=1: a table entry outside [0, num_blocks) is found on the host
-    before anything is enqueued (the entry points at memory the pools do hold,
-    past the num_blocks the descriptor declares)."""
+    before anything is enqueued.  The pools hold 4 blocks past the num_blocks
+    the descriptor declares, and the bad entry points at one of them, so the
+    memory it names exists either way."""
     import paper_2606_09061_amd as cp
     rng = np.random.default_rng(31)
-    batch = make_batch("debug", 8, 2, 64, 16, [(40, 24), (70, 1)], rng, n_spare=8)
+    batch = make_batch("debug", 8, 2, 64, 16, [(40, 24), (70, 1)], rng)
     tens = to_dev(make_tensors(batch, seed=3201))
+    for k in ("k_cache", "v_cache"):   # 4 NaN blocks past the declared pool
+        pad = torch.full((4,) + tuple(tens[k].shape[1:]), float("nan"), dtype=torch.bfloat16,
+                         device="cuda")
+        tens[k] = torch.cat([tens[k], pad]).contiguous()
     d = cp.desc_for(batch)
-    d.num_blocks = batch.num_blocks - 4            # the pools hold 4 blocks more
+    assert d.num_blocks == batch.num_blocks
     req, s, c, ctx = (int(x) for x in batch.rows[0])
     bt = tens["block_tables"].clone()
-    bt[req, 1] = batch.num_blocks - 2              # declared out of range, allocated
+    bt[req, 1] = batch.num_blocks + 1              # declared out of range, allocated
     ws = torch.empty(cp.workspace_bytes(d, batch.rows), dtype=torch.uint8, device="cuda")
     out = torch.zeros(batch.num_tokens, 8, 64, dtype=torch.bfloat16, device="cuda")
     kc0, vc0 = tens["k_cache"].clone(), tens["v_cache"].clone()
@@ -154,10 +159,13 @@ def test_debug_mode_rejects_out_of_range_block_ids(monkeypatch):
     assert torch.equal(out, torch.zeros_like(out)), "output written after a refused call"
     assert np.array_equal(words(tens["k_cache"]), words(kc0)) and np.array_equal(
         words(tens["v_cache"]), words(vc0)), "pools written after a refused call"
-    # the intact table passes the same checks and the step runs
+    # the intact table passes the same checks and the step matches the oracle
+    kc_ref, vc_ref = oracle.kv_append(batch, tens["k_new"].cpu(), tens["v_new"].cpu(),
+                                      words(tens["k_cache"])[: batch.num_blocks],
+                                      words(tens["v_cache"])[: batch.num_blocks])
     cp.kv_append(d, tens["k_new"], tens["v_new"], tens["k_cache"], tens["v_cache"],
                  tens["block_tables"], batch.rows, ws)
     cp.attn_mixed(d, tens["q"], tens["k_cache"], tens["v_cache"], tens["block_tables"],
                   batch.rows, out, ws)
     torch.cuda.synchronize()
-    assert torch.isfinite(out.float()).all()
+    assert_close(out, oracle.attn(batch, tens["q"].cpu(), kc_ref, vc_ref), "CP_DEBUG run")
