@@ -196,6 +196,43 @@ int cp_plan_summary(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n
 int64_t cp_plan_items(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows,
                       int32_t *items, int64_t cap);
 
+/* ---- Allocation-free variant of cp_attn_mixed --------------------------
+ *
+ * For callers that cannot allocate device memory per call: code that must
+ * not call hipMalloc (under HIP graph capture, in tight serving loops, in
+ * harnesses that forbid it).  cp_attn_mixed_noalloc runs the same plan and
+ * kernels as cp_attn_mixed (identical output), but takes no workspace: its
+ * plan lists and split partials live in a static device array of
+ * CP_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends, and its plan is staged through two pinned host
+ * buffers of CP_NOALLOC_PLAN_BYTES set up once per device.
+ *
+ * cp_noalloc_init: the set-up.  Call it once per device, with that device
+ * current, before the first cp_attn_mixed_noalloc there (further calls
+ * return CP_OK at once).  It takes the device address of the scratch array
+ * and allocates the two pinned staging buffers; CP_ERR_HIP if that fails.
+ *
+ * cp_attn_mixed_noalloc: cp_attn_mixed's arguments without ws / ws_bytes,
+ * same validation and codes, plus CP_ERR_WORKSPACE (nothing enqueued) when
+ * the batch's workspace would exceed CP_NOALLOC_SCRATCH_BYTES or its plan
+ * lists CP_NOALLOC_PLAN_BYTES (cp_workspace_bytes gives the former; the five
+ * synthetic mixes of this library's benchmark need at most 42 MB), and
+ * CP_ERR_INVALID_ARG when cp_noalloc_init has not run on the current device.
+ * It calls no device or pinned allocator: it waits for the staging buffer's
+ * previous copy, writes the plan into it, enqueues one copy and the kernels.
+ * The scratch needs no clearing (the plan is uploaded whole and every
+ * partial row is written before it is read).  Every call on one GPU shares
+ * that GPU's scratch: calls that overlap on one GPU (different streams, or
+ * threads without ordering) race; calls on one stream are ordered. */
+#define CP_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define CP_NOALLOC_PLAN_BYTES (1u << 20)
+
+int cp_noalloc_init(void);
+
+int cp_attn_mixed_noalloc(const cp_attn_desc *desc, const void *q, const void *k_cache,
+                          const void *v_cache, const int32_t *block_tables,
+                          const cp_row_meta *rows, int32_t n_rows, void *out, void *stream);
+
 /* Diagnostics: per-kernel GPU time.  After cp_profile_begin(), every kernel
  * the compute calls launch is bracketed by a pair of HIP events recorded on
  * the call's stream.  cp_profile_end() waits for those events and writes,

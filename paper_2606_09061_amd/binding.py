@@ -91,6 +91,9 @@ def load():
     lib.cp_plan_summary.restype = ctypes.c_int
     lib.cp_plan_items.argtypes = [dp, vp, i32, vp, i64]
     lib.cp_plan_items.restype = i64
+    lib.cp_noalloc_init.argtypes, lib.cp_noalloc_init.restype = [], ctypes.c_int
+    lib.cp_attn_mixed_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp]
+    lib.cp_attn_mixed_noalloc.restype = ctypes.c_int
     lib.cp_profile_begin.argtypes, lib.cp_profile_begin.restype = [], ctypes.c_int
     lib.cp_profile_end.argtypes, lib.cp_profile_end.restype = [vp, vp], ctypes.c_int
     _lib = lib
@@ -101,7 +104,7 @@ def exported_symbols():
     return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch",
             "cp_check_block_tables", "cp_kv_append",
             "cp_attn_mixed", "cp_attn_prepare", "cp_attn_run", "cp_plan_summary", "cp_plan_items",
-            "cp_profile_begin", "cp_profile_end"]
+            "cp_noalloc_init", "cp_attn_mixed_noalloc", "cp_profile_begin", "cp_profile_end"]
 
 
 def strerror(code: int) -> str:
@@ -214,6 +217,28 @@ def attn_run(plan: AttnPlan, q, k_cache, v_cache, block_tables, out, ws, ws_byte
                             _ptr(block_tables), _ptr(out), _ptr(ws), nbytes, _stream(stream))
     if rc != CP_OK:
         raise CpError(rc, "cp_attn_run")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20   # CP_NOALLOC_SCRATCH_BYTES
+NOALLOC_PLAN_BYTES = 1 << 20       # CP_NOALLOC_PLAN_BYTES
+
+
+def noalloc_init() -> None:
+    """cp_noalloc_init on the current device."""
+    rc = load().cp_noalloc_init()
+    if rc != CP_OK:
+        raise CpError(rc, "cp_noalloc_init")
+
+
+def attn_mixed_noalloc(desc: Desc, q, k_cache, v_cache, block_tables, rows, out,
+                       stream=None) -> None:
+    """cp_attn_mixed_noalloc: cp_attn_mixed on the library's static scratch."""
+    r = _rows(rows)
+    rc = load().cp_attn_mixed_noalloc(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                      _ptr(block_tables), r.ctypes.data, r.shape[0], _ptr(out),
+                                      _stream(stream))
+    if rc != CP_OK:
+        raise CpError(rc, "cp_attn_mixed_noalloc")
 
 
 def plan_summary(desc: Desc, rows) -> dict:

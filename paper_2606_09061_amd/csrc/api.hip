@@ -17,6 +17,13 @@ namespace {
 
 constexpr int kRingSlots = 8;
 
+// Device scratch of the allocation-free entry point, one copy per GPU (each
+// device holds it from the library's load until the process ends).  Host code
+// never passes `scratch` itself: it stands for the array only on the host
+// side; the per-device address comes from hipGetSymbolAddress at set-up.
+static __device__ __align__(256) uint8_t scratch[CP_NOALLOC_SCRATCH_BYTES];
+constexpr int kNoallocSlots = 2;  // pinned plan-staging slots of that path
+
 // Pinned host staging for plan uploads.  A slot is reused only after the
 // copy that last read it has completed (its event), so a host write never
 // races an in-flight DMA.
@@ -27,10 +34,15 @@ struct Stage {
   bool pending = false;
 };
 
-// Per-device state: the staging ring.
+// Per-device state: the staging ring; for the allocation-free path the
+// device address of `scratch` and its fixed-size staging slots (set up by
+// cp_noalloc_init).
 struct DeviceCtx {
   Stage ring[kRingSlots];
   int next = 0;
+  uint8_t* scratch_dev = nullptr;
+  Stage noalloc_ring[kNoallocSlots];
+  int noalloc_next = 0;
 };
 
 std::mutex g_mu;
@@ -174,18 +186,62 @@ int finish(hipError_t e, hipStream_t s) {
 }
 
 template <class T>
-void put(std::vector<uint8_t>& buf, size_t off, const std::vector<T>& v) {
-  if (!v.empty()) std::memcpy(buf.data() + off, v.data(), v.size() * sizeof(T));
+void put(uint8_t* buf, size_t off, const std::vector<T>& v) {
+  if (!v.empty()) std::memcpy(buf + off, v.data(), v.size() * sizeof(T));
 }
 
-void serialize(const Plan& p, std::vector<uint8_t>& buf) {
-  buf.resize(p.plan_bytes);
+// The plan's item lists at their workspace offsets (p.plan_bytes bytes).
+void serialize_into(const Plan& p, uint8_t* buf) {
   put(buf, p.off_prefill, p.prefill);
   put(buf, p.off_prefill_slots, p.prefill_slots);
   put(buf, p.off_prefill_wide, p.prefill_wide);
   put(buf, p.off_prefill_wide_slots, p.prefill_wide_slots);
   put(buf, p.off_decode, p.decode);
   put(buf, p.off_merge, p.merge);
+}
+
+void serialize(const Plan& p, std::vector<uint8_t>& buf) {
+  buf.resize(p.plan_bytes);
+  serialize_into(p, buf.data());
+}
+
+// The plan's lists, counts and workspace offsets as the caller-visible struct.
+void fill_plan(const Plan& p, cp_attn_plan& pl) {
+  pl.ws_bytes = (int64_t)p.ws_bytes;
+  pl.n_prefill_slots = (int32_t)p.prefill_slots.size();
+  pl.n_prefill_wide_slots = (int32_t)p.prefill_wide_slots.size();
+  pl.n_decode = (int32_t)p.decode.size();
+  pl.n_merge = (int32_t)p.merge.size();
+  pl.off_prefill = (int64_t)p.off_prefill;
+  pl.off_prefill_slots = (int64_t)p.off_prefill_slots;
+  pl.off_prefill_wide = (int64_t)p.off_prefill_wide;
+  pl.off_prefill_wide_slots = (int64_t)p.off_prefill_wide_slots;
+  pl.off_decode = (int64_t)p.off_decode;
+  pl.off_merge = (int64_t)p.off_merge;
+  pl.off_part_o = (int64_t)p.off_part_o;
+  pl.off_part_lse = (int64_t)p.off_part_lse;
+  pl.n_prefill_items = (int32_t)p.prefill.size();
+  pl.n_prefill_wide_items = (int32_t)p.prefill_wide.size();
+  pl.partial_rows = p.partial_rows;
+}
+
+// Allocation-free upload: writes the plan straight into one of the device's
+// fixed pinned slots (after the copy that last read it has completed) and
+// enqueues the copy into `dst`.  Requires g_mu held and plan_bytes within
+// the slot size.
+int upload_noalloc(DeviceCtx* c, void* dst, const Plan& p, hipStream_t s) {
+  Stage& st = c->noalloc_ring[c->noalloc_next];
+  c->noalloc_next = (c->noalloc_next + 1) % kNoallocSlots;
+  if (st.pending) {
+    if (hipEventSynchronize(st.ev) != hipSuccess) return CP_ERR_HIP;
+    st.pending = false;
+  }
+  serialize_into(p, static_cast<uint8_t*>(st.host));
+  if (hipMemcpyAsync(dst, st.host, p.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess)
+    return CP_ERR_HIP;
+  if (hipEventRecord(st.ev, s) != hipSuccess) return CP_ERR_HIP;
+  st.pending = true;
+  return CP_OK;
 }
 
 // One plan per thread, reused across calls (its vectors keep their capacity).
@@ -380,22 +436,7 @@ int cp_attn_prepare(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
     serialize(p, buf);
     const int rc = upload(ws, buf.data(), buf.size(), reinterpret_cast<hipStream_t>(stream));
     if (rc != CP_OK) return rc;
-    pl.ws_bytes = (int64_t)p.ws_bytes;
-    pl.n_prefill_slots = (int32_t)p.prefill_slots.size();
-    pl.n_prefill_wide_slots = (int32_t)p.prefill_wide_slots.size();
-    pl.n_decode = (int32_t)p.decode.size();
-    pl.n_merge = (int32_t)p.merge.size();
-    pl.off_prefill = (int64_t)p.off_prefill;
-    pl.off_prefill_slots = (int64_t)p.off_prefill_slots;
-    pl.off_prefill_wide = (int64_t)p.off_prefill_wide;
-    pl.off_prefill_wide_slots = (int64_t)p.off_prefill_wide_slots;
-    pl.off_decode = (int64_t)p.off_decode;
-    pl.off_merge = (int64_t)p.off_merge;
-    pl.off_part_o = (int64_t)p.off_part_o;
-    pl.off_part_lse = (int64_t)p.off_part_lse;
-    pl.n_prefill_items = (int32_t)p.prefill.size();
-    pl.n_prefill_wide_items = (int32_t)p.prefill_wide.size();
-    pl.partial_rows = p.partial_rows;
+    fill_plan(p, pl);
     *plan = pl;
     return CP_OK;
   } catch (...) {
@@ -510,6 +551,76 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
   const int rc = cp_attn_prepare(desc, rows, n_rows, ws, ws_bytes, stream, &plan);
   if (rc != CP_OK) return rc;
   return cp_attn_run(&plan, q, k_cache, v_cache, block_tables, out, ws, ws_bytes, stream);
+}
+
+int cp_noalloc_init(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  int err = CP_OK;
+  DeviceCtx* c = device_ctx(&err);
+  if (!c) return err;
+  if (c->scratch_dev) return CP_OK;
+  for (Stage& st : c->noalloc_ring) {
+    if (!st.host) {
+      if (hipHostMalloc(&st.host, CP_NOALLOC_PLAN_BYTES, hipHostMallocDefault) != hipSuccess) {
+        st.host = nullptr;
+        return CP_ERR_HIP;
+      }
+      st.cap = CP_NOALLOC_PLAN_BYTES;
+    }
+    if (!st.ev && hipEventCreateWithFlags(&st.ev, hipEventDisableTiming) != hipSuccess) {
+      st.ev = nullptr;
+      return CP_ERR_HIP;
+    }
+  }
+  void* addr = nullptr;
+  if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return CP_ERR_HIP;
+  if (!aligned(addr, 256)) return CP_ERR_HIP;
+  c->scratch_dev = static_cast<uint8_t*>(addr);
+  return CP_OK;
+}
+
+int cp_attn_mixed_noalloc(const cp_attn_desc* desc, const void* q, const void* k_cache,
+                          const void* v_cache, const int32_t* block_tables,
+                          const cp_row_meta* rows, int32_t n_rows, void* out, void* stream) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  cp_attn_plan pl{};
+  pl.desc = *desc;
+  pl.tokens = total_tokens(rows, n_rows);
+  if (pl.tokens == 0) return CP_OK;
+  if (!q || !k_cache || !v_cache || !block_tables || !out) return CP_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
+      !aligned(block_tables, 4))
+    return CP_ERR_INVALID_ARG;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  try {
+    // plan first: the size limits are host-side facts, checked before the
+    // device is touched
+    Plan& p = thread_plan();
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    if (p.ws_bytes > CP_NOALLOC_SCRATCH_BYTES || p.plan_bytes > CP_NOALLOC_PLAN_BYTES)
+      return CP_ERR_WORKSPACE;
+    fill_plan(p, pl);
+    uint8_t* ws = nullptr;
+    {
+      std::lock_guard<std::mutex> lk(g_mu);
+      int err = CP_OK;
+      DeviceCtx* c = device_ctx(&err);
+      if (!c) return err;
+      if (!c->scratch_dev) return CP_ERR_INVALID_ARG;  // cp_noalloc_init not called here
+      if (debug_mode()) {
+        const int rc = debug_check_tables(desc, block_tables, rows, n_rows, s);
+        if (rc != CP_OK) return rc;
+      }
+      ws = c->scratch_dev;
+      const int rc = upload_noalloc(c, ws, p, s);
+      if (rc != CP_OK) return rc;
+    }
+    return cp_attn_run(&pl, q, k_cache, v_cache, block_tables, out, ws, CP_NOALLOC_SCRATCH_BYTES,
+                       stream);
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
 }
 
 int cp_profile_begin(void) {
