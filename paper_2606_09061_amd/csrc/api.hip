@@ -5,6 +5,7 @@
 #include <cstring>
 #include <mutex>
 #include <new>
+#include <thread>
 #include <vector>
 
 #include "cp_attn.h"
@@ -24,15 +25,79 @@ constexpr int kRingSlots = 8;
 static __device__ __align__(256) uint8_t scratch[CP_NOALLOC_SCRATCH_BYTES];
 constexpr int kNoallocSlots = 2;  // pinned plan-staging slots of that path
 
-// Pinned host staging for plan uploads.  A slot is reused only after the
-// copy that last read it has completed (its event), so a host write never
-// races an in-flight DMA.
+// Pinned host staging for plan uploads: fine-grained (coherent) host memory
+// that the plan-copy kernel reads directly.  A call takes a slot (busy),
+// enqueues the copy and, after its last launch, records the slot's event and
+// frees it; the slot is written again only after that event, so a host write
+// never races a GPU read.
 struct Stage {
   void* host = nullptr;
+  const void* dev = nullptr;  // the same memory as the GPU addresses it
   size_t cap = 0;
   hipEvent_t ev = nullptr;
   bool pending = false;
+  bool busy = false;
 };
+constexpr size_t kStageMinBytes = 1u << 20;
+
+// Copies n16 16-byte words of a staged plan from pinned host memory into the
+// workspace: a workgroup per 8 words x 1024 threads, each thread's loads all
+// in flight before its stores (one host round trip per workgroup).  Replaces
+// hipMemcpyAsync, which sends copies above 16 KB to the DMA engine and leaves
+// the GPU idle for ~24 us before the next kernel.
+constexpr int kCopyPer = 8;
+__global__ __launch_bounds__(1024) void plan_copy_kernel(const uint4* __restrict__ src,
+                                                         uint4* __restrict__ dst, int n16) {
+  const int base = blockIdx.x * (kCopyPer * 1024) + (int)threadIdx.x;
+  uint4 v[kCopyPer];
+#pragma unroll
+  for (int k = 0; k < kCopyPer; ++k) {
+    const int i = base + k * 1024;
+    if (i < n16) v[k] = src[i];
+  }
+#pragma unroll
+  for (int k = 0; k < kCopyPer; ++k) {
+    const int i = base + k * 1024;
+    if (i < n16) dst[i] = v[k];
+  }
+}
+
+// Allocates (or grows) a slot's pinned buffer; the slot's last copy must be done.
+int stage_reserve(Stage& st, size_t bytes) {
+  if (!st.ev && hipEventCreateWithFlags(&st.ev, hipEventDisableTiming) != hipSuccess) {
+    st.ev = nullptr;
+    return CP_ERR_HIP;
+  }
+  if (st.cap >= bytes) return CP_OK;
+  if (st.host) (void)hipHostFree(st.host);
+  st.host = nullptr;
+  st.dev = nullptr;
+  st.cap = 0;
+  size_t cap = kStageMinBytes;
+  while (cap < bytes) cap *= 2;
+  if (hipHostMalloc(&st.host, cap, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
+    st.host = nullptr;
+    return CP_ERR_HIP;
+  }
+  void* d = nullptr;
+  if (hipHostGetDevicePointer(&d, st.host, 0) != hipSuccess || !d) {
+    (void)hipHostFree(st.host);
+    st.host = nullptr;
+    return CP_ERR_HIP;
+  }
+  st.dev = d;
+  st.cap = cap;
+  return CP_OK;
+}
+
+// Enqueues the copy of a staged slot's first `bytes` (a multiple of 16) into dst.
+int launch_plan_copy(const Stage& st, void* dst, size_t bytes, hipStream_t s) {
+  const int n16 = (int)(bytes / 16);
+  const int grid = (n16 + kCopyPer * 1024 - 1) / (kCopyPer * 1024);
+  hipLaunchKernelGGL(plan_copy_kernel, dim3(grid), dim3(1024), 0, s,
+                     static_cast<const uint4*>(st.dev), static_cast<uint4*>(dst), n16);
+  return hipGetLastError() == hipSuccess ? CP_OK : CP_ERR_HIP;
+}
 
 // Per-device state: the staging ring; for the allocation-free path the
 // device address of `scratch` and its fixed-size staging slots (set up by
@@ -107,34 +172,53 @@ DeviceCtx* device_ctx(int* err) {
   return g_devs[dev];
 }
 
-int upload(void* dst, const void* src, size_t bytes, hipStream_t s) {
+// Takes a free ring slot of the current device (waiting for its previous
+// copy if that is still pending), fills it through `fill(host)` and enqueues
+// the plan copy into dst.  The slot stays busy until release_stage.
+template <class Fill>
+int upload(void* dst, size_t bytes, hipStream_t s, Stage** taken, Fill&& fill) {
+  *taken = nullptr;
   if (bytes == 0) return CP_OK;
+  for (;;) {
+    std::unique_lock<std::mutex> lk(g_mu);
+    int err = CP_OK;
+    DeviceCtx* c = device_ctx(&err);
+    if (!c) return err;
+    Stage* st = nullptr;
+    for (int k = 0; k < kRingSlots && !st; ++k) {
+      Stage& cand = c->ring[(c->next + k) % kRingSlots];
+      if (!cand.busy) {
+        st = &cand;
+        c->next = (c->next + k + 1) % kRingSlots;
+      }
+    }
+    if (!st) {  // every slot inside another thread's call: let one finish
+      lk.unlock();
+      std::this_thread::yield();
+      continue;
+    }
+    if (st->pending) {
+      if (hipEventSynchronize(st->ev) != hipSuccess) return CP_ERR_HIP;
+      st->pending = false;
+    }
+    const int rc = stage_reserve(*st, bytes);
+    if (rc != CP_OK) return rc;
+    fill(static_cast<uint8_t*>(st->host));
+    if (launch_plan_copy(*st, dst, bytes, s) != CP_OK) return CP_ERR_HIP;
+    st->busy = true;
+    *taken = st;
+    return CP_OK;
+  }
+}
+
+// After the call's last launch: the slot's event marks when its copy (and
+// everything before it on the stream) is done; the slot is free again.
+int release_stage(Stage* st, hipStream_t s) {
+  if (!st) return CP_OK;
   std::lock_guard<std::mutex> lk(g_mu);
-  int err = CP_OK;
-  DeviceCtx* c = device_ctx(&err);
-  if (!c) return err;
-  Stage& st = c->ring[c->next];
-  c->next = (c->next + 1) % kRingSlots;
-  if (st.pending) {
-    if (hipEventSynchronize(st.ev) != hipSuccess) return CP_ERR_HIP;
-    st.pending = false;
-  }
-  if (!st.ev && hipEventCreateWithFlags(&st.ev, hipEventDisableTiming) != hipSuccess)
-    return CP_ERR_HIP;
-  if (st.cap < bytes) {
-    if (st.host) (void)hipHostFree(st.host);
-    st.host = nullptr;
-    st.cap = 0;
-    size_t cap = 64 << 10;
-    while (cap < bytes) cap *= 2;
-    if (hipHostMalloc(&st.host, cap, hipHostMallocDefault) != hipSuccess) return CP_ERR_HIP;
-    st.cap = cap;
-  }
-  std::memcpy(st.host, src, bytes);
-  if (hipMemcpyAsync(dst, st.host, bytes, hipMemcpyHostToDevice, s) != hipSuccess)
-    return CP_ERR_HIP;
-  if (hipEventRecord(st.ev, s) != hipSuccess) return CP_ERR_HIP;
-  st.pending = true;
+  st->busy = false;
+  if (hipEventRecord(st->ev, s) != hipSuccess) return CP_ERR_HIP;
+  st->pending = true;
   return CP_OK;
 }
 
@@ -200,11 +284,6 @@ void serialize_into(const Plan& p, uint8_t* buf) {
   put(buf, p.off_merge, p.merge);
 }
 
-void serialize(const Plan& p, std::vector<uint8_t>& buf) {
-  buf.resize(p.plan_bytes);
-  serialize_into(p, buf.data());
-}
-
 // The plan's lists, counts and workspace offsets as the caller-visible struct.
 void fill_plan(const Plan& p, cp_attn_plan& pl) {
   pl.ws_bytes = (int64_t)p.ws_bytes;
@@ -227,9 +306,9 @@ void fill_plan(const Plan& p, cp_attn_plan& pl) {
 
 // Allocation-free upload: writes the plan straight into one of the device's
 // fixed pinned slots (after the copy that last read it has completed) and
-// enqueues the copy into `dst`.  Requires g_mu held and plan_bytes within
-// the slot size.
-int upload_noalloc(DeviceCtx* c, void* dst, const Plan& p, hipStream_t s) {
+// enqueues the copy into `dst`; *taken is released by the caller after its
+// last launch.  Requires g_mu held and plan_bytes within the slot size.
+int upload_noalloc(DeviceCtx* c, void* dst, const Plan& p, hipStream_t s, Stage** taken) {
   Stage& st = c->noalloc_ring[c->noalloc_next];
   c->noalloc_next = (c->noalloc_next + 1) % kNoallocSlots;
   if (st.pending) {
@@ -237,10 +316,9 @@ int upload_noalloc(DeviceCtx* c, void* dst, const Plan& p, hipStream_t s) {
     st.pending = false;
   }
   serialize_into(p, static_cast<uint8_t*>(st.host));
-  if (hipMemcpyAsync(dst, st.host, p.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess)
-    return CP_ERR_HIP;
-  if (hipEventRecord(st.ev, s) != hipSuccess) return CP_ERR_HIP;
-  st.pending = true;
+  if (launch_plan_copy(st, dst, p.plan_bytes, s) != CP_OK) return CP_ERR_HIP;
+  st.busy = true;
+  *taken = &st;
   return CP_OK;
 }
 
@@ -398,25 +476,39 @@ int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new,
     a.hkv = desc->num_kv_heads;
     a.mbr = desc->max_blocks_per_req;
     const AppendInline* inl = nullptr;
+    Stage* st = nullptr;
     if (a.n_items <= kAppendInlineItems) {
       thread_local AppendInline buf;
       std::memcpy(buf.items, p.items.data(), p.items.size() * sizeof(AppendItem));
       inl = &buf;
     } else {
-      const int rc = upload(ws, p.items.data(), p.items.size() * sizeof(AppendItem), s);
+      const size_t bytes = p.items.size() * sizeof(AppendItem);
+      const int rc = upload(ws, bytes, s, &st, [&](uint8_t* h) {
+        std::memcpy(h, p.items.data(), bytes);
+      });
       if (rc != CP_OK) return rc;
     }
     const long pi = prof_open(0, s);
     const hipError_t e = launch_append(desc->head_dim, desc->block_size, a, inl, s);
     prof_close(pi, s);
-    return finish(e, s);
+    const int rs = release_stage(st, s);
+    const int rf = finish(e, s);
+    return rf != CP_OK ? rf : rs;
   } catch (...) {
     return CP_ERR_INVALID_ARG;
   }
 }
 
-int cp_attn_prepare(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows, void* ws,
-                    size_t ws_bytes, void* stream, cp_attn_plan* plan) {
+}  // extern "C"
+
+namespace {
+
+// cp_attn_prepare, leaving the plan's staging slot busy in *st (released by
+// the caller after its last launch, so the slot's event follows the kernels
+// rather than sitting between the copy and the first of them).
+int prepare_impl(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows, void* ws,
+                 size_t ws_bytes, hipStream_t s, cp_attn_plan* plan, Stage** st) {
+  *st = nullptr;
   if (!plan) return CP_ERR_INVALID_ARG;
   const int v = validate(desc, rows, n_rows);
   if (v != CP_OK) return v;
@@ -432,9 +524,7 @@ int cp_attn_prepare(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
     Plan& p = thread_plan();
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
     if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
-    thread_local std::vector<uint8_t> buf;
-    serialize(p, buf);
-    const int rc = upload(ws, buf.data(), buf.size(), reinterpret_cast<hipStream_t>(stream));
+    const int rc = upload(ws, p.plan_bytes, s, st, [&](uint8_t* h) { serialize_into(p, h); });
     if (rc != CP_OK) return rc;
     fill_plan(p, pl);
     *plan = pl;
@@ -442,6 +532,19 @@ int cp_attn_prepare(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
   } catch (...) {
     return CP_ERR_INVALID_ARG;
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+int cp_attn_prepare(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows, void* ws,
+                    size_t ws_bytes, void* stream, cp_attn_plan* plan) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Stage* st = nullptr;
+  const int rc = prepare_impl(desc, rows, n_rows, ws, ws_bytes, s, plan, &st);
+  const int rs = release_stage(st, s);
+  return rc != CP_OK ? rc : rs;
 }
 
 int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, const void* v_cache,
@@ -548,9 +651,16 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
     if (rc != CP_OK) return rc;
   }
   cp_attn_plan plan;
-  const int rc = cp_attn_prepare(desc, rows, n_rows, ws, ws_bytes, stream, &plan);
-  if (rc != CP_OK) return rc;
-  return cp_attn_run(&plan, q, k_cache, v_cache, block_tables, out, ws, ws_bytes, stream);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Stage* st = nullptr;
+  const int rc = prepare_impl(desc, rows, n_rows, ws, ws_bytes, s, &plan, &st);
+  if (rc != CP_OK) {
+    (void)release_stage(st, s);
+    return rc;
+  }
+  const int rr = cp_attn_run(&plan, q, k_cache, v_cache, block_tables, out, ws, ws_bytes, stream);
+  const int rs = release_stage(st, s);
+  return rr != CP_OK ? rr : rs;
 }
 
 int cp_noalloc_init(void) {
@@ -560,17 +670,8 @@ int cp_noalloc_init(void) {
   if (!c) return err;
   if (c->scratch_dev) return CP_OK;
   for (Stage& st : c->noalloc_ring) {
-    if (!st.host) {
-      if (hipHostMalloc(&st.host, CP_NOALLOC_PLAN_BYTES, hipHostMallocDefault) != hipSuccess) {
-        st.host = nullptr;
-        return CP_ERR_HIP;
-      }
-      st.cap = CP_NOALLOC_PLAN_BYTES;
-    }
-    if (!st.ev && hipEventCreateWithFlags(&st.ev, hipEventDisableTiming) != hipSuccess) {
-      st.ev = nullptr;
-      return CP_ERR_HIP;
-    }
+    const int rc = stage_reserve(st, CP_NOALLOC_PLAN_BYTES);
+    if (rc != CP_OK) return rc;
   }
   void* addr = nullptr;
   if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return CP_ERR_HIP;
@@ -602,6 +703,7 @@ int cp_attn_mixed_noalloc(const cp_attn_desc* desc, const void* q, const void* k
       return CP_ERR_WORKSPACE;
     fill_plan(p, pl);
     uint8_t* ws = nullptr;
+    Stage* st = nullptr;
     {
       std::lock_guard<std::mutex> lk(g_mu);
       int err = CP_OK;
@@ -613,11 +715,13 @@ int cp_attn_mixed_noalloc(const cp_attn_desc* desc, const void* q, const void* k
         if (rc != CP_OK) return rc;
       }
       ws = c->scratch_dev;
-      const int rc = upload_noalloc(c, ws, p, s);
+      const int rc = upload_noalloc(c, ws, p, s, &st);
       if (rc != CP_OK) return rc;
     }
-    return cp_attn_run(&pl, q, k_cache, v_cache, block_tables, out, ws, CP_NOALLOC_SCRATCH_BYTES,
-                       stream);
+    const int rr = cp_attn_run(&pl, q, k_cache, v_cache, block_tables, out, ws,
+                               CP_NOALLOC_SCRATCH_BYTES, stream);
+    const int rs = release_stage(st, s);
+    return rr != CP_OK ? rr : rs;
   } catch (...) {
     return CP_ERR_INVALID_ARG;
   }

@@ -39,18 +39,21 @@ void add_merge(Plan& p, int32_t tok0, int32_t n_tok, int32_t ns, int32_t part0, 
 // with idle slots (-1).
 void order_for_xcds(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_xcds,
                     PlanScratch& sc, std::vector<int32_t>& slots) {
-  using detail::Slot;
   slots.clear();
   auto& groups = sc.groups;
   groups.clear();
+  int64_t max_cost = 0;
   for (int32_t c = 0; c < (int32_t)sc.chunks.size(); ++c) {
     const detail::Chunk& ch = sc.chunks[c];
     if (ch.wide != wide) continue;
     for (int32_t s = 0; s < ch.max_ns; ++s) {
       int64_t gc = 0;
       for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i)
-        if (sc.tiles[i].ns > s) gc += cost[sc.tiles[i].item0 + s];
-      for (int32_t h = 0; h < Hkv; ++h) groups.push_back({c, h, s, gc});
+        if (sc.tiles[i].ns > s) {
+          gc += cost[sc.tiles[i].item0 + s];
+          max_cost = std::max(max_cost, cost[sc.tiles[i].item0 + s]);
+        }
+      for (int32_t h = 0; h < Hkv; ++h) groups.push_back({c, h, s, gc, 0});
     }
   }
   if (groups.empty()) return;
@@ -58,28 +61,46 @@ void order_for_xcds(bool wide, const std::vector<int64_t>& cost, int Hkv, int nu
   std::stable_sort(groups.begin(), groups.end(),
                    [](const detail::Group& a, const detail::Group& b) { return a.cost > b.cost; });
   sc.load.assign(X, 0);
-  if ((int)sc.lists.size() < X) sc.lists.resize(X);
-  for (int x = 0; x < X; ++x) sc.lists[x].clear();
-  for (const detail::Group& g : groups) {
-    const int x = (int)(std::min_element(sc.load.begin(), sc.load.end()) - sc.load.begin());
-    sc.load[x] += g.cost;
-    const detail::Chunk& ch = sc.chunks[g.chunk];
-    for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i) {
-      const detail::Tile& tl = sc.tiles[i];
-      if (tl.ns <= g.split) continue;
-      const int32_t item = tl.item0 + g.split;
-      sc.lists[x].push_back({item * Hkv + g.kvh, cost[item]});
+  for (detail::Group& g : groups) {
+    g.xcd = (int32_t)(std::min_element(sc.load.begin(), sc.load.end()) - sc.load.begin());
+    sc.load[g.xcd] += g.cost;
+  }
+  // Each XCD's slots, longest first, equal costs in the order their groups
+  // were dealt: a counting sort keyed on (XCD, max_cost - cost).
+  const int64_t K = max_cost + 1;
+  auto& pos = sc.count;
+  pos.assign((size_t)X * K + 1, 0);
+  auto for_each_slot = [&](auto&& f) {
+    for (const detail::Group& g : groups) {
+      const detail::Chunk& ch = sc.chunks[g.chunk];
+      for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i) {
+        const detail::Tile& tl = sc.tiles[i];
+        if (tl.ns <= g.split) continue;
+        const int32_t item = tl.item0 + g.split;
+        f((size_t)g.xcd * K + (max_cost - cost[item]), item * Hkv + g.kvh);
+      }
     }
+  };
+  for_each_slot([&](size_t key, int32_t) { ++pos[key + 1]; });
+  auto& len = sc.load;  // slots per XCD
+  len.assign(X, 0);
+  for (int x = 0; x < X; ++x)
+    for (int64_t k = 0; k < K; ++k) len[x] += pos[(size_t)x * K + k + 1];
+  for (size_t k = 1; k < pos.size(); ++k) pos[k] += pos[k - 1];
+  auto& flat = sc.flat;
+  flat.resize((size_t)pos.back());
+  for_each_slot([&](size_t key, int32_t slot) { flat[(size_t)pos[key]++] = slot; });
+  // pos[x*K] is now the end of XCD x-1's run; its start is the sum of the lengths before it
+  const int64_t longest = *std::max_element(len.begin(), len.end());
+  slots.reserve((size_t)longest * X);
+  int64_t start[64];
+  int64_t acc = 0;
+  for (int x = 0; x < X && x < 64; ++x) {
+    start[x] = acc;
+    acc += len[x];
   }
-  size_t longest = 0;
-  for (int x = 0; x < X; ++x) {
-    auto& l = sc.lists[x];
-    std::stable_sort(l.begin(), l.end(), [](const Slot& a, const Slot& b) { return a.cost > b.cost; });
-    longest = std::max(longest, l.size());
-  }
-  slots.reserve(longest * X);
-  for (size_t k = 0; k < longest; ++k)
-    for (int x = 0; x < X; ++x) slots.push_back(k < sc.lists[x].size() ? sc.lists[x][k].slot : -1);
+  for (int64_t k = 0; k < longest; ++k)
+    for (int x = 0; x < X; ++x) slots.push_back(k < len[x] ? flat[(size_t)(start[x] + k)] : -1);
   // trailing idle slots change no XCD assignment
   while (!slots.empty() && slots.back() < 0) slots.pop_back();
 }
@@ -179,7 +200,7 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_DECODE_TARGET_ITEMS")) t.decode_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_TARGET_ITEMS")) t.prefill_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_MIN_SPLIT")) t.prefill_min_split = std::max(1, atoi(s));
-  if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::max(1, atoi(s));
+  if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::min(64, std::max(1, atoi(s)));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_ROWS"))
     t.prefill_wide_min_rows = std::max<int64_t>(1, atoll(s));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_KEYS"))
@@ -229,34 +250,68 @@ static int64_t choose_split_steps(const cp_attn_desc& d, const Tuning& t,
   // merge: one step of a wide tile is ~2 us at the kernel's rate, in which
   // HBM moves ~10 MB; a partial row is written and read once, (D + 1) fp32
   const double merge_bytes_per_step = 10.0e6 * d.head_dim / 128.0;
-  int64_t best_s = max_steps;
-  double best = -1.0;
-  for (const int64_t S : cand) {
+  // Each candidate reduces to (cost, count) groups per tile width: a tile's
+  // splits are all S steps long except its last.  The unsplit grid goes
+  // first; a candidate whose lower bound -- per width, the larger of the
+  // longest item and the average slot load, plus its merge traffic --
+  // cannot beat the best estimate so far is not simulated.
+  // cuts of a tile are the multiples of split_keys in (0, cut_lim], with
+  // cut_lim = min(its first query's step start, kv_end - 1)
+  auto& cut_lim = sc.cut_lim;
+  cut_lim.resize(tiles.size());
+  for (size_t i = 0; i < tiles.size(); ++i)
+    cut_lim[i] = (uint32_t)std::min<int64_t>((tiles[i].pos0 / kPrefillKeys) * (int64_t)kPrefillKeys,
+                                             tiles[i].kv_end - 1);
+  auto cuts_of = [&](size_t i, uint32_t split_keys) -> int64_t {
+    return cut_lim[i] < split_keys ? 0 : cut_lim[i] / split_keys;
+  };
+  auto evaluate = [&](int64_t S, double best) -> double {
     const int64_t split_keys = S * kPrefillKeys;
-    double est = 0.0;
+    const uint32_t sk32 = (uint32_t)std::min<int64_t>(split_keys, UINT32_MAX);
+    auto& groups = sc.groups2;
+    double lb = 0.0;
     int64_t partial_rows = 0;
-    for (int wide = 0; wide < 2; ++wide) {
-      if (!has[wide]) continue;
-      auto& groups = sc.groups2;
+    int64_t total[2] = {0, 0}, longest[2] = {0, 0}, full[2] = {0, 0};
+    for (size_t i = 0; i < tiles.size(); ++i) {
+      const detail::Tile& tl = tiles[i];
+      const int w = tl.wide ? 1 : 0;
+      const int64_t cuts = cuts_of(i, sk32);
+      const int64_t tail = ceil_div(tl.kv_end - cuts * split_keys, kPrefillKeys) + kItemOverhead;
+      full[w] += cuts;
+      total[w] += (tail + cuts * (S + kItemOverhead)) * Hkv;
+      longest[w] = std::max(longest[w], cuts > 0 ? std::max(tail, S + kItemOverhead) : tail);
+      if (cuts > 0) partial_rows += Hkv * (1 + cuts) * tl.n_tok * G;
+    }
+    const double merge = (double)partial_rows * (d.head_dim + 1) * 8 / merge_bytes_per_step;
+    for (int w = 0; w < 2; ++w) {
+      if (!has[w]) continue;
+      const int64_t slots = (int64_t)t.num_cus * (w ? 1 : 2);
+      lb += (double)std::max(longest[w], ceil_div(total[w], slots));
+    }
+    if (best >= 0 && lb + merge > best) return -1.0;  // cannot win (ties still can)
+    double est = merge;
+    for (int w = 0; w < 2; ++w) {
+      if (!has[w]) continue;
       groups.clear();
-      int64_t full = 0;  // splits of exactly S steps
-      for (const detail::Tile& tl : tiles) {
-        if ((int)tl.wide != wide) continue;
-        // cuts are the multiples of split_keys in (0, min(last_cut, kv_end - 1)]
-        const int64_t last_cut = (tl.pos0 / kPrefillKeys) * (int64_t)kPrefillKeys;
-        const int64_t cuts = std::min<int64_t>(last_cut, tl.kv_end - 1) / split_keys;
-        const int64_t ns = 1 + cuts;
-        const int64_t start = cuts * split_keys;
-        full += cuts;
-        groups.push_back({ceil_div(tl.kv_end - start, kPrefillKeys) + kItemOverhead, Hkv});
-        if (ns > 1) partial_rows += Hkv * ns * tl.n_tok * G;
+      for (size_t i = 0; i < tiles.size(); ++i) {
+        const detail::Tile& tl = tiles[i];
+        if ((int)tl.wide != w) continue;
+        const int64_t cuts = cuts_of(i, sk32);
+        groups.push_back({ceil_div(tl.kv_end - cuts * split_keys, kPrefillKeys) + kItemOverhead, Hkv});
       }
-      if (full > 0) groups.push_back({S + kItemOverhead, full * Hkv});
-      const int64_t slots = (int64_t)t.num_cus * (wide ? 1 : 2);
+      if (full[w] > 0) groups.push_back({S + kItemOverhead, full[w] * Hkv});
+      const int64_t slots = (int64_t)t.num_cus * (w ? 1 : 2);
       est += (double)lpt_makespan(groups, slots, sc.load_hist);
     }
-    est += (double)partial_rows * (d.head_dim + 1) * 8 / merge_bytes_per_step;
-    if (best < 0 || est < best) {
+    return est;
+  };
+  // the smallest S among those with the least estimate (candidates ascend)
+  int64_t best_s = max_steps;
+  double best = evaluate(max_steps, -1.0);
+  for (const int64_t S : cand) {
+    if (S == max_steps) break;
+    const double est = evaluate(S, best);
+    if (est >= 0 && (est < best || (est == best && best_s == max_steps))) {
       best = est;
       best_s = S;
     }
@@ -364,6 +419,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   }
   if ((int64_t)std::max(p.prefill.size(), p.prefill_wide.size()) * Hkv > INT32_MAX)
     throw std::length_error("prefill slot index overflows int32");
+  if (t.num_xcds > 64) throw std::length_error("more than 64 XCDs");
   order_for_xcds(false, sc.item_cost[0], Hkv, t.num_xcds, sc, p.prefill_slots);
   order_for_xcds(true, sc.item_cost[1], Hkv, t.num_xcds, sc, p.prefill_wide_slots);
 

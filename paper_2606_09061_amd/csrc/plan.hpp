@@ -100,10 +100,7 @@ struct Chunk {        // the tiles of one chunk, cut on one split grid
 struct Group {        // items sharing one kv head's K/V range: (chunk, kv head, split)
   int32_t chunk, kvh, split;
   int64_t cost;
-};
-struct Slot {
-  int32_t slot;
-  int64_t cost;
+  int32_t xcd;        // the XCD it is dealt to
 };
 }  // namespace detail
 
@@ -117,9 +114,10 @@ struct PlanScratch {
   std::vector<int64_t> item_cost[2];
   std::vector<detail::Group> groups;
   std::vector<int64_t> load;
-  std::vector<std::vector<detail::Slot>> lists;
   std::vector<int64_t> count;
+  std::vector<int32_t> flat;                          // slots grouped by XCD, longest first
   std::vector<int64_t> candidates;                    // split lengths to score
+  std::vector<uint32_t> cut_lim;                      // per tile: last key a split may start at
   std::vector<std::pair<int64_t, int64_t>> groups2;  // (cost, count) of one split candidate
   std::vector<std::pair<int64_t, int64_t>> load_hist; // (slot load, slots), by load
 };
