@@ -262,15 +262,18 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
                 evs[i + 1].record(stream)
         if mode != "steps":
             evs[1].record(stream)
+        issue_s = time.perf_counter() - w0   # host time to enqueue the n steps
         torch.cuda.synchronize()
         wall_s = time.perf_counter() - w0
         prof_ = binding.profile_end() if mode == "kernels" else None
         per = (np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(n)])
                if mode == "steps" else None)
+        timed.issue_s = issue_s
         return float(evs[0].elapsed_time(evs[-1])), wall_s, per, prof_
 
     # headline region: only the two bracketing events
     total_ms, wall, _, _ = timed(steps_n, "total")
+    issue = timed.issue_s
     # per-step latencies (at least 100 steps), then per-kernel durations
     n_lat = max(steps_n, 100)
     _, _, per_step, _ = timed(n_lat, "steps")
@@ -344,6 +347,7 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
                        "p10": float(np.percentile(per_step, 10)),
                        "p90": float(np.percentile(per_step, 90)), "reps": n_lat},
         "wall_ms_per_step": wall * 1e3 / steps_n,
+        "host_issue_ms_per_step": issue * 1e3 / steps_n,
         "kernels": kern,
         "roofline": roof,
         "roofline_step": roof_step,

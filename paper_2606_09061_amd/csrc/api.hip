@@ -1,6 +1,8 @@
 // C ABI of libcpattn: validation, planning, plan upload and launches.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <chrono>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -26,77 +28,113 @@ static __device__ __align__(256) uint8_t scratch[CP_NOALLOC_SCRATCH_BYTES];
 constexpr int kNoallocSlots = 2;  // pinned plan-staging slots of that path
 
 // Pinned host staging for plan uploads: fine-grained (coherent) host memory
-// that the plan-copy kernel reads directly.  A call takes a slot (busy),
-// enqueues the copy and, after its last launch, records the slot's event and
-// frees it; the slot is written again only after that event, so a host write
-// never races a GPU read.
+// that the plan-copy kernel reads directly.  Each workgroup of that kernel,
+// once it has read its part of the slot, writes the call's sequence number
+// into the slot's completion words (fine-grained host memory too); a slot is
+// rewritten only after all of them show its last sequence number.  So a host
+// write never races a GPU read, whatever the stream, and no event sits
+// between the kernels (an event record costs the GPU 5-10 us of idle time).
+constexpr int kCopyBlocksMax = 16;      // workgroups of one plan copy
+constexpr size_t kStageHeader = 256;    // completion words ahead of the data
 struct Stage {
-  void* host = nullptr;
-  const void* dev = nullptr;  // the same memory as the GPU addresses it
+  void* base = nullptr;                 // allocation: [completion words][data]
+  uint8_t* host = nullptr;              // data, as the host writes it
+  const void* dev = nullptr;            // data, as the GPU addresses it
+  uint32_t* done_host = nullptr;        // kCopyBlocksMax completion words
+  uint32_t* done_dev = nullptr;
   size_t cap = 0;
-  hipEvent_t ev = nullptr;
-  bool pending = false;
+  uint32_t seq = 0;                     // sequence number of its last copy (0: none)
+  int blocks = 0;                       // workgroups of that copy
   bool busy = false;
 };
 constexpr size_t kStageMinBytes = 1u << 20;
 
 // Copies n16 16-byte words of a staged plan from pinned host memory into the
-// workspace: a workgroup per 8 words x 1024 threads, each thread's loads all
-// in flight before its stores (one host round trip per workgroup).  Replaces
-// hipMemcpyAsync, which sends copies above 16 KB to the DMA engine and leaves
-// the GPU idle for ~24 us before the next kernel.
+// workspace: each workgroup takes 128 KiB pieces (8 words per thread, all
+// loads in flight before the stores: one host round trip per piece), then
+// marks its part done with `seq`.  Replaces hipMemcpyAsync, which sends
+// copies above 16 KB to the DMA engine and leaves the GPU idle ~24 us.
 constexpr int kCopyPer = 8;
+constexpr int kCopyPiece = kCopyPer * 1024;
 __global__ __launch_bounds__(1024) void plan_copy_kernel(const uint4* __restrict__ src,
-                                                         uint4* __restrict__ dst, int n16) {
-  const int base = blockIdx.x * (kCopyPer * 1024) + (int)threadIdx.x;
-  uint4 v[kCopyPer];
+                                                         uint4* __restrict__ dst, int n16,
+                                                         uint32_t* __restrict__ done,
+                                                         uint32_t seq) {
+  for (int base = blockIdx.x * kCopyPiece + (int)threadIdx.x; base < n16;
+       base += gridDim.x * kCopyPiece) {
+    uint4 v[kCopyPer];
 #pragma unroll
-  for (int k = 0; k < kCopyPer; ++k) {
-    const int i = base + k * 1024;
-    if (i < n16) v[k] = src[i];
-  }
+    for (int k = 0; k < kCopyPer; ++k) {
+      const int i = base + k * 1024;
+      v[k] = i < n16 ? src[i] : make_uint4(0, 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first store
 #pragma unroll
-  for (int k = 0; k < kCopyPer; ++k) {
-    const int i = base + k * 1024;
-    if (i < n16) dst[i] = v[k];
+    for (int k = 0; k < kCopyPer; ++k) {
+      const int i = base + k * 1024;
+      if (i < n16) dst[i] = v[k];
+    }
   }
+  __syncthreads();  // every read of this workgroup has returned
+  if (threadIdx.x == 0)
+    __hip_atomic_store(done + blockIdx.x, seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
-// Allocates (or grows) a slot's pinned buffer; the slot's last copy must be done.
-int stage_reserve(Stage& st, size_t bytes) {
-  if (!st.ev && hipEventCreateWithFlags(&st.ev, hipEventDisableTiming) != hipSuccess) {
-    st.ev = nullptr;
-    return CP_ERR_HIP;
+// Waits until the slot's last copy has read it (normally long done: a slot
+// comes round again only several calls later).
+int wait_copied(const Stage& st) {
+  if (st.seq == 0) return CP_OK;
+  const auto t0 = std::chrono::steady_clock::now();
+  for (int b = 0; b < st.blocks; ++b) {
+    long spins = 0;
+    while (__atomic_load_n(&st.done_host[b], __ATOMIC_ACQUIRE) != st.seq) {
+      if (++spins % 256 == 0) {
+        std::this_thread::yield();
+        if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60)) return CP_ERR_HIP;
+      }
+    }
   }
+  return CP_OK;
+}
+
+// Allocates (or grows) a slot's pinned buffer; its last copy must be done.
+int stage_reserve(Stage& st, size_t bytes) {
   if (st.cap >= bytes) return CP_OK;
-  if (st.host) (void)hipHostFree(st.host);
-  st.host = nullptr;
-  st.dev = nullptr;
-  st.cap = 0;
+  if (st.base) (void)hipHostFree(st.base);
+  st = Stage{};
   size_t cap = kStageMinBytes;
   while (cap < bytes) cap *= 2;
-  if (hipHostMalloc(&st.host, cap, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
-    st.host = nullptr;
+  void* b = nullptr;
+  if (hipHostMalloc(&b, cap + kStageHeader, hipHostMallocMapped | hipHostMallocCoherent) !=
+      hipSuccess)
     return CP_ERR_HIP;
-  }
   void* d = nullptr;
-  if (hipHostGetDevicePointer(&d, st.host, 0) != hipSuccess || !d) {
-    (void)hipHostFree(st.host);
-    st.host = nullptr;
+  if (hipHostGetDevicePointer(&d, b, 0) != hipSuccess || !d) {
+    (void)hipHostFree(b);
     return CP_ERR_HIP;
   }
-  st.dev = d;
+  std::memset(b, 0, kStageHeader);
+  st.base = b;
+  st.done_host = static_cast<uint32_t*>(b);
+  st.done_dev = static_cast<uint32_t*>(d);
+  st.host = static_cast<uint8_t*>(b) + kStageHeader;
+  st.dev = static_cast<const uint8_t*>(d) + kStageHeader;
   st.cap = cap;
   return CP_OK;
 }
 
-// Enqueues the copy of a staged slot's first `bytes` (a multiple of 16) into dst.
-int launch_plan_copy(const Stage& st, void* dst, size_t bytes, hipStream_t s) {
+// Enqueues the copy of a staged slot's first `bytes` (a multiple of 16) into
+// dst under the next sequence number `seq` (never 0).
+int launch_plan_copy(Stage& st, void* dst, size_t bytes, uint32_t seq, hipStream_t s) {
   const int n16 = (int)(bytes / 16);
-  const int grid = (n16 + kCopyPer * 1024 - 1) / (kCopyPer * 1024);
+  const int grid = std::min(kCopyBlocksMax, (n16 + kCopyPiece - 1) / kCopyPiece);
   hipLaunchKernelGGL(plan_copy_kernel, dim3(grid), dim3(1024), 0, s,
-                     static_cast<const uint4*>(st.dev), static_cast<uint4*>(dst), n16);
-  return hipGetLastError() == hipSuccess ? CP_OK : CP_ERR_HIP;
+                     static_cast<const uint4*>(st.dev), static_cast<uint4*>(dst), n16, st.done_dev,
+                     seq);
+  if (hipGetLastError() != hipSuccess) return CP_ERR_HIP;
+  st.seq = seq;
+  st.blocks = grid;
+  return CP_OK;
 }
 
 // Per-device state: the staging ring; for the allocation-free path the
@@ -105,6 +143,7 @@ int launch_plan_copy(const Stage& st, void* dst, size_t bytes, hipStream_t s) {
 struct DeviceCtx {
   Stage ring[kRingSlots];
   int next = 0;
+  uint32_t seq = 0;  // sequence numbers of plan copies on this device
   uint8_t* scratch_dev = nullptr;
   Stage noalloc_ring[kNoallocSlots];
   int noalloc_next = 0;
@@ -160,6 +199,12 @@ int debug_check_tables(const cp_attn_desc* d, const int32_t* bt_dev, const cp_ro
 }
 
 // Requires g_mu held.
+uint32_t next_seq(DeviceCtx* c) {
+  if (++c->seq == 0) ++c->seq;
+  return c->seq;
+}
+
+// Requires g_mu held.
 DeviceCtx* device_ctx(int* err) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) {
@@ -197,28 +242,23 @@ int upload(void* dst, size_t bytes, hipStream_t s, Stage** taken, Fill&& fill) {
       std::this_thread::yield();
       continue;
     }
-    if (st->pending) {
-      if (hipEventSynchronize(st->ev) != hipSuccess) return CP_ERR_HIP;
-      st->pending = false;
-    }
-    const int rc = stage_reserve(*st, bytes);
+    int rc = wait_copied(*st);
+    if (rc == CP_OK) rc = stage_reserve(*st, bytes);
     if (rc != CP_OK) return rc;
-    fill(static_cast<uint8_t*>(st->host));
-    if (launch_plan_copy(*st, dst, bytes, s) != CP_OK) return CP_ERR_HIP;
+    fill(st->host);
+    if (launch_plan_copy(*st, dst, bytes, next_seq(c), s) != CP_OK) return CP_ERR_HIP;
     st->busy = true;
     *taken = st;
     return CP_OK;
   }
 }
 
-// After the call's last launch: the slot's event marks when its copy (and
-// everything before it on the stream) is done; the slot is free again.
-int release_stage(Stage* st, hipStream_t s) {
+// After the call's last launch the slot may be taken again (its completion
+// words guard the data until the copy has read it).
+int release_stage(Stage* st, hipStream_t) {
   if (!st) return CP_OK;
   std::lock_guard<std::mutex> lk(g_mu);
   st->busy = false;
-  if (hipEventRecord(st->ev, s) != hipSuccess) return CP_ERR_HIP;
-  st->pending = true;
   return CP_OK;
 }
 
@@ -311,12 +351,10 @@ void fill_plan(const Plan& p, cp_attn_plan& pl) {
 int upload_noalloc(DeviceCtx* c, void* dst, const Plan& p, hipStream_t s, Stage** taken) {
   Stage& st = c->noalloc_ring[c->noalloc_next];
   c->noalloc_next = (c->noalloc_next + 1) % kNoallocSlots;
-  if (st.pending) {
-    if (hipEventSynchronize(st.ev) != hipSuccess) return CP_ERR_HIP;
-    st.pending = false;
-  }
-  serialize_into(p, static_cast<uint8_t*>(st.host));
-  if (launch_plan_copy(st, dst, p.plan_bytes, s) != CP_OK) return CP_ERR_HIP;
+  const int rc = wait_copied(st);
+  if (rc != CP_OK) return rc;
+  serialize_into(p, st.host);
+  if (launch_plan_copy(st, dst, p.plan_bytes, next_seq(c), s) != CP_OK) return CP_ERR_HIP;
   st.busy = true;
   *taken = &st;
   return CP_OK;
