@@ -327,8 +327,10 @@ void serialize_into(const Plan& p, uint8_t* buf) {
 // The plan's lists, counts and workspace offsets as the caller-visible struct.
 void fill_plan(const Plan& p, cp_attn_plan& pl) {
   pl.ws_bytes = (int64_t)p.ws_bytes;
-  pl.n_prefill_slots = (int32_t)p.prefill_slots.size();
-  pl.n_prefill_wide_slots = (int32_t)p.prefill_wide_slots.size();
+  // workgroups of each prefill launch (their list offsets hold one entry more)
+  pl.n_prefill_slots = p.prefill_slots.empty() ? 0 : (int32_t)p.prefill_slots.size() - 1;
+  pl.n_prefill_wide_slots =
+      p.prefill_wide_slots.empty() ? 0 : (int32_t)p.prefill_wide_slots.size() - 1;
   pl.n_decode = (int32_t)p.decode.size();
   pl.n_merge = (int32_t)p.merge.size();
   pl.off_prefill = (int64_t)p.off_prefill;
@@ -423,7 +425,7 @@ int cp_plan_summary(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
     Plan& p = thread_plan();
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
     const int64_t hkv = desc->num_kv_heads;
-    counts[0] = (int64_t)(p.prefill.size() + p.prefill_wide.size()) * hkv;
+    counts[0] = (int64_t)(p.prefill.size() + p.prefill_wide.size());
     counts[1] = (int64_t)p.decode.size() * hkv;
     counts[2] = (int64_t)p.merge.size() * hkv;
     counts[3] = p.partial_rows;
@@ -456,15 +458,10 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
       }
       ++n;
     };
-    // prefill work in slot order (the order the kernels' workgroups take it)
-    for (int w = 1; w >= 0; --w) {
-      const auto& list = w ? p.prefill_wide : p.prefill;
-      for (int32_t slot : (w ? p.prefill_wide_slots : p.prefill_slots)) {
-        if (slot < 0) continue;
-        const PrefillItem& it = list[slot / hkv];
-        put_item(0, it.tok0, it.n_tok, it.pos0, it.req, slot % hkv, it.kv_begin, it.kv_end);
-      }
-    }
+    // prefill records, workgroup list after workgroup list
+    for (int w = 1; w >= 0; --w)
+      for (const PrefillRec& r : (w ? p.prefill_wide : p.prefill))
+        put_item(0, r.tok0, r.n_tok, r.pos0, r.req, r.kvh, r.kv_begin, r.kv_end);
     // position of a decode query: chunk_start + its index inside the row
     std::vector<int32_t> pos_of_tok;
     {
@@ -609,10 +606,10 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   // every list the kernels read lies inside the plan's workspace
   const int64_t D64 = desc->head_dim;
   const int64_t ends[8] = {
-      plan->off_prefill + (int64_t)plan->n_prefill_items * (int64_t)sizeof(PrefillItem),
-      plan->off_prefill_slots + (int64_t)plan->n_prefill_slots * 4,
-      plan->off_prefill_wide + (int64_t)plan->n_prefill_wide_items * (int64_t)sizeof(PrefillItem),
-      plan->off_prefill_wide_slots + (int64_t)plan->n_prefill_wide_slots * 4,
+      plan->off_prefill + (int64_t)plan->n_prefill_items * (int64_t)sizeof(PrefillRec),
+      plan->off_prefill_slots + ((int64_t)plan->n_prefill_slots + 1) * 4,
+      plan->off_prefill_wide + (int64_t)plan->n_prefill_wide_items * (int64_t)sizeof(PrefillRec),
+      plan->off_prefill_wide_slots + ((int64_t)plan->n_prefill_wide_slots + 1) * 4,
       plan->off_decode + (int64_t)plan->n_decode * (int64_t)sizeof(DecodeItem),
       plan->off_merge + (int64_t)plan->n_merge * (int64_t)sizeof(MergeGroup),
       plan->off_part_o + plan->partial_rows * D64 * 4,
@@ -622,12 +619,12 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* base = static_cast<uint8_t*>(ws);
   AttnArgs a;
-  a.prefill = reinterpret_cast<const PrefillItem*>(base + plan->off_prefill);
+  a.prefill = reinterpret_cast<const PrefillRec*>(base + plan->off_prefill);
   a.prefill_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_slots);
   a.n_prefill_slots = plan->n_prefill_slots;
   a.n_prefill_items = plan->n_prefill_items;
   a.n_prefill_wide_items = plan->n_prefill_wide_items;
-  a.prefill_wide = reinterpret_cast<const PrefillItem*>(base + plan->off_prefill_wide);
+  a.prefill_wide = reinterpret_cast<const PrefillRec*>(base + plan->off_prefill_wide);
   a.prefill_wide_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_wide_slots);
   a.n_prefill_wide_slots = plan->n_prefill_wide_slots;
   a.decode = reinterpret_cast<const DecodeItem*>(base + plan->off_decode);

@@ -31,17 +31,19 @@ void add_merge(Plan& p, int32_t tok0, int32_t n_tok, int32_t ns, int32_t part0, 
   }
 }
 
-// Orders the prefill slots of one item list (narrow or wide tiles) so that
-// slots sharing a K/V range -- the tiles of one chunk in one split, for one
-// kv head -- run on one XCD (workgroup i is dispatched to XCD i mod
-// num_xcds), and each XCD runs its slots longest first.  Groups are dealt to
-// the least-loaded XCD, largest group first; shorter XCD lists are padded
-// with idle slots (-1).
-void order_for_xcds(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_xcds,
-                    PlanScratch& sc, std::vector<int32_t>& slots) {
-  slots.clear();
+// Groups the prefill slots (item * Hkv + kv head) of one tile width by XCD
+// so that slots sharing a K/V range -- the tiles of one chunk in one split,
+// for one kv head -- run on one XCD (a workgroup runs on XCD w mod
+// num_xcds), each XCD's slots longest first.  Groups are dealt to the
+// least-loaded XCD, largest group first.  Result: sc.flat holds XCD 0's
+// slots, then XCD 1's, ...; sc.xcd_len[x] how many.
+void lists_by_xcd(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_xcds,
+                  PlanScratch& sc) {
   auto& groups = sc.groups;
   groups.clear();
+  const int X = std::max(1, num_xcds);
+  sc.xcd_len.assign(X, 0);
+  sc.flat.clear();
   int64_t max_cost = 0;
   for (int32_t c = 0; c < (int32_t)sc.chunks.size(); ++c) {
     const detail::Chunk& ch = sc.chunks[c];
@@ -57,7 +59,6 @@ void order_for_xcds(bool wide, const std::vector<int64_t>& cost, int Hkv, int nu
     }
   }
   if (groups.empty()) return;
-  const int X = std::max(1, num_xcds);
   std::stable_sort(groups.begin(), groups.end(),
                    [](const detail::Group& a, const detail::Group& b) { return a.cost > b.cost; });
   sc.load.assign(X, 0);
@@ -82,27 +83,71 @@ void order_for_xcds(bool wide, const std::vector<int64_t>& cost, int Hkv, int nu
     }
   };
   for_each_slot([&](size_t key, int32_t) { ++pos[key + 1]; });
-  auto& len = sc.load;  // slots per XCD
-  len.assign(X, 0);
   for (int x = 0; x < X; ++x)
-    for (int64_t k = 0; k < K; ++k) len[x] += pos[(size_t)x * K + k + 1];
+    for (int64_t k = 0; k < K; ++k) sc.xcd_len[x] += pos[(size_t)x * K + k + 1];
   for (size_t k = 1; k < pos.size(); ++k) pos[k] += pos[k - 1];
-  auto& flat = sc.flat;
-  flat.resize((size_t)pos.back());
-  for_each_slot([&](size_t key, int32_t slot) { flat[(size_t)pos[key]++] = slot; });
-  // pos[x*K] is now the end of XCD x-1's run; its start is the sum of the lengths before it
-  const int64_t longest = *std::max_element(len.begin(), len.end());
-  slots.reserve((size_t)longest * X);
-  int64_t start[64];
-  int64_t acc = 0;
-  for (int x = 0; x < X && x < 64; ++x) {
-    start[x] = acc;
-    acc += len[x];
+  sc.flat.resize((size_t)pos.back());
+  for_each_slot([&](size_t key, int32_t slot) { sc.flat[(size_t)pos[key]++] = slot; });
+}
+
+// Deals each XCD's slots (sc.flat, longest first) to the persistent
+// workgroups that run on that XCD -- workgroup w = k * X + x runs on XCD x --
+// each to the least-loaded one (longest processing time first; ties to the
+// lower k), and writes every workgroup's records, list after list, with the
+// list offsets.  wg_per_xcd <= 0: one workgroup per slot.
+void deal_to_workgroups(const std::vector<detail::PrefillItem>& items,
+                        const std::vector<int64_t>& cost, int Hkv, int num_xcds,
+                        int64_t wg_per_xcd, PlanScratch& sc, std::vector<PrefillRec>& recs,
+                        std::vector<int32_t>& off) {
+  recs.clear();
+  off.clear();
+  if (sc.flat.empty()) return;
+  const int X = std::max(1, num_xcds);
+  int64_t used = 0;  // workgroups per XCD that get a list
+  for (int x = 0; x < X; ++x)
+    used = std::max(used, wg_per_xcd > 0 ? std::min(wg_per_xcd, sc.xcd_len[x]) : sc.xcd_len[x]);
+  const int64_t n_wg = used * X;
+  sc.wg_of.resize(sc.flat.size());
+  auto& heap = sc.heap;
+  auto later = [](const std::pair<int64_t, int32_t>& a, const std::pair<int64_t, int32_t>& b) {
+    return a.first != b.first ? a.first > b.first : a.second > b.second;  // min-heap on (load, k)
+  };
+  int64_t start = 0;
+  for (int x = 0; x < X; ++x) {
+    const int64_t len = sc.xcd_len[x];
+    const int64_t w = std::min(used, len);
+    heap.clear();
+    for (int64_t k = 0; k < w; ++k) heap.push_back({0, (int32_t)k});
+    for (int64_t j = start; j < start + len; ++j) {
+      std::pop_heap(heap.begin(), heap.end(), later);
+      auto& top = heap.back();
+      sc.wg_of[(size_t)j] = (int32_t)(top.second * X + x);
+      top.first += cost[sc.flat[(size_t)j] / Hkv] + 1;  // +1: an item's fixed cost, in steps
+      std::push_heap(heap.begin(), heap.end(), later);
+    }
+    start += len;
   }
-  for (int64_t k = 0; k < longest; ++k)
-    for (int x = 0; x < X; ++x) slots.push_back(k < len[x] ? flat[(size_t)(start[x] + k)] : -1);
-  // trailing idle slots change no XCD assignment
-  while (!slots.empty() && slots.back() < 0) slots.pop_back();
+  // counting sort of the slots by workgroup, keeping each list longest first
+  off.assign((size_t)n_wg + 1, 0);
+  for (int32_t w : sc.wg_of) ++off[(size_t)w + 1];
+  for (size_t k = 1; k < off.size(); ++k) off[k] += off[k - 1];
+  recs.resize(sc.flat.size());
+  auto& fill = sc.count;
+  fill.assign(off.begin(), off.end() - 1);
+  for (size_t j = 0; j < sc.flat.size(); ++j) {
+    const int32_t slot = sc.flat[j];
+    const detail::PrefillItem& it = items[(size_t)(slot / Hkv)];
+    const int32_t kvh = slot % Hkv;
+    PrefillRec& r = recs[(size_t)fill[(size_t)sc.wg_of[j]]++];
+    r.tok0 = it.tok0;
+    r.n_tok = it.n_tok;
+    r.pos0 = it.pos0;
+    r.req = it.req;
+    r.kv_begin = it.kv_begin;
+    r.kv_end = it.kv_end;
+    r.part = it.part < 0 ? -1 : it.part + kvh * it.part_kvh_stride;
+    r.kvh = kvh;
+  }
 }
 
 // Makespan, in steps, of longest-first list scheduling of `groups` (cost,
@@ -201,6 +246,8 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_PREFILL_TARGET_ITEMS")) t.prefill_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_MIN_SPLIT")) t.prefill_min_split = std::max(1, atoi(s));
   if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::min(64, std::max(1, atoi(s)));
+  if (const char* s = std::getenv("CP_PREFILL_WG_PER_CU"))
+    t.prefill_wg_per_cu = std::min(64, std::max(0, atoi(s)));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_ROWS"))
     t.prefill_wide_min_rows = std::max<int64_t>(1, atoll(s));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_KEYS"))
@@ -381,8 +428,10 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   auto& bounds = sc.bounds;
   sc.item_cost[0].clear();
   sc.item_cost[1].clear();
+  sc.items[0].clear();
+  sc.items[1].clear();
   for (detail::Chunk& ch : chunks) {
-    auto& items = ch.wide ? p.prefill_wide : p.prefill;
+    auto& items = sc.items[ch.wide ? 1 : 0];
     auto& cost = sc.item_cost[ch.wide ? 1 : 0];
     for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i) {
       detail::Tile& tl = tiles[i];
@@ -403,7 +452,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
       tl.ns = ns;
       ch.max_ns = std::max(ch.max_ns, ns);
       for (int32_t s = 0; s < ns; ++s) {
-        PrefillItem it;
+        detail::PrefillItem it;
         it.tok0 = tl.tok0;
         it.n_tok = tl.n_tok;
         it.pos0 = tl.pos0;
@@ -417,11 +466,20 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
       }
     }
   }
-  if ((int64_t)std::max(p.prefill.size(), p.prefill_wide.size()) * Hkv > INT32_MAX)
+  if ((int64_t)std::max(sc.items[0].size(), sc.items[1].size()) * Hkv > INT32_MAX)
     throw std::length_error("prefill slot index overflows int32");
-  if (t.num_xcds > 64) throw std::length_error("more than 64 XCDs");
-  order_for_xcds(false, sc.item_cost[0], Hkv, t.num_xcds, sc, p.prefill_slots);
-  order_for_xcds(true, sc.item_cost[1], Hkv, t.num_xcds, sc, p.prefill_wide_slots);
+  // persistent workgroups: t.prefill_wg_per_cu per CU for 256-row tiles (one
+  // fills a CU's registers), twice that for 128-row tiles
+  for (int w = 0; w < 2; ++w) {
+    const int X = std::max(1, t.num_xcds);
+    const int64_t per_xcd =
+        t.prefill_wg_per_cu > 0
+            ? std::max<int64_t>(1, (int64_t)t.num_cus * t.prefill_wg_per_cu * (w ? 1 : 2) / X)
+            : 0;
+    lists_by_xcd(w == 1, sc.item_cost[w], Hkv, t.num_xcds, sc);
+    deal_to_workgroups(sc.items[w], sc.item_cost[w], Hkv, t.num_xcds, per_xcd, sc,
+                       w ? p.prefill_wide : p.prefill, w ? p.prefill_wide_slots : p.prefill_slots);
+  }
 
   // ---- decode ranges --------------------------------------------------
   // Rows shorter than prefill_min_len run on the split-K decode kernel, one
@@ -498,11 +556,11 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   // ---- workspace layout ------------------------------------------------
   size_t o = 0;
   p.off_prefill = o;
-  o = align_up(o + p.prefill.size() * sizeof(PrefillItem), 256);
+  o = align_up(o + p.prefill.size() * sizeof(PrefillRec), 256);
   p.off_prefill_slots = o;
   o = align_up(o + p.prefill_slots.size() * sizeof(int32_t), 256);
   p.off_prefill_wide = o;
-  o = align_up(o + p.prefill_wide.size() * sizeof(PrefillItem), 256);
+  o = align_up(o + p.prefill_wide.size() * sizeof(PrefillRec), 256);
   p.off_prefill_wide_slots = o;
   o = align_up(o + p.prefill_wide_slots.size() * sizeof(int32_t), 256);
   p.off_decode = o;

@@ -31,22 +31,30 @@ constexpr int kDecodeWaves = 4;
 // decode item list per token, which only pays for few-token chunks.
 constexpr int kMaxPrefillMinLen = 64;
 
-// One item describes the work of every kv head.  Decode and merge kernels run
-// on a grid of (items, num_kv_heads).  Prefill workgroups take a slot each:
-// slot = item * num_kv_heads + kv head, in an order the planner chooses for
-// the XCDs, or -1 for an idle padding slot.  A split item's partial rows for
-// kv head h start at part + h * part_kvh_stride.
+// A decode or merge item describes the work of every kv head; those kernels
+// run on a grid of (items, num_kv_heads), and a split item's partial rows for
+// kv head h start at part + h * part_kvh_stride.  The prefill kernel is
+// persistent: workgroup w runs the records [off[w], off[w + 1]) of its list,
+// one record per (tile, key split, kv head).
 
-struct PrefillItem {  // 32 bytes
+struct PrefillRec {   // 32 bytes
   int32_t tok0;       // first query token (index into q / out)
   int32_t n_tok;      // tokens in the tile, 1 .. kPrefillRows / G (or kPrefillRowsWide / G)
   int32_t pos0;       // absolute position of tok0 inside its request
   int32_t req;        // block-table row
   int32_t kv_begin;   // keys [kv_begin, kv_end) of the request
   int32_t kv_end;
-  int32_t part;       // -1: final output; else first partial row of this split (kv head 0)
+  int32_t part;       // -1: final output; else the first partial row of this split and kv head
+  int32_t kvh;        // kv head
+};
+
+namespace detail {
+struct PrefillItem {  // a tile's key split, for every kv head (planner only)
+  int32_t tok0, n_tok, pos0, req, kv_begin, kv_end;
+  int32_t part;       // -1, or the first partial row of kv head 0
   int32_t part_kvh_stride;
 };
+}  // namespace detail
 
 struct DecodeItem {   // 32 bytes
   int32_t tok;        // query token
@@ -85,6 +93,8 @@ struct Tuning {
   int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
   int64_t prefill_wide_min_rows = 129;  // chunks with chunk_len * G >= this use 256-row tiles,
   int64_t prefill_wide_min_keys = 1200; // ... when the step's mean key range per query is this
+  int prefill_wg_per_cu = 1;    // persistent prefill workgroups per CU (x2 for 128-row tiles);
+                                // 0: one workgroup per record
 };
 
 namespace detail {
@@ -116,6 +126,10 @@ struct PlanScratch {
   std::vector<int64_t> load;
   std::vector<int64_t> count;
   std::vector<int32_t> flat;                          // slots grouped by XCD, longest first
+  std::vector<int64_t> xcd_len;                       // slots per XCD in flat
+  std::vector<detail::PrefillItem> items[2];          // 128- and 256-row tiles' key splits
+  std::vector<std::pair<int64_t, int32_t>> heap;      // (load, workgroup) of one XCD
+  std::vector<int32_t> wg_of;                         // workgroup of each slot in flat
   std::vector<int64_t> candidates;                    // split lengths to score
   std::vector<uint32_t> cut_lim;                      // per tile: last key a split may start at
   std::vector<std::pair<int64_t, int64_t>> groups2;  // (cost, count) of one split candidate
@@ -123,9 +137,11 @@ struct PlanScratch {
 };
 
 struct Plan {
-  std::vector<PrefillItem> prefill;       // 128-row tiles
+  // prefill records and per-workgroup list offsets (workgroups + 1 entries),
+  // 128-row tiles and 256-row tiles
+  std::vector<PrefillRec> prefill;
   std::vector<int32_t> prefill_slots;
-  std::vector<PrefillItem> prefill_wide;  // 256-row tiles
+  std::vector<PrefillRec> prefill_wide;
   std::vector<int32_t> prefill_wide_slots;
   std::vector<DecodeItem> decode;
   std::vector<MergeGroup> merge;
