@@ -607,9 +607,10 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   const int64_t D64 = desc->head_dim;
   const int64_t ends[8] = {
       plan->off_prefill + (int64_t)plan->n_prefill_items * (int64_t)sizeof(PrefillRec),
-      plan->off_prefill_slots + ((int64_t)plan->n_prefill_slots + 1) * 4,
+      plan->off_prefill_slots + (plan->n_prefill_slots > 0 ? plan->n_prefill_slots + 1 : 0) * 4,
       plan->off_prefill_wide + (int64_t)plan->n_prefill_wide_items * (int64_t)sizeof(PrefillRec),
-      plan->off_prefill_wide_slots + ((int64_t)plan->n_prefill_wide_slots + 1) * 4,
+      plan->off_prefill_wide_slots +
+          (plan->n_prefill_wide_slots > 0 ? plan->n_prefill_wide_slots + 1 : 0) * 4,
       plan->off_decode + (int64_t)plan->n_decode * (int64_t)sizeof(DecodeItem),
       plan->off_merge + (int64_t)plan->n_merge * (int64_t)sizeof(MergeGroup),
       plan->off_part_o + plan->partial_rows * D64 * 4,

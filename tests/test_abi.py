@@ -290,6 +290,11 @@ def test_attn_run_rejects_lists_past_the_workspace():
     assert run(off_part_o=0, partial_rows=9) == binding.CP_ERR_INVALID_ARG        # 9 x 512 B
     assert run(off_part_lse=big - 8, partial_rows=3) == binding.CP_ERR_INVALID_ARG
     assert run(n_prefill_items=-1) == binding.CP_ERR_INVALID_ARG
+    # an empty launch has an empty offset list: a list offset at the very end
+    # of the workspace is fine then (nothing to launch, so this runs on a CPU)
+    assert run(off_prefill_slots=big, off_prefill_wide_slots=big, off_decode=big,
+               off_merge=big, off_part_o=big, off_part_lse=big) == binding.CP_OK
+    assert run(off_prefill_slots=big, n_prefill_slots=1) == binding.CP_ERR_INVALID_ARG
     assert run(partial_rows=-1) == binding.CP_ERR_INVALID_ARG
 
 
