@@ -159,13 +159,11 @@ typedef struct {
     cp_attn_desc desc;            /* the geometry it was made for             */
     int64_t tokens;               /* scheduled tokens T of the batch          */
     int64_t ws_bytes;             /* workspace bytes it occupies              */
-    /* workgroups of the 128-row and 256-row prefill launches (each has a
-     * list-offset array of that many entries plus one), decode items and
-     * merge groups */
-    int32_t n_prefill_slots, n_prefill_wide_slots, n_decode, n_merge;
-    int64_t off_prefill, off_prefill_slots, off_prefill_wide, off_prefill_wide_slots;
-    int64_t off_decode, off_merge, off_part_o, off_part_lse;  /* byte offsets in ws */
-    int32_t n_prefill_items, n_prefill_wide_items;  /* prefill work records   */
+    /* work records of the 128-row and 256-row prefill launches (one
+     * workgroup each, idle padding included), decode items, merge groups */
+    int32_t n_prefill_items, n_prefill_wide_items, n_decode, n_merge;
+    int64_t off_prefill, off_prefill_wide, off_decode, off_merge;
+    int64_t off_part_o, off_part_lse;  /* byte offsets in ws */
     int64_t partial_rows;         /* fp32 partial rows of split key ranges    */
 } cp_attn_plan;
 

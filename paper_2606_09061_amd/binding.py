@@ -49,13 +49,11 @@ class AttnPlan(ctypes.Structure):
     """cp_attn_plan: a batch's attention plan, prepared once, run per layer."""
 
     _fields_ = [("desc", Desc), ("tokens", ctypes.c_int64), ("ws_bytes", ctypes.c_int64),
-                ("n_prefill_slots", ctypes.c_int32), ("n_prefill_wide_slots", ctypes.c_int32),
+                ("n_prefill_items", ctypes.c_int32), ("n_prefill_wide_items", ctypes.c_int32),
                 ("n_decode", ctypes.c_int32), ("n_merge", ctypes.c_int32)] + [
-        (n, ctypes.c_int64) for n in ("off_prefill", "off_prefill_slots", "off_prefill_wide",
-                                      "off_prefill_wide_slots", "off_decode", "off_merge",
-                                      "off_part_o", "off_part_lse")] + [
-        ("n_prefill_items", ctypes.c_int32), ("n_prefill_wide_items", ctypes.c_int32),
-        ("partial_rows", ctypes.c_int64)]
+        (n, ctypes.c_int64) for n in ("off_prefill", "off_prefill_wide", "off_decode",
+                                      "off_merge", "off_part_o", "off_part_lse",
+                                      "partial_rows")]
 
 
 _lib = None

@@ -317,9 +317,7 @@ void put(uint8_t* buf, size_t off, const std::vector<T>& v) {
 // The plan's item lists at their workspace offsets (p.plan_bytes bytes).
 void serialize_into(const Plan& p, uint8_t* buf) {
   put(buf, p.off_prefill, p.prefill);
-  put(buf, p.off_prefill_slots, p.prefill_slots);
   put(buf, p.off_prefill_wide, p.prefill_wide);
-  put(buf, p.off_prefill_wide_slots, p.prefill_wide_slots);
   put(buf, p.off_decode, p.decode);
   put(buf, p.off_merge, p.merge);
 }
@@ -327,16 +325,10 @@ void serialize_into(const Plan& p, uint8_t* buf) {
 // The plan's lists, counts and workspace offsets as the caller-visible struct.
 void fill_plan(const Plan& p, cp_attn_plan& pl) {
   pl.ws_bytes = (int64_t)p.ws_bytes;
-  // workgroups of each prefill launch (their list offsets hold one entry more)
-  pl.n_prefill_slots = p.prefill_slots.empty() ? 0 : (int32_t)p.prefill_slots.size() - 1;
-  pl.n_prefill_wide_slots =
-      p.prefill_wide_slots.empty() ? 0 : (int32_t)p.prefill_wide_slots.size() - 1;
   pl.n_decode = (int32_t)p.decode.size();
   pl.n_merge = (int32_t)p.merge.size();
   pl.off_prefill = (int64_t)p.off_prefill;
-  pl.off_prefill_slots = (int64_t)p.off_prefill_slots;
   pl.off_prefill_wide = (int64_t)p.off_prefill_wide;
-  pl.off_prefill_wide_slots = (int64_t)p.off_prefill_wide_slots;
   pl.off_decode = (int64_t)p.off_decode;
   pl.off_merge = (int64_t)p.off_merge;
   pl.off_part_o = (int64_t)p.off_part_o;
@@ -425,7 +417,9 @@ int cp_plan_summary(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n
     Plan& p = thread_plan();
     build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
     const int64_t hkv = desc->num_kv_heads;
-    counts[0] = (int64_t)(p.prefill.size() + p.prefill_wide.size());
+    counts[0] = 0;
+    for (const PrefillRec& r : p.prefill) counts[0] += r.n_tok > 0;
+    for (const PrefillRec& r : p.prefill_wide) counts[0] += r.n_tok > 0;
     counts[1] = (int64_t)p.decode.size() * hkv;
     counts[2] = (int64_t)p.merge.size() * hkv;
     counts[3] = p.partial_rows;
@@ -458,10 +452,10 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
       }
       ++n;
     };
-    // prefill records, workgroup list after workgroup list
+    // prefill records in dispatch order (idle padding skipped)
     for (int w = 1; w >= 0; --w)
       for (const PrefillRec& r : (w ? p.prefill_wide : p.prefill))
-        put_item(0, r.tok0, r.n_tok, r.pos0, r.req, r.kvh, r.kv_begin, r.kv_end);
+        if (r.n_tok > 0) put_item(0, r.tok0, r.n_tok, r.pos0, r.req, r.kvh, r.kv_begin, r.kv_end);
     // position of a decode query: chunk_start + its index inside the row
     std::vector<int32_t> pos_of_tok;
     {
@@ -589,28 +583,23 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   const int vd = validate(desc, nullptr, 0);
   if (vd != CP_OK) return vd;
   if (plan->tokens == 0) return CP_OK;
-  if (plan->ws_bytes <= 0 || plan->n_prefill_slots < 0 || plan->n_prefill_wide_slots < 0 ||
-      plan->n_decode < 0 || plan->n_merge < 0 || plan->n_prefill_items < 0 ||
-      plan->n_prefill_wide_items < 0 || plan->partial_rows < 0)
+  if (plan->ws_bytes <= 0 || plan->n_prefill_items < 0 || plan->n_prefill_wide_items < 0 ||
+      plan->n_decode < 0 || plan->n_merge < 0 || plan->partial_rows < 0)
     return CP_ERR_INVALID_ARG;
   if ((size_t)plan->ws_bytes > ws_bytes) return CP_ERR_WORKSPACE;
   if (!q || !k_cache || !v_cache || !block_tables || !out || !ws) return CP_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
       !aligned(ws, 256) || !aligned(block_tables, 4))
     return CP_ERR_INVALID_ARG;
-  const int64_t offs[8] = {plan->off_prefill,  plan->off_prefill_slots, plan->off_prefill_wide,
-                           plan->off_prefill_wide_slots, plan->off_decode, plan->off_merge,
-                           plan->off_part_o, plan->off_part_lse};
+  const int64_t offs[6] = {plan->off_prefill, plan->off_prefill_wide, plan->off_decode,
+                           plan->off_merge,   plan->off_part_o,       plan->off_part_lse};
   for (int64_t o : offs)
     if (o < 0 || o > plan->ws_bytes) return CP_ERR_INVALID_ARG;
   // every list the kernels read lies inside the plan's workspace
   const int64_t D64 = desc->head_dim;
-  const int64_t ends[8] = {
+  const int64_t ends[6] = {
       plan->off_prefill + (int64_t)plan->n_prefill_items * (int64_t)sizeof(PrefillRec),
-      plan->off_prefill_slots + (plan->n_prefill_slots > 0 ? plan->n_prefill_slots + 1 : 0) * 4,
       plan->off_prefill_wide + (int64_t)plan->n_prefill_wide_items * (int64_t)sizeof(PrefillRec),
-      plan->off_prefill_wide_slots +
-          (plan->n_prefill_wide_slots > 0 ? plan->n_prefill_wide_slots + 1 : 0) * 4,
       plan->off_decode + (int64_t)plan->n_decode * (int64_t)sizeof(DecodeItem),
       plan->off_merge + (int64_t)plan->n_merge * (int64_t)sizeof(MergeGroup),
       plan->off_part_o + plan->partial_rows * D64 * 4,
@@ -621,13 +610,9 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   uint8_t* base = static_cast<uint8_t*>(ws);
   AttnArgs a;
   a.prefill = reinterpret_cast<const PrefillRec*>(base + plan->off_prefill);
-  a.prefill_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_slots);
-  a.n_prefill_slots = plan->n_prefill_slots;
   a.n_prefill_items = plan->n_prefill_items;
-  a.n_prefill_wide_items = plan->n_prefill_wide_items;
   a.prefill_wide = reinterpret_cast<const PrefillRec*>(base + plan->off_prefill_wide);
-  a.prefill_wide_slots = reinterpret_cast<const int32_t*>(base + plan->off_prefill_wide_slots);
-  a.n_prefill_wide_slots = plan->n_prefill_wide_slots;
+  a.n_prefill_wide_items = plan->n_prefill_wide_items;
   a.decode = reinterpret_cast<const DecodeItem*>(base + plan->off_decode);
   a.n_decode = plan->n_decode;
   a.merge = reinterpret_cast<const MergeGroup*>(base + plan->off_merge);
@@ -647,7 +632,7 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   const int D = desc->head_dim;
   const int G = desc->num_q_heads / desc->num_kv_heads;
   int rc = CP_OK;
-  if (a.n_prefill_slots > 0 || a.n_prefill_wide_slots > 0) {
+  if (a.n_prefill_items > 0 || a.n_prefill_wide_items > 0) {
     const long pi = prof_open(1, s);
     const hipError_t e = launch_prefill(D, G, a, s);
     prof_close(pi, s);

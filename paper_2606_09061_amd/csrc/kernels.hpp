@@ -27,13 +27,10 @@ struct AppendArgs {
 };
 
 struct AttnArgs {
-  const PrefillRec* prefill;        // 128-row tiles (4-wave kernel): records
-  const int32_t* prefill_slots;     // per-workgroup list offsets (n_prefill_slots + 1)
-  int n_prefill_slots;              // workgroups of the launch
-  int n_prefill_items, n_prefill_wide_items;  // records; list entries past them are skipped
+  const PrefillRec* prefill;        // 128-row tiles (4-wave kernel): one record per workgroup
+  int n_prefill_items;
   const PrefillRec* prefill_wide;   // 256-row tiles (8-wave kernel)
-  const int32_t* prefill_wide_slots;
-  int n_prefill_wide_slots;
+  int n_prefill_wide_items;
   const DecodeItem* decode;         // grid (n_decode, hkv)
   int n_decode;
   const MergeGroup* merge;          // grid (n_merge, hkv)

@@ -90,64 +90,34 @@ void lists_by_xcd(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_
   for_each_slot([&](size_t key, int32_t slot) { sc.flat[(size_t)pos[key]++] = slot; });
 }
 
-// Deals each XCD's slots (sc.flat, longest first) to the persistent
-// workgroups that run on that XCD -- workgroup w = k * X + x runs on XCD x --
-// each to the least-loaded one (longest processing time first; ties to the
-// lower k), and writes every workgroup's records, list after list, with the
-// list offsets.  wg_per_xcd <= 0: one workgroup per slot.
-void deal_to_workgroups(const std::vector<detail::PrefillItem>& items,
-                        const std::vector<int64_t>& cost, int Hkv, int num_xcds,
-                        int64_t wg_per_xcd, PlanScratch& sc, std::vector<PrefillRec>& recs,
-                        std::vector<int32_t>& off) {
+// Lays the slots out in dispatch order: workgroup i runs on XCD i mod X, so
+// position k * X + x takes XCD x's k-th slot (longest first), or an idle
+// record when XCD x has fewer; trailing idle records are dropped.
+void interleave_by_xcd(const std::vector<detail::PrefillItem>& items, int Hkv, int num_xcds,
+                       PlanScratch& sc, std::vector<PrefillRec>& recs) {
   recs.clear();
-  off.clear();
   if (sc.flat.empty()) return;
   const int X = std::max(1, num_xcds);
-  int64_t used = 0;  // workgroups per XCD that get a list
-  for (int x = 0; x < X; ++x)
-    used = std::max(used, wg_per_xcd > 0 ? std::min(wg_per_xcd, sc.xcd_len[x]) : sc.xcd_len[x]);
-  const int64_t n_wg = used * X;
-  sc.wg_of.resize(sc.flat.size());
-  auto& heap = sc.heap;
-  auto later = [](const std::pair<int64_t, int32_t>& a, const std::pair<int64_t, int32_t>& b) {
-    return a.first != b.first ? a.first > b.first : a.second > b.second;  // min-heap on (load, k)
-  };
-  int64_t start = 0;
-  for (int x = 0; x < X; ++x) {
-    const int64_t len = sc.xcd_len[x];
-    const int64_t w = std::min(used, len);
-    heap.clear();
-    for (int64_t k = 0; k < w; ++k) heap.push_back({0, (int32_t)k});
-    for (int64_t j = start; j < start + len; ++j) {
-      std::pop_heap(heap.begin(), heap.end(), later);
-      auto& top = heap.back();
-      sc.wg_of[(size_t)j] = (int32_t)(top.second * X + x);
-      top.first += cost[sc.flat[(size_t)j] / Hkv] + 1;  // +1: an item's fixed cost, in steps
-      std::push_heap(heap.begin(), heap.end(), later);
+  int64_t longest = 0, start[64];
+  for (int x = 0, acc = 0; x < X; ++x) {
+    start[x] = acc;
+    acc += (int)sc.xcd_len[x];
+    longest = std::max(longest, sc.xcd_len[x]);
+  }
+  recs.reserve((size_t)(longest * X));
+  for (int64_t k = 0; k < longest; ++k)
+    for (int x = 0; x < X; ++x) {
+      PrefillRec r{0, 0, 0, 0, 0, 0, -1, 0};
+      if (k < sc.xcd_len[x]) {
+        const int32_t slot = sc.flat[(size_t)(start[x] + k)];
+        const detail::PrefillItem& it = items[(size_t)(slot / Hkv)];
+        const int32_t kvh = slot % Hkv;
+        r = PrefillRec{it.tok0, it.n_tok, it.pos0, it.req, it.kv_begin, it.kv_end,
+                       it.part < 0 ? -1 : it.part + kvh * it.part_kvh_stride, kvh};
+      }
+      recs.push_back(r);
     }
-    start += len;
-  }
-  // counting sort of the slots by workgroup, keeping each list longest first
-  off.assign((size_t)n_wg + 1, 0);
-  for (int32_t w : sc.wg_of) ++off[(size_t)w + 1];
-  for (size_t k = 1; k < off.size(); ++k) off[k] += off[k - 1];
-  recs.resize(sc.flat.size());
-  auto& fill = sc.count;
-  fill.assign(off.begin(), off.end() - 1);
-  for (size_t j = 0; j < sc.flat.size(); ++j) {
-    const int32_t slot = sc.flat[j];
-    const detail::PrefillItem& it = items[(size_t)(slot / Hkv)];
-    const int32_t kvh = slot % Hkv;
-    PrefillRec& r = recs[(size_t)fill[(size_t)sc.wg_of[j]]++];
-    r.tok0 = it.tok0;
-    r.n_tok = it.n_tok;
-    r.pos0 = it.pos0;
-    r.req = it.req;
-    r.kv_begin = it.kv_begin;
-    r.kv_end = it.kv_end;
-    r.part = it.part < 0 ? -1 : it.part + kvh * it.part_kvh_stride;
-    r.kvh = kvh;
-  }
+  while (!recs.empty() && recs.back().n_tok == 0) recs.pop_back();
 }
 
 // Makespan, in steps, of longest-first list scheduling of `groups` (cost,
@@ -246,8 +216,6 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_PREFILL_TARGET_ITEMS")) t.prefill_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_MIN_SPLIT")) t.prefill_min_split = std::max(1, atoi(s));
   if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::min(64, std::max(1, atoi(s)));
-  if (const char* s = std::getenv("CP_PREFILL_WG_PER_CU"))
-    t.prefill_wg_per_cu = std::min(64, std::max(0, atoi(s)));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_ROWS"))
     t.prefill_wide_min_rows = std::max<int64_t>(1, atoll(s));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_KEYS"))
@@ -370,9 +338,7 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
                 Plan& p) {
   PlanScratch& sc = p.scratch;
   p.prefill.clear();
-  p.prefill_slots.clear();
   p.prefill_wide.clear();
-  p.prefill_wide_slots.clear();
   p.decode.clear();
   p.merge.clear();
   p.partial_rows = 0;
@@ -468,17 +434,9 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   }
   if ((int64_t)std::max(sc.items[0].size(), sc.items[1].size()) * Hkv > INT32_MAX)
     throw std::length_error("prefill slot index overflows int32");
-  // persistent workgroups: t.prefill_wg_per_cu per CU for 256-row tiles (one
-  // fills a CU's registers), twice that for 128-row tiles
   for (int w = 0; w < 2; ++w) {
-    const int X = std::max(1, t.num_xcds);
-    const int64_t per_xcd =
-        t.prefill_wg_per_cu > 0
-            ? std::max<int64_t>(1, (int64_t)t.num_cus * t.prefill_wg_per_cu * (w ? 1 : 2) / X)
-            : 0;
     lists_by_xcd(w == 1, sc.item_cost[w], Hkv, t.num_xcds, sc);
-    deal_to_workgroups(sc.items[w], sc.item_cost[w], Hkv, t.num_xcds, per_xcd, sc,
-                       w ? p.prefill_wide : p.prefill, w ? p.prefill_wide_slots : p.prefill_slots);
+    interleave_by_xcd(sc.items[w], Hkv, t.num_xcds, sc, w ? p.prefill_wide : p.prefill);
   }
 
   // ---- decode ranges --------------------------------------------------
@@ -557,12 +515,8 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   size_t o = 0;
   p.off_prefill = o;
   o = align_up(o + p.prefill.size() * sizeof(PrefillRec), 256);
-  p.off_prefill_slots = o;
-  o = align_up(o + p.prefill_slots.size() * sizeof(int32_t), 256);
   p.off_prefill_wide = o;
   o = align_up(o + p.prefill_wide.size() * sizeof(PrefillRec), 256);
-  p.off_prefill_wide_slots = o;
-  o = align_up(o + p.prefill_wide_slots.size() * sizeof(int32_t), 256);
   p.off_decode = o;
   o = align_up(o + p.decode.size() * sizeof(DecodeItem), 256);
   p.off_merge = o;

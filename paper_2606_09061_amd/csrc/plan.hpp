@@ -33,13 +33,15 @@ constexpr int kMaxPrefillMinLen = 64;
 
 // A decode or merge item describes the work of every kv head; those kernels
 // run on a grid of (items, num_kv_heads), and a split item's partial rows for
-// kv head h start at part + h * part_kvh_stride.  The prefill kernel is
-// persistent: workgroup w runs the records [off[w], off[w + 1]) of its list,
-// one record per (tile, key split, kv head).
+// kv head h start at part + h * part_kvh_stride.  A prefill workgroup runs
+// one record, a (tile, key split, kv head), the one its index names: the
+// planner lays the records out in the order the workgroups are dispatched to
+// the XCDs, padded with idle records (n_tok == 0).
 
 struct PrefillRec {   // 32 bytes
   int32_t tok0;       // first query token (index into q / out)
-  int32_t n_tok;      // tokens in the tile, 1 .. kPrefillRows / G (or kPrefillRowsWide / G)
+  int32_t n_tok;      // tokens in the tile, 1 .. kPrefillRows / G (or kPrefillRowsWide / G);
+                      // 0: an idle record
   int32_t pos0;       // absolute position of tok0 inside its request
   int32_t req;        // block-table row
   int32_t kv_begin;   // keys [kv_begin, kv_end) of the request
@@ -93,8 +95,6 @@ struct Tuning {
   int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
   int64_t prefill_wide_min_rows = 129;  // chunks with chunk_len * G >= this use 256-row tiles,
   int64_t prefill_wide_min_keys = 1200; // ... when the step's mean key range per query is this
-  int prefill_wg_per_cu = 1;    // persistent prefill workgroups per CU (x2 for 128-row tiles);
-                                // 0: one workgroup per record
 };
 
 namespace detail {
@@ -128,8 +128,6 @@ struct PlanScratch {
   std::vector<int32_t> flat;                          // slots grouped by XCD, longest first
   std::vector<int64_t> xcd_len;                       // slots per XCD in flat
   std::vector<detail::PrefillItem> items[2];          // 128- and 256-row tiles' key splits
-  std::vector<std::pair<int64_t, int32_t>> heap;      // (load, workgroup) of one XCD
-  std::vector<int32_t> wg_of;                         // workgroup of each slot in flat
   std::vector<int64_t> candidates;                    // split lengths to score
   std::vector<uint32_t> cut_lim;                      // per tile: last key a split may start at
   std::vector<std::pair<int64_t, int64_t>> groups2;  // (cost, count) of one split candidate
@@ -137,19 +135,16 @@ struct PlanScratch {
 };
 
 struct Plan {
-  // prefill records and per-workgroup list offsets (workgroups + 1 entries),
-  // 128-row tiles and 256-row tiles
+  // prefill records in dispatch order, 128-row tiles and 256-row tiles
   std::vector<PrefillRec> prefill;
-  std::vector<int32_t> prefill_slots;
   std::vector<PrefillRec> prefill_wide;
-  std::vector<int32_t> prefill_wide_slots;
   std::vector<DecodeItem> decode;
   std::vector<MergeGroup> merge;
   int64_t partial_rows = 0;
   int32_t decode_split_blocks = 0;
   // workspace layout (byte offsets from the workspace base)
-  size_t off_prefill = 0, off_prefill_slots = 0, off_prefill_wide = 0, off_prefill_wide_slots = 0,
-         off_decode = 0, off_merge = 0, off_part_o = 0, off_part_lse = 0;
+  size_t off_prefill = 0, off_prefill_wide = 0, off_decode = 0, off_merge = 0, off_part_o = 0,
+         off_part_lse = 0;
   size_t plan_bytes = 0;   // bytes of the uploaded item lists
   size_t ws_bytes = 0;     // total workspace
   PlanScratch scratch;

@@ -99,23 +99,6 @@ __device__ __forceinline__ void copy16_to_lds(const void* src, uint8_t* lds) {
 #endif
 }
 
-// 4 bytes per lane from global memory straight into LDS at lds + 4 * lane
-// (global_load_lds_dword); `lds` must be wave-uniform.
-__device__ __forceinline__ void copy4_to_lds(const void* src, uint8_t* lds) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)lds, 4, 0, 0);
-#endif
-}
-
-// keeps LDS reads after this point (they read what an asynchronous
-// global-to-LDS copy wrote, waited for just before)
-__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
-
-// s_waitcnt lgkmcnt(0): every LDS read (and scalar load) of this wave has returned
-__device__ __forceinline__ void wait_lgkm0() {
-  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14));
-}
-
 // s_waitcnt with vmcnt <= N, the other counters unconstrained (gfx9 encoding)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -170,8 +153,7 @@ using namespace prefill_impl;
 
 template <int D, int B, int G, int NW, int RG>
 __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
-    const PrefillRec* __restrict__ recs, const int32_t* __restrict__ wg_off, int n_recs,
-    const uint16_t* __restrict__ q,
+    const PrefillRec* __restrict__ recs, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
@@ -187,85 +169,45 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
   __shared__ __attribute__((aligned(1024))) uint8_t vb0[C::TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t vb1[C::TILE_BYTES];
 
+  // this workgroup's record (the grid is the record list, in the planner's
+  // XCD-interleaved order); records with no tokens are idle padding
+  const PrefillRec it = recs[blockIdx.x];
+  if (it.n_tok <= 0) return;
+  const int kvh = it.kvh;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = uniform(tid >> 6);
   const int col = lane & 31;
   const int g = lane >> 5;
+  const int32_t* bt_row = bt + (int64_t)it.req * mbr;
   const int64_t blk_elems = (int64_t)hkv * B * D;
-
-  // This workgroup's list of records (a persistent workgroup runs them in
-  // turn); entries past n_recs are never read.
-  const int r_first = uniform(wg_off[blockIdx.x]);
-  const int r_stop = min(uniform(wg_off[blockIdx.x + 1]), n_recs);
-  if (r_first < 0 || r_first >= r_stop) return;
-
-  // Per-wave LDS for the list walk (each wave reads only what it wrote):
-  // record slots at 32 * (r & 3); at 128 + 16 * (r & 1) the table entries of
-  // the blocks this wave copies in record r's first two steps (NBW each); at
-  // 160 the index of the running record and the list end.  Keeping these
-  // here rather than in scalar registers leaves the main loop its registers.
-  constexpr int kMetaBlocks = 128, kMetaIndex = 160;
-  __shared__ __attribute__((aligned(16))) uint8_t meta[NW][192];
-  uint8_t* const my_meta = &meta[wave][0];
-  auto rec_slot = [&](int ri) { return my_meta + 32 * (ri & 3); };
-
-  // the record being run and what follows from it (wave-uniform)
-  PrefillRec it;
-  int n_step, lb_first, lb_last, e_step;
-  bool partial;
-  const int32_t* bt_row;
-  const uint16_t* kbase;
-  const uint16_t* vbase;
-  auto set_item = [&](const PrefillRec& r) {
-    it = r;
-    bt_row = bt + (int64_t)r.req * mbr;
-    kbase = k_cache + (int64_t)r.kvh * B * D;
-    vbase = v_cache + (int64_t)r.kvh * B * D;
-    n_step = (r.kv_end - r.kv_begin + BN - 1) / BN;
-    lb_first = r.kv_begin >> C::LOG2B;
-    lb_last = (r.kv_end - 1) >> C::LOG2B;
-    partial = (r.kv_end - r.kv_begin) % BN != 0;
-    // first edge step: steps >= e_step cross the causal diagonal or the range end
-    const int lim = min(r.pos0 + 1, r.kv_end) - BN;
-    e_step = r.kv_begin > lim ? 0 : (lim - r.kv_begin) / BN + 1;
-  };
+  const uint16_t* kbase = k_cache + (int64_t)kvh * B * D;
+  const uint16_t* vbase = v_cache + (int64_t)kvh * B * D;
+  const int n_step = (it.kv_end - it.kv_begin + BN - 1) / BN;
 
   // row groups: rows 32*RG*wave + 32*rg + col of the tile
   int tl[RG], qpos[RG];
   bool row_valid[RG];
   uint4 qreg[RG][NKS];  // Q^T operand: lane holds features [16 ks + 8 g, +8) of its row
-  auto set_rows = [&]() {
-    static_for<0, RG>([&](auto rg_c) {
-      constexpr int rg = decltype(rg_c)::value;
-      const int row = (wave * RG + rg) * 32 + col;
-      tl[rg] = row / G;
-      row_valid[rg] = tl[rg] < it.n_tok;
-      qpos[rg] = it.pos0 + tl[rg];
+  static_for<0, RG>([&](auto rg_c) {
+    constexpr int rg = decltype(rg_c)::value;
+    const int row = (wave * RG + rg) * 32 + col;
+    tl[rg] = row / G;
+    row_valid[rg] = tl[rg] < it.n_tok;
+    qpos[rg] = it.pos0 + tl[rg];
+    const uint16_t* qp = q + ((int64_t)(it.tok0 + (row_valid[rg] ? tl[rg] : 0)) * hq + kvh * G +
+                              row % G) * D + g * 8;
+    static_for<0, NKS>([&](auto ks_c) {
+      constexpr int ks = decltype(ks_c)::value;
+      qreg[rg][ks] = row_valid[rg] ? ld_global16(qp + ks * 16) : make_uint4(0, 0, 0, 0);
     });
-  };
-  // Q^T of record r into qreg.  Every lane issues all its loads (rows past
-  // the tile read the tile's first token and are zeroed), so the number of
-  // loads in flight is fixed and the waits can count them.
-  auto load_q = [&](const PrefillRec& r) {
-    static_for<0, RG>([&](auto rg_c) {
-      constexpr int rg = decltype(rg_c)::value;
-      const int row = (wave * RG + rg) * 32 + col;
-      const int t = row / G;
-      const bool valid = t < r.n_tok;
-      const uint16_t* qp =
-          q + ((int64_t)(r.tok0 + (valid ? t : 0)) * hq + r.kvh * G + row % G) * D + g * 8;
-      static_for<0, NKS>([&](auto ks_c) {
-        constexpr int ks = decltype(ks_c)::value;
-        const uint4 v = ld_global16(qp + ks * 16);
-        qreg[rg][ks] = valid ? v : make_uint4(0, 0, 0, 0);
-      });
-    });
-  };
+  });
 
   // ---- gather geometry: wave w copies pieces [w*PW, (w+1)*PW) of every K
   // and V step; piece p lies in block p / PPB of the step, the same for K
   // and V.  Lane offsets (elements inside a block) are fixed for the item.
+  const int lb_first = it.kv_begin >> C::LOG2B;
+  const int lb_last = (it.kv_end - 1) >> C::LOG2B;
   uint32_t koff[PW], voff[PW];
   static_for<0, PW>([&](auto i_c) {
     constexpr int i = decltype(i_c)::value;
@@ -310,61 +252,30 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
     else wait_vmcnt<0>();
   };
 
-  // ---- fetch-ahead of the records to come, into this wave's LDS slots.
-  // Record ri (two lanes of 16 bytes):
-  auto prefetch_rec = [&](int ri) {
-    if (lane < 2) copy16_to_lds(reinterpret_cast<const uint8_t*>(recs + ri) + 16 * lane, rec_slot(ri));
-  };
-  // the table entries of the blocks this wave copies in record ri's first two
-  // steps (lane l < 2 * NBW: step l / NBW, block l % NBW):
-  auto prefetch_blocks = [&](const PrefillRec& rr, int ri) {
-    if (lane < 2 * NBW) {
-      const int lbf = rr.kv_begin >> C::LOG2B, lbl = (rr.kv_end - 1) >> C::LOG2B;
-      const int lb = min(lbf + (lane / NBW) * (BN / B) + (wave * PW) / C::PPB + lane % NBW, lbl);
-      copy4_to_lds(bt + (int64_t)rr.req * mbr + lb, my_meta + kMetaBlocks + 16 * (ri & 1));
-    }
-  };
-  auto read_rec = [&](int ri) {
-    const uint4 a = *reinterpret_cast<const uint4*>(rec_slot(ri));
-    const uint4 b = *reinterpret_cast<const uint4*>(rec_slot(ri) + 16);
-    PrefillRec x;
-    x.tok0 = uniform((int)a.x), x.n_tok = uniform((int)a.y), x.pos0 = uniform((int)a.z),
-    x.req = uniform((int)a.w), x.kv_begin = uniform((int)b.x), x.kv_end = uniform((int)b.y),
-    x.part = uniform((int)b.z), x.kvh = uniform((int)b.w);
-    return x;
-  };
-  auto read_index = [&](int k) { return uniform(*reinterpret_cast<const int*>(my_meta + kMetaIndex + 4 * k)); };
-  auto write_index = [&](int k, int v) {
-    if (lane == 0) *reinterpret_cast<int*>(my_meta + kMetaIndex + 4 * k) = v;
-  };
-  auto read_blocks = [&](int ri, int st) {
-    Blocks r;
-    static_for<0, NBW>([&](auto j_c) {
-      constexpr int j = decltype(j_c)::value;
-      r.b[j] = uniform(
-          *reinterpret_cast<const int*>(my_meta + kMetaBlocks + 16 * (ri & 1) + 4 * (st * NBW + j)));
-    });
-    return r;
-  };
-
   f32x16_t oacc[RG][NDT];
   // scores of two consecutive steps; iteration st (parity p) reads sbuf[p]
   // (its step) and writes sbuf[p ^ 1] (the next step), so no copies
   f32x16_t sbuf[2][RG][2];  // [buffer][row group][32-key half]
   uint4 pk[RG][2][2];  // P^T operands of the current step: [row group][key half][16-key slice]
-  float m_run[RG], l_run[RG];  // running max of the scaled (base-2) scores; this half's sum
-  auto reset_acc = [&]() {
-    static_for<0, RG>([&](auto rg_c) {
-      constexpr int rg = decltype(rg_c)::value;
-      static_for<0, NDT>([&](auto i_c) {
-        constexpr int i = decltype(i_c)::value;
-        static_for<0, 16>([&](auto r_c) { oacc[rg][i][decltype(r_c)::value] = 0.f; });
-      });
-      m_run[rg] = -INFINITY;
-      l_run[rg] = 0.f;
+  static_for<0, RG>([&](auto rg_c) {
+    constexpr int rg = decltype(rg_c)::value;
+    static_for<0, NDT>([&](auto i_c) {
+      constexpr int i = decltype(i_c)::value;
+      static_for<0, 16>([&](auto r_c) { oacc[rg][i][decltype(r_c)::value] = 0.f; });
     });
-  };
-  // (phase K zeroes the score buffer it accumulates into, so sbuf needs no reset)
+    static_for<0, 2>([&](auto kt_c) {
+      constexpr int kt = decltype(kt_c)::value;
+      static_for<0, 16>([&](auto r_c) {
+        sbuf[0][rg][kt][decltype(r_c)::value] = 0.f;
+        sbuf[1][rg][kt][decltype(r_c)::value] = 0.f;
+      });
+    });
+  });
+  float m_run[RG], l_run[RG];  // running max of the scaled (base-2) scores; this half's sum
+  static_for<0, RG>([&](auto rg_c) {
+    m_run[decltype(rg_c)::value] = -INFINITY;
+    l_run[decltype(rg_c)::value] = 0.f;
+  });
   const int krow0 = sigma(col);
 
   // MFMA operand addresses inside a tile.  K read i: key half i / NKS, k-step
@@ -603,6 +514,7 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
   };
   // Zeroes the values of keys [vlim, BN) of the V tile vb: the 16-byte slot
   // (block bi, feature d, 8 keys) of step keys [8x, 8x + 8), x = bi*B/8 + s.
+  const bool partial = (it.kv_end - it.kv_begin) % BN != 0;
   auto zero_tail = [&](uint8_t* vb, int vlim) {
     constexpr int SLOTS = BN / 8;  // 16-byte slots per feature row of a step
     for (int x = tid; x < SLOTS * D; x += NW * 64) {
@@ -625,23 +537,11 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
     }
   };
 
-  // ---- first record of the list: its state, the fetch-ahead of the next
-  // two records (issued before this record's copies, so every wait on those
-  // copies covers them too), Q, copies K0 -> kb0, K1 -> kb1, V0 -> vb0.
-  set_item(recs[r_first]);
-  if (lane == 0) {  // the running record and the list position live in LDS
-    *reinterpret_cast<PrefillRec*>(rec_slot(r_first)) = it;
-    *reinterpret_cast<int*>(my_meta + kMetaIndex) = r_first;
-    *reinterpret_cast<int*>(my_meta + kMetaIndex + 4) = r_stop;
-  }
-  set_rows();
-  reset_acc();
-  if (r_first + 1 < r_stop) {
-    prefetch_rec(r_first + 1);
-    prefetch_blocks(recs[r_first + 1], r_first + 1);
-  }
-  if (r_first + 2 < r_stop) prefetch_rec(r_first + 2);
-  load_q(it);
+  // first edge step: steps >= e_step cross the causal diagonal or the range end
+  const int lim = min(it.pos0 + 1, it.kv_end) - BN;
+  const int e_step = it.kv_begin > lim ? 0 : (lim - it.kv_begin) / BN + 1;
+
+  // ---- prologue: copies K0 -> kb0, K1 -> kb1, V0 -> vb0; S_0 = K0 . Q^T
   {
     const Blocks b0 = blocks_of(0);
     issue(kbase, koff, b0, kb0);
@@ -649,6 +549,10 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
     issue(vbase, voff, b0, vb0);
   }
   wait_groups(n_step > 1 ? 2 : 1);
+  barrier();
+  phase_k(kb0, std::integral_constant<int, 1>(), F_());  // writes sbuf[0]
+  if (e_step == 0) mask_scores(sbuf[0], 0);
+  first_max();
 
   // ---- main loop.  Iteration st (parity p = st & 1): phase K reads K_{st+1}
   // from kb[1-p], phase V reads V_st from vb[p].  Copies: V_{st+1} into vb[1-p]
@@ -656,29 +560,8 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
   // kb[1-p] after the phase-V barrier (phase K of st read it last); K_2 into
   // kb0 at st = 0, before V_1.  Buffers are chosen at compile time so every
   // LDS access names its array.
-  Blocks blk_k, blk_v;  // entries of the next K copy and of the next V copy
-  bool has_next = false;
-  // In the last iteration of a record with a successor: after the phase-K
-  // barrier no wave reads kb0 or kb1 any more, nor vb0 when this iteration
-  // reads vb1 (PAR), so the successor's K0, K1 (and V0) are issued here and
-  // are in flight during the last exponentials, the last PV products and the
-  // stores (its Q follows the stores: the Q^T registers are still taken).  Its record has been in LDS since the previous record started,
-  // its first table entries since this record started.
-  auto issue_next = [&](auto par_c) {
-    constexpr bool PAR = decltype(par_c)::value;
-    if (n_step >= 2) wait_vmcnt<PW>();  // all but V_{n-1}, which is younger
-    else wait_vmcnt<0>();
-    compiler_fence();
-    const int rn_i = read_index(0) + 1;
-    const int kvh_n = read_rec(rn_i).kvh;
-    const Blocks b0 = read_blocks(rn_i, 0);
-    const uint16_t* kb_n = k_cache + (int64_t)kvh_n * B * D;
-    issue(kb_n, koff, b0, kb0);
-    issue(kb_n, koff, read_blocks(rn_i, 1), kb1);
-    if constexpr (PAR) issue(v_cache + (int64_t)kvh_n * B * D, voff, b0, vb0);
-  };
-  // loads issue_next leaves in flight: K0, K1 (and V0)
-  constexpr int kNextLoads = 2 * PW;
+  Blocks blk_k = n_step > 2 ? blocks_of(2) : Blocks{};  // entries of the next K copy
+  Blocks blk_v = n_step > 1 ? blocks_of(1) : Blocks{};  // entries of the next V copy
   auto iter = [&](int st, auto par_c, auto last_c) {
     constexpr bool PAR = decltype(par_c)::value;
     constexpr bool LAST = decltype(last_c)::value;
@@ -698,20 +581,13 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
     }
     if (st + 2 < n_step) blk_v = blocks_of(st + 2);
     if constexpr (LAST) {
-      if (has_next) issue_next(par_c);
       exp_only(P_);
     } else {
       phase_k(kb_read, P_, T_());
       if (st + 1 >= e_step) mask_scores(sbuf[PAR ? 0 : 1], st + 1);
     }
     // -- phase V
-    if constexpr (LAST) {
-      // V_st done; the successor's loads, younger, may stay in flight
-      if (has_next) wait_vmcnt<kNextLoads + (PAR ? PW : 0)>();
-      else wait_vmcnt<0>();
-    } else {
-      wait_groups((st + 2 < n_step) + (st + 1 < n_step));
-    }
+    wait_groups((st + 2 < n_step) + (st + 1 < n_step));
     barrier();
     if (st + 3 < n_step) {
       issue(kbase, koff, blk_k, kb_read);
@@ -733,142 +609,94 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
       });
     }
   };
-
-  for (;;) {
-    // S_0 = K0 . Q^T (K0 and Q of this record are complete in every wave)
-    barrier();
-    phase_k(kb0, std::integral_constant<int, 1>(), F_());  // writes sbuf[0]
-    if (e_step == 0) mask_scores(sbuf[0], 0);
-    first_max();
-    blk_k = n_step > 2 ? blocks_of(2) : Blocks{};
-    blk_v = n_step > 1 ? blocks_of(1) : Blocks{};
-    has_next = read_index(0) + 1 < read_index(1);
-
-    // iterations in pairs (even parity first), then the last one
-    int st = 0;
-    for (; st + 2 < n_step; st += 2) {
-      iter(st, F_(), F_());
-      iter(st + 1, T_(), F_());
-    }
-    if (st + 1 < n_step) {
-      iter(st, F_(), F_());
-      iter(st + 1, T_(), T_());
-    } else {
-      iter(st, F_(), T_());
-    }
-
-    // ---- finish: the two lane halves hold disjoint keys of the same query
-    // (the record's output fields come back from its LDS slot)
-    {
-      const PrefillRec cur = read_rec(read_index(0));
-      it.tok0 = cur.tok0, it.part = cur.part, it.kvh = cur.kvh;
-    }
-    static_for<0, RG>([&](auto rg_c) {
-      constexpr int rg = decltype(rg_c)::value;
-      const float l_tot = halves_sum(l_run[rg]);
-      if (!row_valid[rg]) return;
-      const int row = (wave * RG + rg) * 32 + col;
-      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      if (it.part < 0) {
-        uint16_t* op = out + ((int64_t)(it.tok0 + tl[rg]) * hq + it.kvh * G + row % G) * D + 4 * g;
-        static_for<0, NDT>([&](auto dt_c) {
-          constexpr int dt = decltype(dt_c)::value;
-          static_for<0, 4>([&](auto i_c) {
-            constexpr int i = decltype(i_c)::value;
-            uint2 w;
-            w.x = pack_bf16x2(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv);
-            w.y = pack_bf16x2(oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
-            *reinterpret_cast<uint2*>(op + dt * 32 + 8 * i) = w;
-          });
-        });
-      } else {
-        const int prow = it.part + row;
-        float* pp = part_o + (int64_t)prow * D + 4 * g;
-        static_for<0, NDT>([&](auto dt_c) {
-          constexpr int dt = decltype(dt_c)::value;
-          static_for<0, 4>([&](auto i_c) {
-            constexpr int i = decltype(i_c)::value;
-            *reinterpret_cast<float4*>(pp + dt * 32 + 8 * i) =
-                make_float4(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv,
-                            oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
-          });
-        });
-        if (g == 0) part_lse[prow] = l_tot > 0.f ? m_run[rg] + __log2f(l_tot) : -INFINITY;
-      }
-    });
-
-    // ---- on to the next record: its K0 and K1 are in flight, and V0 too
-    // if the last iteration read vb1; otherwise V0 goes to vb0 once every
-    // wave is past its last PV products.
-    if (!has_next) break;
-    const bool v0_issued = ((n_step - 1) & 1) != 0;
-    const int r = read_index(0) + 1;
-    write_index(0, r);
-    set_item(read_rec(r));
-    set_rows();
-    reset_acc();
-    load_q(it);
-    if (!v0_issued) {
-      barrier();
-      issue(vbase, voff, read_blocks(r, 0), vb0);
-    }
-    wait_vmcnt<0>();  // this record's Q, K0, K1, V0 and the previous stores
-    wait_lgkm0();     // LDS reads above have returned before the fetch-ahead lands
-    compiler_fence();
-    // fetch-ahead: the table entries of record r + 1 (its record is in LDS
-    // since record r - 1 started) and record r + 2
-    const int r_end = read_index(1);
-    if (r + 1 < r_end) prefetch_blocks(read_rec(r + 1), r + 1);
-    if (r + 2 < r_end) prefetch_rec(r + 2);
+  // iterations in pairs (even parity first), then the last one
+  int st = 0;
+  for (; st + 2 < n_step; st += 2) {
+    iter(st, F_(), F_());
+    iter(st + 1, T_(), F_());
   }
+  if (st + 1 < n_step) {
+    iter(st, F_(), F_());
+    iter(st + 1, T_(), T_());
+  } else {
+    iter(st, F_(), T_());
+  }
+
+  // ---- finish: the two lane halves hold disjoint keys of the same query
+  static_for<0, RG>([&](auto rg_c) {
+    constexpr int rg = decltype(rg_c)::value;
+    const float l_tot = halves_sum(l_run[rg]);
+    if (!row_valid[rg]) return;
+    const int row = (wave * RG + rg) * 32 + col;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    if (it.part < 0) {
+      uint16_t* op = out + ((int64_t)(it.tok0 + tl[rg]) * hq + kvh * G + row % G) * D + 4 * g;
+      static_for<0, NDT>([&](auto dt_c) {
+        constexpr int dt = decltype(dt_c)::value;
+        static_for<0, 4>([&](auto i_c) {
+          constexpr int i = decltype(i_c)::value;
+          uint2 w;
+          w.x = pack_bf16x2(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv);
+          w.y = pack_bf16x2(oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
+          *reinterpret_cast<uint2*>(op + dt * 32 + 8 * i) = w;
+        });
+      });
+    } else {
+      const int prow = it.part + row;
+      float* pp = part_o + (int64_t)prow * D + 4 * g;
+      static_for<0, NDT>([&](auto dt_c) {
+        constexpr int dt = decltype(dt_c)::value;
+        static_for<0, 4>([&](auto i_c) {
+          constexpr int i = decltype(i_c)::value;
+          *reinterpret_cast<float4*>(pp + dt * 32 + 8 * i) =
+              make_float4(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv,
+                          oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
+        });
+      });
+      if (g == 0) part_lse[prow] = l_tot > 0.f ? m_run[rg] + __log2f(l_tot) : -INFINITY;
+    }
+  });
 }
 
 template <int D, int B, int G, int NW>
-static hipError_t launch_prefill_t(const PrefillRec* recs, const int32_t* wg_off, int n_wg,
-                                   int n_recs, const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((prefill_kernel<D, B, G, NW, kPrefillRG>), dim3(n_wg), dim3(NW * 64), 0, s,
-                     recs, wg_off, n_recs, a.q, a.k_cache, a.v_cache, a.bt, a.out, a.part_o,
-                     a.part_lse, a.hq, a.hkv, a.mbr, a.scale_log2);
+static hipError_t launch_prefill_t(const PrefillRec* recs, int n, const AttnArgs& a,
+                                   hipStream_t s) {
+  hipLaunchKernelGGL((prefill_kernel<D, B, G, NW, kPrefillRG>), dim3(n), dim3(NW * 64), 0, s, recs,
+                     a.q, a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv,
+                     a.mbr, a.scale_log2);
   return hipGetLastError();
 }
 
 template <int D, int B, int NW>
-static hipError_t launch_prefill_g(int G, const PrefillRec* recs, const int32_t* wg_off, int n_wg,
-                                   int n_recs, const AttnArgs& a, hipStream_t s) {
+static hipError_t launch_prefill_g(int G, const PrefillRec* recs, int n, const AttnArgs& a,
+                                   hipStream_t s) {
   switch (G) {
-    case 1: return launch_prefill_t<D, B, 1, NW>(recs, wg_off, n_wg, n_recs, a, s);
-    case 2: return launch_prefill_t<D, B, 2, NW>(recs, wg_off, n_wg, n_recs, a, s);
-    case 4: return launch_prefill_t<D, B, 4, NW>(recs, wg_off, n_wg, n_recs, a, s);
-    case 8: return launch_prefill_t<D, B, 8, NW>(recs, wg_off, n_wg, n_recs, a, s);
+    case 1: return launch_prefill_t<D, B, 1, NW>(recs, n, a, s);
+    case 2: return launch_prefill_t<D, B, 2, NW>(recs, n, a, s);
+    case 4: return launch_prefill_t<D, B, 4, NW>(recs, n, a, s);
+    case 8: return launch_prefill_t<D, B, 8, NW>(recs, n, a, s);
   }
   return hipErrorInvalidValue;
 }
 
 template <int NW>
-static hipError_t launch_prefill_w(int D, int G, const PrefillRec* recs, const int32_t* wg_off,
-                                   int n_wg, int n_recs, const AttnArgs& a, hipStream_t s) {
-  if (D == 128 && a.block_size == 16)
-    return launch_prefill_g<128, 16, NW>(G, recs, wg_off, n_wg, n_recs, a, s);
-  if (D == 128 && a.block_size == 32)
-    return launch_prefill_g<128, 32, NW>(G, recs, wg_off, n_wg, n_recs, a, s);
-  if (D == 64 && a.block_size == 16)
-    return launch_prefill_g<64, 16, NW>(G, recs, wg_off, n_wg, n_recs, a, s);
-  if (D == 64 && a.block_size == 32)
-    return launch_prefill_g<64, 32, NW>(G, recs, wg_off, n_wg, n_recs, a, s);
+static hipError_t launch_prefill_w(int D, int G, const PrefillRec* recs, int n, const AttnArgs& a,
+                                   hipStream_t s) {
+  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, recs, n, a, s);
+  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, recs, n, a, s);
+  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, recs, n, a, s);
+  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, recs, n, a, s);
   return hipErrorInvalidValue;
 }
 
-// 256-row and 128-row tiles: 32 * kPrefillRG rows per wave; one persistent
-// workgroup per list.
+// 256-row and 128-row tiles: 32 * kPrefillRG rows per wave; one workgroup per record.
 hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s) {
   constexpr int kWide = kPrefillRowsWide / (32 * kPrefillRG), kNarrow = kPrefillRows / (32 * kPrefillRG);
   hipError_t e = hipSuccess;
-  if (a.n_prefill_wide_slots > 0)
-    e = launch_prefill_w<kWide>(D, G, a.prefill_wide, a.prefill_wide_slots, a.n_prefill_wide_slots,
-                                a.n_prefill_wide_items, a, s);
-  if (e == hipSuccess && a.n_prefill_slots > 0)
-    e = launch_prefill_w<kNarrow>(D, G, a.prefill, a.prefill_slots, a.n_prefill_slots,
-                                  a.n_prefill_items, a, s);
+  if (a.n_prefill_wide_items > 0)
+    e = launch_prefill_w<kWide>(D, G, a.prefill_wide, a.n_prefill_wide_items, a, s);
+  if (e == hipSuccess && a.n_prefill_items > 0)
+    e = launch_prefill_w<kNarrow>(D, G, a.prefill, a.n_prefill_items, a, s);
   return e;
 }
 

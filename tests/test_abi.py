@@ -283,19 +283,16 @@ def test_attn_run_rejects_lists_past_the_workspace():
     big = 4096
     assert run(off_decode=big - 64, n_decode=3) == binding.CP_ERR_INVALID_ARG     # 96 B past 4032
     assert run(off_merge=big - 32, n_merge=2) == binding.CP_ERR_INVALID_ARG
-    assert run(off_prefill_slots=big - 4, n_prefill_slots=2) == binding.CP_ERR_INVALID_ARG
-    assert run(off_prefill_wide_slots=big - 8, n_prefill_wide_slots=3) == binding.CP_ERR_INVALID_ARG
     assert run(off_prefill=big - 32, n_prefill_items=2) == binding.CP_ERR_INVALID_ARG
     assert run(off_prefill_wide=0, n_prefill_wide_items=129) == binding.CP_ERR_INVALID_ARG
     assert run(off_part_o=0, partial_rows=9) == binding.CP_ERR_INVALID_ARG        # 9 x 512 B
     assert run(off_part_lse=big - 8, partial_rows=3) == binding.CP_ERR_INVALID_ARG
     assert run(n_prefill_items=-1) == binding.CP_ERR_INVALID_ARG
-    # an empty launch has an empty offset list: a list offset at the very end
-    # of the workspace is fine then (nothing to launch, so this runs on a CPU)
-    assert run(off_prefill_slots=big, off_prefill_wide_slots=big, off_decode=big,
-               off_merge=big, off_part_o=big, off_part_lse=big) == binding.CP_OK
-    assert run(off_prefill_slots=big, n_prefill_slots=1) == binding.CP_ERR_INVALID_ARG
     assert run(partial_rows=-1) == binding.CP_ERR_INVALID_ARG
+    # empty lists may start at the very end of the workspace (nothing to
+    # launch, so this runs on a CPU)
+    assert run(off_prefill=big, off_prefill_wide=big, off_decode=big, off_merge=big,
+               off_part_o=big, off_part_lse=big) == binding.CP_OK
 
 
 def test_prepared_plan_lists_fit_its_workspace():
