@@ -106,11 +106,12 @@ def cpu_baseline(batches, pools0, steps_host, budget_s=10.0, seed=0):
     the (token, q head) outputs of every batch, in order.  Each batch's pools
     are rebuilt on the host by the oracle's own append, batch after batch, in
     ``pools0`` (written in place), so every sampled output reads the context
-    it reads on the GPU.
-    Each output is drawn with one probability f, chosen from a pilot so that
-    the timed work is about ``budget_s``; only the attention calls are timed
-    (the append is a bit copy, under 0.1 % of the oracle's work).  Tokens/s is
-    sampled outputs / Hq over the timed seconds."""
+    it reads on the GPU.  Batch i's outputs are each drawn with probability
+    f_i, set from the seconds per key read measured so far (a warmed-up pilot
+    first) so that the timed work comes to about ``budget_s``; the whole job's
+    time is estimated as sum(t_i / f_i) over the batches' timed calls, and
+    tokens/s = all tokens / that time.  Only the attention calls are timed
+    (the append is a bit copy, under 0.1 % of the oracle's work)."""
     import numpy as np
     import oracle
 
@@ -122,35 +123,44 @@ def cpu_baseline(batches, pools0, steps_host, budget_s=10.0, seed=0):
                              [np.zeros(0, np.int64)])
         return np.repeat(pos + 1, Hq)
 
-    total_keys = sum(int(keys_per_output(b).sum()) for b in batches)
+    kpos = [keys_per_output(b) for b in batches]
+    keys_left = float(sum(int(k.sum()) for k in kpos))
     kc, vc = pools0
-    f, timed, n_out, n_all = None, 0.0, 0, 0
+    per_key, spent, keys_timed, est_total, n_out, n_all, fs = None, 0.0, 0, 0.0, 0, 0, []
     for i, b in enumerate(batches):
         kc, vc = oracle.kv_append(b, steps_host[i]["k_new"], steps_host[i]["v_new"], kc, vc,
                                   inplace=True)
-        kpo = keys_per_output(b)
+        kpo = kpos[i]
         n_all += kpo.size
         if kpo.size == 0:
             continue
-        if f is None:  # pilot: seconds per key read, on the first batch
-            pilot = rng.choice(kpo.size, size=min(kpo.size, 64), replace=False)
+        if per_key is None:  # pilot on the first batch, after one warm-up call
+            oracle.attn(b, steps_host[i]["q"], kc, vc, sel=rng.choice(kpo.size, 16))
+            pilot = rng.choice(kpo.size, size=min(kpo.size, 256), replace=False)
             t0 = time.perf_counter()
             oracle.attn(b, steps_host[i]["q"], kc, vc, sel=pilot)
             per_key = (time.perf_counter() - t0) / max(1, int(kpo[pilot].sum()))
-            f = min(1.0, budget_s / max(per_key * total_keys, 1e-9))
+        f = min(1.0, max(1e-4, (budget_s - spent) / max(per_key * keys_left, 1e-9)))
+        fs.append(f)
+        keys_left -= float(kpo.sum())
         sel = np.nonzero(rng.random(kpo.size) < f)[0]
         if sel.size == 0:
             continue
         t0 = time.perf_counter()
         oracle.attn(b, steps_host[i]["q"], kc, vc, sel=sel)
-        timed += time.perf_counter() - t0
+        dt = time.perf_counter() - t0
+        spent += dt
+        est_total += dt / f
+        keys_timed += int(kpo[sel].sum())
+        per_key = spent / max(1, keys_timed)
         n_out += sel.size
-    tok = n_out / Hq
-    return {"value": tok / timed if timed > 0 else None, "unit": "tokens/s",
+    tokens = n_all / Hq
+    return {"value": tokens / est_total if est_total > 0 else None, "unit": "tokens/s",
             "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{n_out} of {n_all} (token, q head) outputs over all {len(batches)} "
-                      f"batch(es), each drawn with probability {f:.4f}, fp64 attention only, "
-                      f"{timed:.2f} s"}
+                      f"batch(es), drawn with per-batch probability {min(fs):.4f}-{max(fs):.4f}; "
+                      f"fp64 attention only, {spent:.2f} s timed, whole job estimated as the sum "
+                      f"of each batch's time / its probability"}
 
 
 # --------------------------------------------------------------------------- gpu run
@@ -1006,6 +1016,81 @@ def per_iteration(cfg, reps=7):
     return {"mix": cfg, "reps": reps, "iterations": out}
 
 
+FEW_TOKEN_LENS = (2, 3, 4, 8, 16)
+FEW_TOKEN_PRIORS = (0, 1024, 4096)
+
+
+def few_token_routing(n_chunks=64, reps=20):
+    """Attention time of batches of n_chunks c-token chunks (one per request,
+    prior context P), routed either to the MFMA tile kernel or to the decode
+    kernel one query token at a time (CP_PREFILL_MIN_LEN), at the Llama-3-8B
+    (32/8 heads, block 16) and 70B (64/8 heads, block 32) shapes, head_dim 128.
+    The two routings compute the same outputs; the faster one for each
+    (shape, c, P) is what the planner's threshold should pick."""
+    import numpy as np
+    import torch
+    import paper_2606_09061_amd as cp
+    from paper_2606_09061_amd import binding
+    import workloads as wl
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    out = []
+    # one untimed pass over both routings first (first launches load kernels)
+    for hq, hkv, bsz in ((32, 8, 16), (64, 8, 32)):
+        b = wl.make_batch("warm", hq, hkv, 128, bsz, [(64, 4)] * 8, np.random.default_rng(0))
+        t = wl.make_tensors(b, seed=1, device=dev)
+        d = cp.desc_for(b)
+        ws = torch.empty(1 << 22, dtype=torch.uint8, device=dev)
+        o = torch.empty(b.num_tokens, hq, 128, dtype=torch.bfloat16, device=dev)
+        for min_len in ("2", "5"):
+            os.environ["CP_PREFILL_MIN_LEN"] = min_len
+            cp.attn_mixed(d, t["q"], t["k_cache"], t["v_cache"], t["block_tables"], b.rows, o, ws)
+        os.environ.pop("CP_PREFILL_MIN_LEN", None)
+    torch.cuda.synchronize()
+    for hq, hkv, bsz in ((32, 8, 16), (64, 8, 32)):
+        for P in FEW_TOKEN_PRIORS:
+            for c in FEW_TOKEN_LENS:
+                rng = np.random.default_rng([hq, P, c])
+                b = wl.make_batch("few", hq, hkv, 128, bsz, [(P, c)] * n_chunks, rng)
+                t = wl.make_tensors(b, seed=9000 + c, device=dev)
+                d = cp.desc_for(b)
+                need = cp.workspace_bytes(d, b.rows)
+                os.environ["CP_PREFILL_MIN_LEN"] = str(c + 1)
+                try:
+                    need = max(need, cp.workspace_bytes(d, b.rows))
+                finally:
+                    os.environ.pop("CP_PREFILL_MIN_LEN", None)
+                ws = torch.empty(need, dtype=torch.uint8, device=dev)
+                o = torch.empty(b.num_tokens, hq, 128, dtype=torch.bfloat16, device=dev)
+                cp.kv_append(d, t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                             t["block_tables"], b.rows, ws)
+                row = {"heads": [hq, hkv], "block": bsz, "prior": P, "chunk": c,
+                       "chunks": n_chunks}
+                for route, min_len in (("tile", "2"), ("decode", str(c + 1))):
+                    os.environ["CP_PREFILL_MIN_LEN"] = min_len
+                    try:
+                        for _ in range(3):
+                            cp.attn_mixed(d, t["q"], t["k_cache"], t["v_cache"], t["block_tables"],
+                                          b.rows, o, ws)
+                        torch.cuda.synchronize()
+                        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                        ev[0].record()
+                        for _ in range(reps):
+                            cp.attn_mixed(d, t["q"], t["k_cache"], t["v_cache"], t["block_tables"],
+                                          b.rows, o, ws)
+                        ev[1].record()
+                        ev[1].synchronize()
+                        row[route + "_us"] = ev[0].elapsed_time(ev[1]) * 1e3 / reps
+                    finally:
+                        os.environ.pop("CP_PREFILL_MIN_LEN", None)
+                row["faster"] = "decode" if row["decode_us"] < row["tile_us"] else "tile"
+                out.append(row)
+                log(f"[few-token] {row}")
+                del t, ws, o
+    return {"few_token_routing": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -1038,6 +1123,9 @@ def main():
     ap.add_argument("--per-iteration", action="store_true",
                     help="prefill / decode kernel time of every batch of --config (mix 5: its "
                          "20 iterations) against its algorithmic work")
+    ap.add_argument("--few-token", action="store_true",
+                    help="only time few-token chunks on the tile kernel against the decode "
+                         "kernel token by token")
     ap.add_argument("--fit", default=None, metavar="CSV",
                     help="only fit a latency table written earlier (no GPU)")
     args = ap.parse_args()
@@ -1056,6 +1144,9 @@ def main():
     if args.sched:
         print(json.dumps(sched_experiment(args.sched, engine=args.sched_engine,
                                           parts=tuple(args.sched_parts.split(",")))), flush=True)
+        return
+    if args.few_token:
+        print(json.dumps(few_token_routing()), flush=True)
         return
     if args.per_iteration:
         print(json.dumps(per_iteration(args.config)), flush=True)
