@@ -144,7 +144,11 @@ int cp_kv_append(const cp_attn_desc *desc, const void *k_new, const void *v_new,
  * over keys [0, its position]; L is 2 unless the environment variable
  * CP_PREFILL_MIN_LEN sets it (clamped to [2, 64], read on every call; every
  * value gives the same definition).  Long key ranges are split and merged by
- * a log-sum-exp pass. */
+ * a log-sum-exp pass.  When a step has both kinds of rows, the decode work
+ * runs inside the prefill launch (workgroups streaming K/V beside the
+ * workgroups on the matrix cores) unless CP_FUSE_DECODE=0 gives it a launch
+ * of its own; CP_FUSE_DECODE 1 / 2 / 3 place those workgroups after / before /
+ * among the prefill tiles (3 is the default); outputs are the same bits. */
 int cp_attn_mixed(const cp_attn_desc *desc, const void *q, const void *k_cache,
                   const void *v_cache, const int32_t *block_tables, const cp_row_meta *rows,
                   int32_t n_rows, void *out, void *ws, size_t ws_bytes, void *stream);
@@ -165,6 +169,11 @@ typedef struct {
     int64_t off_prefill, off_prefill_wide, off_decode, off_merge;
     int64_t off_part_o, off_part_lse;  /* byte offsets in ws */
     int64_t partial_rows;         /* fp32 partial rows of split key ranges    */
+    int32_t decode_in_prefill;    /* 0: decode items have their own launch;
+                                   * 1 / 2: they run inside the 128-row / 256-row
+                                   * prefill launch, whose record list then
+                                   * names them                                */
+    int32_t reserved;             /* 0                                         */
 } cp_attn_plan;
 
 /* Validates the batch, plans it and uploads the plan into ws (asynchronous on
@@ -178,8 +187,8 @@ int cp_attn_prepare(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n
  * the plan was prepared in (ws_bytes >= plan->ws_bytes); stream order must put
  * the prepare before the run.  Every list the plan names (its offset plus
  * its length times the item size) must lie inside plan->ws_bytes, else
- * CP_ERR_INVALID_ARG and nothing is enqueued; the kernels skip any prefill
- * slot that does not index an item of the plan. */
+ * CP_ERR_INVALID_ARG and nothing is enqueued; a decode block of a prefill
+ * record list that names no decode unit of the plan does nothing. */
 int cp_attn_run(const cp_attn_plan *plan, const void *q, const void *k_cache,
                 const void *v_cache, const int32_t *block_tables, void *out, void *ws,
                 size_t ws_bytes, void *stream);
@@ -196,6 +205,17 @@ int cp_plan_summary(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n
  * and returns n (the full count), or a negative CP_ERR_* code. */
 int64_t cp_plan_items(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows,
                       int32_t *items, int64_t cap);
+
+/* Host-only copy of one prefill launch's record list in dispatch order
+ * (which = 0: 128-row tiles, 1: 256-row tiles), for layout tests: workgroup i
+ * runs record i, 8 int32 {first token, tokens, first position, req_id, key
+ * begin, key end, first partial row or -1, kv head}.  tokens == 0 marks an
+ * idle record; tokens == -1 a decode block, whose first token and first
+ * position fields name the decode units of its waves 0-3 and 4-7 (-1: none;
+ * unit u is decode item u / num_kv_heads for kv head u % num_kv_heads).
+ * Writes min(cap, n) records and returns n, or a negative CP_ERR_* code. */
+int64_t cp_plan_records(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n_rows,
+                        int32_t which, int32_t *recs, int64_t cap);
 
 /* ---- Allocation-free variant of cp_attn_mixed --------------------------
  *

@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     kv_append,
     make_desc,
     plan_items,
+    plan_records,
     plan_summary,
     version,
     workspace_bytes,

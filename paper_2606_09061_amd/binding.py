@@ -53,7 +53,8 @@ class AttnPlan(ctypes.Structure):
                 ("n_decode", ctypes.c_int32), ("n_merge", ctypes.c_int32)] + [
         (n, ctypes.c_int64) for n in ("off_prefill", "off_prefill_wide", "off_decode",
                                       "off_merge", "off_part_o", "off_part_lse",
-                                      "partial_rows")]
+                                      "partial_rows")] + [
+        ("decode_in_prefill", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 _lib = None
@@ -89,6 +90,8 @@ def load():
     lib.cp_plan_summary.restype = ctypes.c_int
     lib.cp_plan_items.argtypes = [dp, vp, i32, vp, i64]
     lib.cp_plan_items.restype = i64
+    lib.cp_plan_records.argtypes = [dp, vp, i32, i32, vp, i64]
+    lib.cp_plan_records.restype = i64
     lib.cp_noalloc_init.argtypes, lib.cp_noalloc_init.restype = [], ctypes.c_int
     lib.cp_attn_mixed_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, i32, vp, vp]
     lib.cp_attn_mixed_noalloc.restype = ctypes.c_int
@@ -102,6 +105,7 @@ def exported_symbols():
     return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch",
             "cp_check_block_tables", "cp_kv_append",
             "cp_attn_mixed", "cp_attn_prepare", "cp_attn_run", "cp_plan_summary", "cp_plan_items",
+            "cp_plan_records",
             "cp_noalloc_init", "cp_attn_mixed_noalloc", "cp_profile_begin", "cp_profile_end"]
 
 
@@ -248,6 +252,22 @@ def plan_summary(desc: Desc, rows) -> dict:
     keys = ["prefill_items", "decode_items", "merge_groups", "partial_rows", "workspace_bytes",
             "decode_split_blocks"]
     return dict(zip(keys, (int(x) for x in c)))
+
+
+def plan_records(desc: Desc, rows, which: int) -> np.ndarray:
+    """[n, 8] int32: one prefill launch's records in dispatch order (which 0:
+    128-row tiles, 1: 256-row tiles); columns tok0, n_tok, pos0, req, key
+    begin, key end, part, kv head (n_tok 0: idle, -1: decode block)."""
+    r = _rows(rows)
+    lib = load()
+    n = lib.cp_plan_records(ctypes.byref(desc), r.ctypes.data, r.shape[0], int(which), None, 0)
+    if n < 0:
+        raise CpError(int(n), "cp_plan_records")
+    out = np.zeros((max(n, 1), 8), dtype=np.int32)
+    n2 = lib.cp_plan_records(ctypes.byref(desc), r.ctypes.data, r.shape[0], int(which),
+                             out.ctypes.data, n)
+    assert n2 == n
+    return out[:n]
 
 
 def plan_items(desc: Desc, rows) -> np.ndarray:

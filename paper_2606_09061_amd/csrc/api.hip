@@ -336,6 +336,8 @@ void fill_plan(const Plan& p, cp_attn_plan& pl) {
   pl.n_prefill_items = (int32_t)p.prefill.size();
   pl.n_prefill_wide_items = (int32_t)p.prefill_wide.size();
   pl.partial_rows = p.partial_rows;
+  pl.decode_in_prefill = p.decode_in_prefill;
+  pl.reserved = 0;
 }
 
 // Allocation-free upload: writes the plan straight into one of the device's
@@ -475,6 +477,23 @@ int64_t cp_plan_items(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t
   }
 }
 
+int64_t cp_plan_records(const cp_attn_desc* desc, const cp_row_meta* rows, int32_t n_rows,
+                        int32_t which, int32_t* recs, int64_t cap) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  if ((which != 0 && which != 1) || (cap > 0 && !recs)) return CP_ERR_INVALID_ARG;
+  try {
+    Plan& p = thread_plan();
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    const std::vector<PrefillRec>& l = which ? p.prefill_wide : p.prefill;
+    const int64_t n = (int64_t)l.size();
+    if (cap > 0) std::memcpy(recs, l.data(), (size_t)std::min(cap, n) * sizeof(PrefillRec));
+    return n;
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
+}
+
 int cp_kv_append(const cp_attn_desc* desc, const void* k_new, const void* v_new, void* k_cache,
                  void* v_cache, const int32_t* block_tables, const cp_row_meta* rows,
                  int32_t n_rows, void* ws, size_t ws_bytes, void* stream) {
@@ -586,6 +605,12 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   if (plan->ws_bytes <= 0 || plan->n_prefill_items < 0 || plan->n_prefill_wide_items < 0 ||
       plan->n_decode < 0 || plan->n_merge < 0 || plan->partial_rows < 0)
     return CP_ERR_INVALID_ARG;
+  // decode items inside a prefill launch need that launch
+  if (plan->decode_in_prefill < 0 || plan->decode_in_prefill > 2 ||
+      (plan->decode_in_prefill == 1 && plan->n_prefill_items == 0) ||
+      (plan->decode_in_prefill == 2 && plan->n_prefill_wide_items == 0) ||
+      (int64_t)plan->n_decode * desc->num_kv_heads > INT32_MAX)
+    return CP_ERR_INVALID_ARG;
   if ((size_t)plan->ws_bytes > ws_bytes) return CP_ERR_WORKSPACE;
   if (!q || !k_cache || !v_cache || !block_tables || !out || !ws) return CP_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
@@ -615,6 +640,7 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
   a.n_prefill_wide_items = plan->n_prefill_wide_items;
   a.decode = reinterpret_cast<const DecodeItem*>(base + plan->off_decode);
   a.n_decode = plan->n_decode;
+  a.decode_in_prefill = plan->decode_in_prefill;
   a.merge = reinterpret_cast<const MergeGroup*>(base + plan->off_merge);
   a.n_merge = plan->n_merge;
   a.q = static_cast<const uint16_t*>(q);
@@ -639,7 +665,7 @@ int cp_attn_run(const cp_attn_plan* plan, const void* q, const void* k_cache, co
     rc = finish(e, s);
     if (rc != CP_OK) return rc;
   }
-  if (a.n_decode > 0) {
+  if (a.n_decode > 0 && a.decode_in_prefill == 0) {
     const long pi = prof_open(2, s);
     const hipError_t e = launch_decode(D, desc->block_size, G, a, s);
     prof_close(pi, s);

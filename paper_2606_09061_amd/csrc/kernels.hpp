@@ -31,8 +31,9 @@ struct AttnArgs {
   int n_prefill_items;
   const PrefillRec* prefill_wide;   // 256-row tiles (8-wave kernel)
   int n_prefill_wide_items;
-  const DecodeItem* decode;         // grid (n_decode, hkv)
+  const DecodeItem* decode;         // grid (n_decode, hkv), or units of a prefill launch
   int n_decode;
+  int decode_in_prefill;            // 0: own launch; 1 / 2: inside the 128- / 256-row launch
   const MergeGroup* merge;          // grid (n_merge, hkv)
   int n_merge;
   const uint16_t* q;

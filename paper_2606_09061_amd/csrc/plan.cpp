@@ -120,6 +120,70 @@ void interleave_by_xcd(const std::vector<detail::PrefillItem>& items, int Hkv, i
   while (!recs.empty() && recs.back().n_tok == 0) recs.pop_back();
 }
 
+// Adds the decode blocks (n_units units, per_block per workgroup) to a prefill
+// record list.  mode 1 appends them after the tiles; modes 2 (before the
+// tiles), 3 (spread evenly over the first `spread` fraction of them, the
+// longest units first) and 4 (rows of decode blocks and rows of tiles merged
+// longest first, a decode unit of k keys costing k / keys_per_step tile
+// steps) insert whole rows of X records, so every tile keeps its position
+// mod X, i.e. its XCD.  Decode blocks dispatched among tiles stream K/V from
+// HBM while the tiles around them keep the matrix cores busy.
+void place_decode_blocks(std::vector<PrefillRec>& recs, const std::vector<DecodeItem>& dec,
+                         int Hkv, bool wide, const Tuning& t, PlanScratch& sc) {
+  const int per_block = wide ? 2 : 1;
+  const int64_t n_units = (int64_t)dec.size() * Hkv;
+  const int64_t X = std::max(1, t.num_xcds);
+  const int64_t n_blk = ceil_div(n_units, per_block);
+  const PrefillRec idle{0, 0, 0, 0, 0, 0, -1, 0};
+  auto marker = [&](int64_t b) {
+    const int64_t u0 = b * per_block;
+    const int64_t u1 = per_block > 1 && u0 + 1 < n_units ? u0 + 1 : -1;
+    return PrefillRec{(int32_t)u0, kDecodeBlock, (int32_t)u1, 0, 0, 0, -1, 0};
+  };
+  if (t.fuse_decode == 1) {
+    for (int64_t b = 0; b < n_blk; ++b) recs.push_back(marker(b));
+    return;
+  }
+  auto& old = sc.recs_tmp;
+  old.swap(recs);
+  recs.clear();
+  const int64_t R = ceil_div((int64_t)old.size(), X), M = ceil_div(n_blk, X);
+  // mode 3: marker rows spread over the first R3 tile rows
+  const double spread = std::min(1.0, std::max(0.0, t.fuse_spread));
+  const int64_t R3 = std::max<int64_t>(1, (int64_t)std::ceil(spread * (double)R));
+  // mode 4: row costs in tile steps (a row's first record is its longest)
+  auto tile_row_cost = [&](int64_t r) {
+    const PrefillRec& q = old[(size_t)(r * X)];
+    return (double)ceil_div(q.kv_end - q.kv_begin, kPrefillKeys) * (wide ? 2.0 : 1.0);
+  };
+  auto dec_row_cost = [&](int64_t m) {
+    const DecodeItem& it = dec[(size_t)(m * X * per_block / Hkv)];
+    return (double)(it.kv_end - it.kv_begin) / std::max(1.0, t.fuse_keys_per_step);
+  };
+  int64_t pi = 0, mi = 0;
+  while (pi < R || mi < M) {
+    bool take_m = false;
+    if (mi < M) {
+      if (pi >= R || t.fuse_decode == 2) take_m = true;
+      else if (t.fuse_decode == 3)  // midpoints as fractions of their spans
+        take_m = pi >= R3 || (2 * mi + 1) * R3 <= (2 * pi + 1) * M;
+      else
+        take_m = dec_row_cost(mi) > tile_row_cost(pi);
+    }
+    for (int64_t x = 0; x < X; ++x) {
+      if (take_m) {
+        const int64_t b = mi * X + x;
+        recs.push_back(b < n_blk ? marker(b) : idle);
+      } else {
+        const int64_t k = pi * X + x;
+        recs.push_back(k < (int64_t)old.size() ? old[(size_t)k] : idle);
+      }
+    }
+    (take_m ? mi : pi) += 1;
+  }
+  while (!recs.empty() && recs.back().n_tok == 0) recs.pop_back();
+}
+
 // Makespan, in steps, of longest-first list scheduling of `groups` (cost,
 // count) on `slots` identical slots.  Slot loads are kept as a histogram
 // (load, slots) sorted by load, so equal items are placed in bulk.
@@ -215,6 +279,12 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_DECODE_TARGET_ITEMS")) t.decode_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_TARGET_ITEMS")) t.prefill_target_items = atoi(s);
   if (const char* s = std::getenv("CP_PREFILL_MIN_SPLIT")) t.prefill_min_split = std::max(1, atoi(s));
+  if (const char* s = std::getenv("CP_FUSE_DECODE")) t.fuse_decode = std::min(4, std::max(0, atoi(s)));
+  if (const char* s = std::getenv("CP_FUSE_SPREAD")) t.fuse_spread = atof(s);
+  if (const char* s = std::getenv("CP_FUSE_KEYS_PER_STEP")) t.fuse_keys_per_step = atof(s);
+  if (const char* s = std::getenv("CP_FUSE_NARROW")) t.fuse_narrow = atoi(s) != 0;
+  if (const char* s = std::getenv("CP_FUSE_UNITS_PER_CU")) t.fuse_units_per_cu = atof(s);
+  if (const char* s = std::getenv("CP_FUSE_FLOPS_PER_BYTE")) t.fuse_flops_per_byte = atof(s);
   if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::min(64, std::max(1, atoi(s)));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_ROWS"))
     t.prefill_wide_min_rows = std::max<int64_t>(1, atoll(s));
@@ -362,14 +432,22 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   // whose start-up and drain nothing overlaps: they pay only when the step's
   // queries see long key ranges (token-weighted mean of chunk_start + len / 2).
   // The choice is per step, so that all prefill tiles share one launch.
+  // When the step's decode rows run inside the prefill launch, 128-row tiles
+  // leave each CU a second workgroup slot, which a decode block can take
+  // beside a tile (measured: the prefill-heavy 2k-token mix runs 6 % faster
+  // fused on 128-row tiles than fused on 256-row ones).
   double pf_tok = 0, pf_keys = 0;
+  bool has_decode = false;
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
+    if (m.chunk_len > 0 && m.chunk_len < t.prefill_min_len) has_decode = true;
     if (m.chunk_len < t.prefill_min_len) continue;
     pf_tok += m.chunk_len;
     pf_keys += (double)m.chunk_len * ((double)m.chunk_start + 0.5 * m.chunk_len);
   }
-  const bool long_keys = pf_tok > 0 && pf_keys >= (double)t.prefill_wide_min_keys * pf_tok;
+  const bool fused = t.fuse_decode > 0 && has_decode && pf_tok > 0;
+  const bool long_keys = !(fused && t.fuse_narrow) && pf_tok > 0 &&
+                         pf_keys >= (double)t.prefill_wide_min_keys * pf_tok;
   for (int32_t r = 0; r < n_rows; ++r) {
     const cp_row_meta& m = rows[r];
     if (m.chunk_len < t.prefill_min_len) continue;
@@ -464,7 +542,13 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     // rising to 6 per CU at 4 GB and above, where finer items balance the
     // tail better (measured on the 0.1, 0.8, 1.8 and 5.5 GB mixes).
     const double dec_bytes = (double)dec_blocks * B * d.head_dim * 4.0;
-    const double per_cu = 3.0 + 3.0 * std::min(1.0, dec_bytes / 4.0e9);
+    double per_cu = 3.0 + 3.0 * std::min(1.0, dec_bytes / 4.0e9);
+    // Inside a prefill-dominated launch, fewer and longer decode units: each
+    // one streams beside the tiles for much of the launch (measured best at
+    // about one per CU on the 2k-token prefill-heavy mix and the 70B replay;
+    // decode-dominated steps keep the rule above).
+    const double pf_flops = 4.0 * d.head_dim * d.num_q_heads * pf_keys;
+    if (fused && pf_flops > t.fuse_flops_per_byte * dec_bytes) per_cu = t.fuse_units_per_cu;
     const int64_t target = t.decode_target_items > 0
                                ? t.decode_target_items
                                : std::max<int64_t>(1, (int64_t)(t.num_cus * per_cu));
@@ -509,6 +593,18 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
         it.pad0 = it.pad1 = 0;
       }
     });
+  }
+
+  // ---- decode blocks inside the prefill launch ----------------------------
+  // The launch that runs last (128-row tiles when there are any) takes the
+  // decode units: one per 4-wave workgroup, two per 8-wave one.
+  p.decode_in_prefill = 0;
+  if (t.fuse_decode > 0 && !p.decode.empty() && !(p.prefill.empty() && p.prefill_wide.empty())) {
+    const bool wide = p.prefill.empty();
+    const int64_t n_units = (int64_t)p.decode.size() * Hkv;
+    if (n_units > INT32_MAX) throw std::length_error("decode unit index overflows int32");
+    place_decode_blocks(wide ? p.prefill_wide : p.prefill, p.decode, Hkv, wide, t, sc);
+    p.decode_in_prefill = wide ? 2 : 1;
   }
 
   // ---- workspace layout ------------------------------------------------

@@ -37,6 +37,13 @@ constexpr int kMaxPrefillMinLen = 64;
 // one record, a (tile, key split, kv head), the one its index names: the
 // planner lays the records out in the order the workgroups are dispatched to
 // the XCDs, padded with idle records (n_tok == 0).
+//
+// When a step's decode rows run inside its prefill launch, that launch's
+// record list also holds decode blocks (n_tok == kDecodeBlock): a workgroup of
+// NW waves runs NW / 4 decode units, unit u being decode item u / num_kv_heads
+// for kv head u % num_kv_heads; tok0 names the unit of waves 0-3 and pos0 the
+// unit of waves 4-7 (-1: none).
+constexpr int32_t kDecodeBlock = -1;
 
 struct PrefillRec {   // 32 bytes
   int32_t tok0;       // first query token (index into q / out)
@@ -95,6 +102,14 @@ struct Tuning {
   int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
   int64_t prefill_wide_min_rows = 129;  // chunks with chunk_len * G >= this use 256-row tiles,
   int64_t prefill_wide_min_keys = 1200; // ... when the step's mean key range per query is this
+  int fuse_decode = 4;          // decode units in the (last) prefill launch: 0 no (own launch),
+                                // 1 after its tiles, 2 before them, 3 spread among them,
+                                // 4 longest first with them
+  double fuse_spread = 1.0;     // mode 3: decode blocks spread over this fraction of the tiles
+  double fuse_keys_per_step = 64.0;  // mode 4: decode keys worth one 64-key step of a tile
+  bool fuse_narrow = true;      // a step with decode blocks in its prefill launch: 128-row tiles
+  double fuse_units_per_cu = 1.0;    // decode units per CU when prefill dominates a fused step
+  double fuse_flops_per_byte = 180.0;  // prefill dominates: its flops > this x decode bytes
 };
 
 namespace detail {
@@ -132,6 +147,7 @@ struct PlanScratch {
   std::vector<uint32_t> cut_lim;                      // per tile: last key a split may start at
   std::vector<std::pair<int64_t, int64_t>> groups2;  // (cost, count) of one split candidate
   std::vector<std::pair<int64_t, int64_t>> load_hist; // (slot load, slots), by load
+  std::vector<PrefillRec> recs_tmp;                   // a record list being re-laid out
 };
 
 struct Plan {
@@ -142,6 +158,9 @@ struct Plan {
   std::vector<MergeGroup> merge;
   int64_t partial_rows = 0;
   int32_t decode_split_blocks = 0;
+  // 0: the decode items have their own launch; 1 / 2: their units run as decode
+  // blocks inside the 128-row / 256-row prefill launch
+  int32_t decode_in_prefill = 0;
   // workspace layout (byte offsets from the workspace base)
   size_t off_prefill = 0, off_prefill_wide = 0, off_decode = 0, off_merge = 0, off_part_o = 0,
          off_part_lse = 0;

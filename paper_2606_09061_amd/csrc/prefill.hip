@@ -35,6 +35,7 @@
 // the in-flight copies from the reads.  The copy of a tile is issued 1.5
 // iterations before it is read; every phase starts with a wait on the copies
 // it needs and one barrier.
+#include "decode_body.hpp"
 #include "device.hpp"
 #include "kernels.hpp"
 #include "prefill_common.hpp"
@@ -156,7 +157,8 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
     const PrefillRec* __restrict__ recs, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
     const int32_t* __restrict__ bt, uint16_t* __restrict__ out, float* __restrict__ part_o,
-    float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2) {
+    float* __restrict__ part_lse, int hq, int hkv, int mbr, float scale_log2,
+    const DecodeItem* __restrict__ dec, int n_units) {
   using C = PrefillGeom<D, B, NW>;
   using L = PrefillLayout<D, B>;
   constexpr int NKS = C::NKS, NDT = C::NDT, NQK = C::NQK, NPV = C::NPV, PW = C::PW;
@@ -172,6 +174,24 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
   // this workgroup's record (the grid is the record list, in the planner's
   // XCD-interleaved order); records with no tokens are idle padding
   const PrefillRec it = recs[blockIdx.x];
+  if (it.n_tok == kDecodeBlock) {
+    // NW / 4 decode units, one per group of four waves, each on LDS buffers
+    // of its own (a decode block copies no tiles); the decode rows' K/V
+    // stream from HBM while the tiles' workgroups keep the matrix cores busy
+    using DL = decode_impl::DecodeLds<D, G>;
+    static_assert(DL::O_BYTES <= C::TILE_BYTES && DL::SMALL_BYTES <= C::TILE_BYTES, "decode LDS");
+    static_assert(NW == 4 || NW == 8, "decode groups");
+    const int grp = uniform((int)threadIdx.x >> 8);
+    const int u = grp == 0 ? it.tok0 : it.pos0;
+    const bool active = u >= 0 && u < n_units;
+    DecodeItem di{0, 0, 0, 0, -1, 0, 0, 0};
+    if (active) di = dec[u / hkv];
+    decode_unit<D, B, G>(di, active ? u % hkv : 0, active, (int)threadIdx.x & 255, q, k_cache,
+                         v_cache, bt, out, part_o, part_lse, hq, hkv, mbr, scale_log2,
+                         decode_impl::DecodeLdsPtrs{reinterpret_cast<float*>(grp == 0 ? kb0 : kb1),
+                                                    grp == 0 ? vb0 : vb1});
+    return;
+  }
   if (it.n_tok <= 0) return;
   const int kvh = it.kvh;
   const int tid = threadIdx.x;
@@ -659,44 +679,48 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
 }
 
 template <int D, int B, int G, int NW>
-static hipError_t launch_prefill_t(const PrefillRec* recs, int n, const AttnArgs& a,
+static hipError_t launch_prefill_t(const PrefillRec* recs, int n, int n_units, const AttnArgs& a,
                                    hipStream_t s) {
   hipLaunchKernelGGL((prefill_kernel<D, B, G, NW, kPrefillRG>), dim3(n), dim3(NW * 64), 0, s, recs,
                      a.q, a.k_cache, a.v_cache, a.bt, a.out, a.part_o, a.part_lse, a.hq, a.hkv,
-                     a.mbr, a.scale_log2);
+                     a.mbr, a.scale_log2, a.decode, n_units);
   return hipGetLastError();
 }
 
 template <int D, int B, int NW>
-static hipError_t launch_prefill_g(int G, const PrefillRec* recs, int n, const AttnArgs& a,
-                                   hipStream_t s) {
+static hipError_t launch_prefill_g(int G, const PrefillRec* recs, int n, int n_units,
+                                   const AttnArgs& a, hipStream_t s) {
   switch (G) {
-    case 1: return launch_prefill_t<D, B, 1, NW>(recs, n, a, s);
-    case 2: return launch_prefill_t<D, B, 2, NW>(recs, n, a, s);
-    case 4: return launch_prefill_t<D, B, 4, NW>(recs, n, a, s);
-    case 8: return launch_prefill_t<D, B, 8, NW>(recs, n, a, s);
+    case 1: return launch_prefill_t<D, B, 1, NW>(recs, n, n_units, a, s);
+    case 2: return launch_prefill_t<D, B, 2, NW>(recs, n, n_units, a, s);
+    case 4: return launch_prefill_t<D, B, 4, NW>(recs, n, n_units, a, s);
+    case 8: return launch_prefill_t<D, B, 8, NW>(recs, n, n_units, a, s);
   }
   return hipErrorInvalidValue;
 }
 
 template <int NW>
-static hipError_t launch_prefill_w(int D, int G, const PrefillRec* recs, int n, const AttnArgs& a,
-                                   hipStream_t s) {
-  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, recs, n, a, s);
-  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, recs, n, a, s);
-  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, recs, n, a, s);
-  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, recs, n, a, s);
+static hipError_t launch_prefill_w(int D, int G, const PrefillRec* recs, int n, int n_units,
+                                   const AttnArgs& a, hipStream_t s) {
+  if (D == 128 && a.block_size == 16) return launch_prefill_g<128, 16, NW>(G, recs, n, n_units, a, s);
+  if (D == 128 && a.block_size == 32) return launch_prefill_g<128, 32, NW>(G, recs, n, n_units, a, s);
+  if (D == 64 && a.block_size == 16) return launch_prefill_g<64, 16, NW>(G, recs, n, n_units, a, s);
+  if (D == 64 && a.block_size == 32) return launch_prefill_g<64, 32, NW>(G, recs, n, n_units, a, s);
   return hipErrorInvalidValue;
 }
 
-// 256-row and 128-row tiles: 32 * kPrefillRG rows per wave; one workgroup per record.
+// 256-row and 128-row tiles: 32 * kPrefillRG rows per wave; one workgroup per
+// record.  The launch the plan names also runs the decode units.
 hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s) {
   constexpr int kWide = kPrefillRowsWide / (32 * kPrefillRG), kNarrow = kPrefillRows / (32 * kPrefillRG);
+  const int units = a.n_decode * a.hkv;
   hipError_t e = hipSuccess;
   if (a.n_prefill_wide_items > 0)
-    e = launch_prefill_w<kWide>(D, G, a.prefill_wide, a.n_prefill_wide_items, a, s);
+    e = launch_prefill_w<kWide>(D, G, a.prefill_wide, a.n_prefill_wide_items,
+                                a.decode_in_prefill == 2 ? units : 0, a, s);
   if (e == hipSuccess && a.n_prefill_items > 0)
-    e = launch_prefill_w<kNarrow>(D, G, a.prefill, a.n_prefill_items, a, s);
+    e = launch_prefill_w<kNarrow>(D, G, a.prefill, a.n_prefill_items,
+                                  a.decode_in_prefill == 1 ? units : 0, a, s);
   return e;
 }
 

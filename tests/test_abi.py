@@ -242,6 +242,28 @@ def test_prefill_tile_width_follows_the_step_key_range():
     assert widest([[0, 0, 2000, 2000], [1, 1200, 8, 1208]]) == 32   # (2000*1000 + 8*1204)/2008
 
 
+def test_fused_steps_use_128_row_tiles_and_fewer_decode_units(monkeypatch):
+    """A step whose decode rows run inside the prefill launch takes 128-row
+    tiles (unless CP_FUSE_NARROW=0) and, when its prefill flops dominate,
+    about one decode unit per CU."""
+    d = _desc(num_blocks=4096, max_blocks_per_req=600, num_reqs_in_table=4)
+    rows = np.array([[0, 8192, 256, 8448], [1, 9000, 1, 9001]], np.int32)
+
+    def widest_and_units():
+        items = cp.plan_items(d, rows)
+        return int(items[items[:, 0] == 0][:, 2].max()), int((items[:, 0] == 1).sum())
+
+    monkeypatch.setenv("CP_NUM_CUS", "256")
+    w, units = widest_and_units()
+    assert w == 32 and units <= 256
+    monkeypatch.setenv("CP_FUSE_NARROW", "0")
+    assert widest_and_units()[0] == 64
+    monkeypatch.delenv("CP_FUSE_NARROW")
+    monkeypatch.setenv("CP_FUSE_DECODE", "0")
+    w, units0 = widest_and_units()
+    assert w == 64 and units0 > units
+
+
 FEW_TOKEN_ROWS = [(0, 2), (5, 3), (100, 2), (4000, 7), (31, 15), (16, 16), (999, 1), (0, 1),
                   (2047, 40), (3, 0)]
 
@@ -289,6 +311,12 @@ def test_attn_run_rejects_lists_past_the_workspace():
     assert run(off_part_lse=big - 8, partial_rows=3) == binding.CP_ERR_INVALID_ARG
     assert run(n_prefill_items=-1) == binding.CP_ERR_INVALID_ARG
     assert run(partial_rows=-1) == binding.CP_ERR_INVALID_ARG
+    # decode items placed inside a prefill launch that the plan does not have
+    assert run(decode_in_prefill=1, n_decode=1, off_decode=0) == binding.CP_ERR_INVALID_ARG
+    assert run(decode_in_prefill=2, n_decode=1, off_decode=0, n_prefill_items=1,
+               off_prefill=256) == binding.CP_ERR_INVALID_ARG
+    assert run(decode_in_prefill=3) == binding.CP_ERR_INVALID_ARG
+    assert run(decode_in_prefill=-1) == binding.CP_ERR_INVALID_ARG
     # empty lists may start at the very end of the workspace (nothing to
     # launch, so this runs on a CPU)
     assert run(off_prefill=big, off_prefill_wide=big, off_decode=big, off_merge=big,
@@ -340,3 +368,74 @@ def test_compute_calls_reject_bad_tables_under_debug_only_after_validation(monke
     fake = 1 << 20
     assert lib.cp_attn_mixed(ctypes.byref(d), fake, fake, fake, fake, bad.ctypes.data, 1, fake,
                              fake, 1 << 30, None) == binding.CP_ERR_BAD_META
+
+
+# ------------------------------------------------- decode blocks in the prefill launch
+
+def _layouts(batch, monkeypatch, mode):
+    # same tile widths and decode split in every mode, so that only the
+    # placement differs
+    monkeypatch.setenv("CP_FUSE_NARROW", "0")
+    monkeypatch.setenv("CP_DECODE_TARGET_ITEMS", "700")
+    monkeypatch.setenv("CP_FUSE_DECODE", str(mode))
+    d = cp.desc_for(batch)
+    return [cp.plan_records(d, batch.rows, w) for w in (0, 1)], cp.plan_items(d, batch.rows)
+
+
+def _fuse_batches():
+    out = [make_config(n) for n in (1, 2, 3)]
+    batches, _ = replay_schedule()
+    out += [batches[i] for i in (1, 4, 9, 15, 19)]
+    rng = np.random.default_rng(12)
+    out.append(make_batch("wide-only", 32, 8, 128, 16,
+                          [(3000, 480), (0, 1), (900, 1), (4000, 1)], rng))
+    out.append(make_batch("g1", 8, 8, 64, 32, [(100, 300), (50, 2), (7, 1), (4000, 1)], rng))
+    return out
+
+
+@pytest.mark.parametrize("mode", [1, 2, 3, 4])
+def test_decode_blocks_in_the_prefill_launch(monkeypatch, mode):
+    """Placing the decode units inside the last prefill launch changes no work
+    item, names every unit exactly once (one per 4-wave workgroup, two per
+    8-wave one), and keeps every tile at its position modulo the XCD count
+    (modes 2 and 3) or at its exact position (mode 1)."""
+    X = 8
+    for b in _fuse_batches():
+        (n0, w0), items0 = _layouts(b, monkeypatch, 0)
+        (n1, w1), items1 = _layouts(b, monkeypatch, mode)
+        key = lambda a: sorted(map(tuple, a.tolist()))
+        assert key(items0) == key(items1), b.name
+        for recs in (n0, w0):
+            assert not (recs[:, 1] < 0).any()
+        n_dec = int((items0[:, 0] == 1).sum())
+        has_pf = len(n0) + len(w0) > 0
+        if n_dec == 0 or not has_pf:
+            assert np.array_equal(n0, n1) and np.array_equal(w0, w1), b.name
+            continue
+        wide = len(n0) == 0
+        fused, plain = (w1, w0) if wide else (n1, n0)
+        other0, other1 = (n0, n1) if wide else (w0, w1)
+        assert np.array_equal(other0, other1)
+        marks = fused[fused[:, 1] == -1]
+        per = 2 if wide else 1
+        units = marks[:, 0].tolist() + [u for u in marks[:, 2].tolist() if u >= 0]
+        assert sorted(units) == list(range(n_dec)), b.name
+        if not wide:
+            assert (marks[:, 2] == -1).all()
+        assert len(marks) == -(-n_dec // per)
+        tiles1 = [(i % X, tuple(r)) for i, r in enumerate(fused.tolist()) if r[1] > 0]
+        tiles0 = [(i % X, tuple(r)) for i, r in enumerate(plain.tolist()) if r[1] > 0]
+        assert [t for _, t in tiles1] == [t for _, t in tiles0], b.name
+        if mode == 1:
+            assert np.array_equal(fused[: len(plain)], plain)
+            assert (fused[len(plain):, 1] == -1).all()
+        else:
+            assert tiles1 == tiles0, b.name
+        if mode == 2:
+            first_tile = min(i for i, r in enumerate(fused.tolist()) if r[1] > 0)
+            assert (fused[:first_tile, 1] <= 0).all() and first_tile >= len(marks)
+        if mode == 3 and len(marks) >= 2 * X and len(tiles0) >= 4 * X:
+            # spread: decode blocks in both halves of the list
+            pos = np.flatnonzero(fused[:, 1] == -1)
+            assert pos.min() < len(fused) // 2 < pos.max()
+        assert len(fused) == 0 or fused[-1, 1] != 0   # no trailing idle records

@@ -49,6 +49,7 @@ def test_geometry_grid(monkeypatch, geom, tiles):
     128 rows runs on the 256-row tiles whatever the step's key range."""
     if tiles == "wide":
         monkeypatch.setenv("CP_PREFILL_WIDE_MIN_KEYS", "0")
+        monkeypatch.setenv("CP_FUSE_NARROW", "0")   # wide tiles beside the decode rows too
     hq, hkv, d, b = geom
     rng = np.random.default_rng(hash(geom) % (2 ** 31))
     # a multi-tile chunk with a ragged tail, a chunk over deep context, a
@@ -169,3 +170,52 @@ def test_debug_mode_rejects_out_of_range_block_ids(monkeypatch):
                   batch.rows, out, ws)
     torch.cuda.synchronize()
     assert_close(out, oracle.attn(batch, tens["q"].cpu(), kc_ref, vc_ref), "CP_DEBUG run")
+
+
+FUSE_GEOMS = [(8, 1, 128, 16), (32, 8, 128, 16), (64, 8, 128, 32), (16, 4, 64, 32), (8, 8, 64, 16)]
+
+
+@pytest.mark.parametrize("width", ["narrow", "wide"])
+@pytest.mark.parametrize("geom", FUSE_GEOMS, ids=lambda g: "hq%d_hkv%d_d%d_b%d" % g)
+def test_decode_inside_the_prefill_launch(monkeypatch, geom, width):
+    """Decode rows run as decode blocks of the prefill launch (CP_FUSE_DECODE
+    1, 2, 3, 4: after, before, spread among or merged longest first with the
+    tiles; 4-wave workgroups with one unit,
+    8-wave ones with two, an odd unit count leaving one group idle) or in
+    their own launch (0): every mode matches the oracle element by element and
+    gives the same output bits as the others (the decode split is pinned: a
+    fused prefill-heavy step otherwise takes fewer, longer decode units)."""
+    monkeypatch.setenv("CP_DECODE_TARGET_ITEMS", "300")
+    hq, hkv, d, b = geom
+    G = hq // hkv
+    if width == "wide":
+        monkeypatch.setenv("CP_PREFILL_WIDE_MIN_KEYS", "0")
+        monkeypatch.setenv("CP_FUSE_NARROW", "0")
+        chunk = max(160 // G + 1, 129)       # every chunk above 128 rows
+        rows = [(3000, chunk), (0, 2 * chunk)]
+    else:
+        monkeypatch.setenv("CP_PREFILL_WIDE_MIN_ROWS", "100000")
+        rows = [(3000, 60), (0, 150), (40, 2)]
+    rows += [(b - 1, 1), (2 * b, 1), (0, 1), (6000, 1), (1000, 1)]
+    rng = np.random.default_rng(hq * 100 + d + b)
+    batch = make_batch("fuse-" + width, hq, hkv, d, b, rows, rng)
+    tens = make_tensors(batch, seed=4000 + hq + d)
+    kc_ref, vc_ref = oracle.kv_append(batch, tens["k_new"], tens["v_new"], tens["k_cache"],
+                                      tens["v_cache"])
+    ref = oracle.attn(batch, tens["q"], kc_ref, vc_ref)
+    outs = {}
+    for mode in (0, 1, 2, 3, 4):
+        monkeypatch.setenv("CP_FUSE_DECODE", str(mode))
+        import paper_2606_09061_amd as cp
+        recs = cp.plan_records(cp.desc_for(batch), batch.rows, 1 if width == "wide" else 0)
+        n_blocks = int((recs[:, 1] == -1).sum())
+        assert (n_blocks > 0) == (mode > 0)
+        say(f"[gpu] decode in prefill launch {width} {geom} mode {mode}: {n_blocks} decode blocks")
+        t = to_dev(tens)
+        out = run_step(batch, t)
+        torch.cuda.synchronize()
+        assert np.array_equal(words(t["k_cache"]).reshape(-1), kc_ref.reshape(-1))
+        assert_close(out, ref, f"fuse {width} {geom} mode {mode}")
+        outs[mode] = words(out)
+    for mode in (1, 2, 3, 4):
+        assert np.array_equal(outs[mode], outs[0]), f"mode {mode} differs from its own launch"

@@ -43,10 +43,12 @@ GEOMS = [(8, 8, 64, 16), (32, 8, 128, 16), (16, 4, 64, 32), (64, 8, 128, 32), (8
 MODES = {
     "prefill-narrow-unsplit": {"CP_PREFILL_WIDE_MIN_ROWS": "100000",
                                "CP_PREFILL_MIN_SPLIT": "100000"},
-    "prefill-wide-unsplit": {"CP_PREFILL_WIDE_MIN_KEYS": "0", "CP_PREFILL_MIN_SPLIT": "100000"},
+    "prefill-wide-unsplit": {"CP_PREFILL_WIDE_MIN_KEYS": "0", "CP_PREFILL_MIN_SPLIT": "100000",
+                             "CP_FUSE_NARROW": "0"},
     "prefill-narrow-split": {"CP_PREFILL_WIDE_MIN_ROWS": "100000", "CP_PREFILL_MIN_SPLIT": "2",
                              "CP_PREFILL_TARGET_ITEMS": "100000"},
     "prefill-wide-split": {"CP_PREFILL_WIDE_MIN_KEYS": "0", "CP_PREFILL_MIN_SPLIT": "2",
+                           "CP_FUSE_NARROW": "0",
                            "CP_PREFILL_TARGET_ITEMS": "100000"},
     "decode-unsplit": {"CP_DECODE_TARGET_ITEMS": "1", "CP_PREFILL_MIN_LEN": "8"},
     "decode-split": {"CP_DECODE_TARGET_ITEMS": "100000", "CP_PREFILL_MIN_LEN": "8"},
