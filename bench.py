@@ -76,7 +76,17 @@ def work_of(batch):
             w["decode_flops"] += fl
             w["decode_bytes"] += byt
     w["append_bytes"] = 8 * Hkv * D * batch.num_tokens
+    # decode rows whose work the planner placed inside the prefill launch
+    w["fused_decode_bytes"] = w["decode_bytes"] if decode_fused(batch) else 0
     return w
+
+
+def decode_fused(batch):
+    """Whether the step runs its decode rows as decode blocks of its prefill
+    launch (the plan's record lists name decode blocks)."""
+    import paper_2606_09061_amd as cp
+    d = cp.desc_for(batch)
+    return any((cp.plan_records(d, batch.rows, w)[:, 1] == -1).any() for w in (0, 1))
 
 
 def kernel_sha(name):
@@ -301,12 +311,25 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
     dominant = max(("prefill", "decode"), key=lambda k: prof[k][0])
     wl_name = CONFIG_NAMES_SHORT[cfg]
     if dominant == "prefill":
-        avg_ms = prof["prefill"][0] / max(1, prof["prefill"][1])
-        per_launch = tot["prefill_flops"] / max(1, prof["prefill"][1])
+        n_launch = max(1, prof["prefill"][1])
+        avg_ms = prof["prefill"][0] / n_launch
+        per_launch = tot["prefill_flops"] / n_launch
         achieved = per_launch / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "kernel": "prefill", "achieved": achieved,
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                 "avg_launch_ms": avg_ms, "work_per_launch": per_launch}
+        if tot["fused_decode_bytes"]:
+            # the launch also streams the decode rows' K/V: `frac` charges its
+            # whole duration to the prefill flops; `fused_frac` is the time the
+            # slower of the two rooflines needs for both (flops at the MFMA
+            # peak, decode bytes at the HBM peak, perfectly overlapped) over
+            # the launch's duration, `fused_frac_serial` their sum over it
+            dec = tot["fused_decode_bytes"] / n_launch
+            t_m = per_launch / (PEAK_BF16_TFLOPS * 1e12)
+            t_h = dec / (PEAK_HBM_GBS * 1e9)
+            roof["fused_decode_bytes_per_launch"] = dec
+            roof["fused_frac"] = max(t_m, t_h) / (avg_ms * 1e-3)
+            roof["fused_frac_serial"] = (t_m + t_h) / (avg_ms * 1e-3)
     else:
         avg_ms = prof["decode"][0] / max(1, prof["decode"][1])
         per_launch = tot["decode_bytes"] / max(1, prof["decode"][1])
