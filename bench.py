@@ -319,16 +319,24 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                 "avg_launch_ms": avg_ms, "work_per_launch": per_launch}
         if tot["fused_decode_bytes"]:
-            # the launch also streams the decode rows' K/V: `frac` charges its
-            # whole duration to the prefill flops; `fused_frac` is the time the
-            # slower of the two rooflines needs for both (flops at the MFMA
-            # peak, decode bytes at the HBM peak, perfectly overlapped) over
-            # the launch's duration, `fused_frac_serial` their sum over it
-            dec = tot["fused_decode_bytes"] / n_launch
+            # The launch also runs the decode rows.  Its roofline time is the
+            # larger of its flops at the MFMA peak and its algorithmic bytes
+            # (the prefill rows' and the fused decode rows' K/V, q and out) at
+            # the HBM peak; the bound is the one that needs longer, and
+            # `frac` is that time over the launch's duration.
+            # `prefill_flops_frac` charges the whole launch to the flops;
+            # `fused_frac_serial` is both times summed over the duration.
+            byt = (tot["prefill_bytes"] + tot["fused_decode_bytes"]) / n_launch
             t_m = per_launch / (PEAK_BF16_TFLOPS * 1e12)
-            t_h = dec / (PEAK_HBM_GBS * 1e9)
-            roof["fused_decode_bytes_per_launch"] = dec
-            roof["fused_frac"] = max(t_m, t_h) / (avg_ms * 1e-3)
+            t_h = byt / (PEAK_HBM_GBS * 1e9)
+            if t_h > t_m:
+                a = byt / (avg_ms * 1e-3) / 1e9
+                roof.update({"bound": "hbm", "achieved": a, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                             "frac": a / PEAK_HBM_GBS, "work_per_launch": byt})
+            roof["kernel"] = "prefill (with the step's decode rows)"
+            roof["prefill_flops_per_launch"] = per_launch
+            roof["prefill_flops_frac"] = achieved / PEAK_BF16_TFLOPS
+            roof["fused_bytes_per_launch"] = byt
             roof["fused_frac_serial"] = (t_m + t_h) / (avg_ms * 1e-3)
     else:
         avg_ms = prof["decode"][0] / max(1, prof["decode"][1])
@@ -337,7 +345,7 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
         roof = {"bound": "hbm", "kernel": "decode", "achieved": achieved, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "avg_launch_ms": avg_ms,
                 "work_per_launch": per_launch}
-    roof["traffic"] = traffic_for(roof["kernel"], wl_name)
+    roof["traffic"] = traffic_for(roof["kernel"].split()[0], wl_name)
     # the other kernel's fraction, for mixes where both matter
     other = {}
     # the step against the roofline: t_pf = prefill flops at the MFMA peak,
@@ -983,7 +991,9 @@ def per_iteration(cfg, reps=7):
     """Prefill and decode kernel time of every batch of mix ``cfg`` (the 20
     iterations of the replay for mix 5), measured one batch at a time with the
     library's per-kernel events after the batches have run once in order,
-    with each batch's algorithmic work and the fractions of the peaks."""
+    with each batch's algorithmic work and the fractions of the peaks.  When
+    a batch's decode rows run inside its prefill launch, "prefill_us" is that
+    launch and "decode_us" is 0."""
     import numpy as np
     import torch
     import paper_2606_09061_amd as cp
@@ -1026,16 +1036,24 @@ def per_iteration(cfg, reps=7):
         pf = b.rows[b.rows[:, 2] >= 2]
         t_pf = float(np.median(times[j]["prefill"][1:]))
         t_dc = float(np.median(times[j]["decode"][1:]))
+        t_attn = t_pf + t_dc
+        # roofline time of the attention launches: flops at the MFMA peak or
+        # bytes at the HBM peak, whichever is longer
+        t_roof = max(w["prefill_flops"] / (PEAK_BF16_TFLOPS * 1e12),
+                     (w["prefill_bytes"] + w["decode_bytes"]) / (PEAK_HBM_GBS * 1e9))
         out.append({"iteration": j, "prefill_chunks": int(len(pf)),
                     "prefill_tokens": int(pf[:, 2].sum()),
                     "max_prior": int(pf[:, 1].max()) if len(pf) else 0,
                     "decode_rows": int((b.rows[:, 2] == 1).sum()),
+                    "decode_fused": bool(w["fused_decode_bytes"]),
                     "prefill_gflop": w["prefill_flops"] / 1e9, "prefill_us": t_pf,
                     "prefill_frac_mfma": (w["prefill_flops"] / (t_pf * 1e-6) / (PEAK_BF16_TFLOPS * 1e12)
                                           if t_pf > 0 else None),
                     "decode_mb": w["decode_bytes"] / 1e6, "decode_us": t_dc,
                     "decode_frac_hbm": (w["decode_bytes"] / (t_dc * 1e-6) / (PEAK_HBM_GBS * 1e9)
-                                        if t_dc > 0 else None)})
+                                        if t_dc > 0 else None),
+                    "attention_us": t_attn,
+                    "roofline_frac": t_roof / (t_attn * 1e-6) if t_attn > 0 else None})
     return {"mix": cfg, "reps": reps, "iterations": out}
 
 
