@@ -1061,6 +1061,57 @@ FEW_TOKEN_LENS = (2, 3, 4, 8, 16)
 FEW_TOKEN_PRIORS = (0, 1024, 4096)
 
 
+GEMM_SHAPES = {"qkv": (6144, 4096), "o": (4096, 4096), "gate_up": (24576, 4096),
+               "down": (4096, 12288)}
+GEMM_ROWS = (33, 64, 128, 256, 512, 1024, 2048, 4096)
+
+
+def gemm_table(reps=20):
+    """The layer's projections (Qwen3-8B: hidden 4096, 32/8 heads, FFN 12288)
+    on the package's tiled MFMA kernel (cpl_gemm) and on the platform BLAS
+    (torch.mm -> hipBLASLt), per batch size: mean time per call over `reps`
+    calls after warm-up (HIP events), and TFLOP/s.  Inputs N(0,1) bf16,
+    weights N(0, 0.02)."""
+    import torch
+    from paper_2606_09061_amd import model as MM
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    g = torch.Generator(device=dev).manual_seed(7)
+    out = []
+    only = os.environ.get("GEMM_PROJ")
+    for name, (N, K) in GEMM_SHAPES.items():
+        if only and name not in only.split(","):
+            continue
+        w = (torch.randn(N, K, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+        for M in GEMM_ROWS:
+            a = torch.randn(M, K, generator=g, device=dev).to(torch.bfloat16)
+            c1 = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+            c2 = torch.empty_like(c1)
+            ws = torch.empty(max(16, MM.gemm_workspace_bytes(M, N, K)), dtype=torch.uint8,
+                             device=dev)
+            row = {"proj": name, "M": M, "N": N, "K": K}
+            for lab, fn in (("own", lambda: MM.gemm(a, w, c1, ws=ws)),
+                            ("blas", lambda: torch.mm(a, w.t(), out=c2))):
+                for _ in range(3):
+                    fn()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                e0.record()
+                for _ in range(reps):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                us = e0.elapsed_time(e1) * 1e3 / reps
+                row[f"{lab}_us"] = us
+                row[f"{lab}_tflops"] = 2.0 * M * N * K / (us * 1e-6) / 1e12
+            d = (c1.float() - c2.float()).abs().max().item()
+            row["max_abs_diff"] = d
+            log(f"[gemm] {name} M={M}: own {row['own_us']:.1f} us, blas {row['blas_us']:.1f} us")
+            out.append(row)
+    return {"peak_tflops": PEAK_BF16_TFLOPS, "rows": out}
+
+
 def few_token_routing(n_chunks=64, reps=20):
     """Attention time of batches of n_chunks c-token chunks (one per request,
     prior context P), routed either to the MFMA tile kernel or to the decode
@@ -1164,6 +1215,8 @@ def main():
     ap.add_argument("--per-iteration", action="store_true",
                     help="prefill / decode kernel time of every batch of --config (mix 5: its "
                          "20 iterations) against its algorithmic work")
+    ap.add_argument("--gemm", action="store_true",
+                    help="the layer's projections on cpl_gemm and on the platform BLAS")
     ap.add_argument("--few-token", action="store_true",
                     help="only time few-token chunks on the tile kernel against the decode "
                          "kernel token by token")
@@ -1188,6 +1241,9 @@ def main():
         return
     if args.few_token:
         print(json.dumps(few_token_routing()), flush=True)
+        return
+    if args.gemm:
+        print(json.dumps(gemm_table()), flush=True)
         return
     if args.per_iteration:
         print(json.dumps(per_iteration(args.config)), flush=True)

@@ -10,8 +10,8 @@
  *        cp_attn_mixed -> O projection (+ x) -> RMSNorm -> gate/up
  *        projection -> cpl_swiglu -> down projection (+ residual)
  *
- * The projections are plain GEMMs: the platform BLAS runs them, except for
- * decode-sized batches, where cpl_gemm_skinny streams the weights itself.  The paper does not describe the model; the layer
+ * The projections are plain GEMMs: cpl_gemm (LDS-tiled MFMA) and, for
+ * decode-sized batches, cpl_gemm_skinny, which streams the weights itself.  The paper does not describe the model; the layer
  * follows the published Qwen3 architecture (RMSNorm, per-head RMSNorm on
  * queries and keys before rotary embedding, SwiGLU feed-forward).
  *
@@ -27,6 +27,7 @@
 #ifndef CP_LAYER_H
 #define CP_LAYER_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #include "cp_attn.h"
@@ -57,6 +58,27 @@ int cpl_qkv_rope(const void* qkv, const void* q_norm_w, const void* k_norm_w,
 /* SwiGLU: out[t][i] = silu(gu[t][i]) * gu[t][inter + i], silu(g) = g / (1 + e^-g);
  * gu [T][2*inter], out [T][inter]; inter % 8 == 0. */
 int cpl_swiglu(const void* gu, void* out, int32_t n_tokens, int32_t inter, void* stream);
+
+/* Projection: c[M][N] = a[M][K] . w[N][K]^T (+ r[M][N]), bf16 in and out, fp32
+ * accumulation on the matrix cores (v_mfma_f32_32x32x16_bf16), for batches of
+ * any size (the layer runs its QKV and output projections on it above the
+ * skinny kernel's batch sizes).  M >= 1, N % 128 == 0, K % 32 == 0; a, w, c,
+ * r and ws 16-byte aligned; r may be NULL or equal to c (in-place residual
+ * add); a and w must not alias c.  Output tiles of 64-256 x 128-256 with K
+ * staged through LDS; when the tiles alone would leave CUs idle, K is split
+ * into slices whose fp32 partial tiles go to ws (the caller's device
+ * memory, at least cpl_gemm_workspace_bytes(m, n, k) bytes to split fully;
+ * with less, or ws NULL, the split shrinks or is skipped: same definition,
+ * fewer workgroups).  The environment variables CPL_GEMM_CFG (tile
+ * configuration 0-7: 64x128, 128x128, 128x256, 256x128 with 32 k per stage,
+ * 64x128, 128x128 with 64, 256x256 with 32 and 64) and CPL_GEMM_SPLIT
+ * (slices) override the choice. */
+int cpl_gemm(const void* a, const void* w, const void* r, void* c, int32_t m, int32_t n,
+             int32_t k, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes cpl_gemm uses for this shape (0: no split), or 0 if the
+ * shape is unsupported. */
+size_t cpl_gemm_workspace_bytes(int32_t m, int32_t n, int32_t k);
 
 /* Projection of a small batch: c[M][N] = a[M][K] . w[N][K]^T (+ r[M][N]), bf16 in and
  * out, fp32 accumulation, for the decode-sized batches where a library GEMM

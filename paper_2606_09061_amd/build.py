@@ -17,7 +17,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcpattn.so")
 SCHED_LIB = os.path.join(PKG, "libcpsched.so")
 LAYER_LIB = os.path.join(PKG, "libcplayer.so")
-LAYER_SOURCES = ["layer.hip"]
+LAYER_SOURCES = ["layer.hip", "gemm.hip"]
 PEAKS_LIB = os.path.join(PKG, "libcppeaks.so")
 PEAKS_SOURCES = ["peaks.hip"]
 CXX = os.environ.get("CXX", "g++")

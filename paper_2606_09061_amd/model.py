@@ -50,14 +50,18 @@ def load():
     lib.cpl_qkv_rope.argtypes = [P, P, P, P, I32, I32, I32, I32, D, F, P, P, P, P]
     lib.cpl_swiglu.argtypes = [P, P, I32, I32, P]
     lib.cpl_gemm_skinny.argtypes = [P, P, P, P, I32, I32, I32, P]
-    for f in (lib.cpl_rmsnorm, lib.cpl_qkv_rope, lib.cpl_swiglu, lib.cpl_gemm_skinny):
+    lib.cpl_gemm.argtypes = [P, P, P, P, I32, I32, I32, P, ctypes.c_size_t, P]
+    lib.cpl_gemm_workspace_bytes.argtypes = [I32, I32, I32]
+    lib.cpl_gemm_workspace_bytes.restype = ctypes.c_size_t
+    for f in (lib.cpl_rmsnorm, lib.cpl_qkv_rope, lib.cpl_swiglu, lib.cpl_gemm_skinny, lib.cpl_gemm):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
 
 
 def exported_symbols():
-    return ["cpl_rmsnorm", "cpl_qkv_rope", "cpl_swiglu", "cpl_gemm_skinny"]
+    return ["cpl_rmsnorm", "cpl_qkv_rope", "cpl_swiglu", "cpl_gemm_skinny", "cpl_gemm",
+            "cpl_gemm_workspace_bytes"]
 
 
 def _check(rc, what):
@@ -127,9 +131,48 @@ def gemm_skinny(a, w, out, residual=None, stream=None):
                                   out.data_ptr(), M, N, K, _s(stream)), "cpl_gemm_skinny")
 
 
+def gemm_workspace_bytes(m, n, k):
+    """Device bytes cpl_gemm uses to split K for this shape (0: no split)."""
+    return int(load().cpl_gemm_workspace_bytes(m, n, k))
+
+
+def gemm(a, w, out, residual=None, stream=None, ws=None):
+    """out [M, N] = a [M, K] @ w [N, K]^T (+ residual, which may be out itself),
+    on the package's LDS-tiled MFMA kernel (cpl_gemm).  ``ws``: a uint8 device
+    tensor for the split over K (allocated here when None and needed)."""
+    import torch
+    _dense(a, w, out)
+    if residual is not None:
+        _dense(residual)
+    M, K = a.shape
+    N = w.shape[0]
+    need = gemm_workspace_bytes(M, N, K)
+    if ws is None and need:
+        ws = torch.empty(need, dtype=torch.uint8, device=a.device)
+    _check(load().cpl_gemm(a.data_ptr(), w.data_ptr(),
+                           residual.data_ptr() if residual is not None else None,
+                           out.data_ptr(), M, N, K, ws.data_ptr() if ws is not None else None,
+                           ws.numel() if ws is not None else 0, _s(stream)), "cpl_gemm")
+
+
+def project_attn(a, w, out, residual=None, stream=None, ws=None):
+    """The QKV and output projections around the attention step, always on
+    the package's kernels: the skinny kernel up to 32 rows, the tiled MFMA
+    GEMM above (``ws``: its split-K workspace, see gemm)."""
+    M, K = a.shape
+    N = w.shape[0]
+    if skinny_faster(M, N, K):
+        gemm_skinny(a, w, out, residual, stream)
+    elif N % 128 == 0 and K % 32 == 0:
+        gemm(a, w, out, residual, stream, ws)
+    else:
+        raise ValueError(f"projection {M}x{N}x{K}: the kernels need N % 128 == 0 and K % 32 == 0")
+
+
 def project(a, w, out, residual=None, stream=None):
     """a @ w^T into out (+ residual): the skinny kernel where it is faster
-    (small batches, moderate projections), the platform BLAS otherwise."""
+    (small batches, moderate projections), the platform BLAS otherwise.
+    The feed-forward and LM-head projections use it."""
     import torch
     M, K = a.shape
     N = w.shape[0]
@@ -235,6 +278,8 @@ class Model:
         self.pos = torch.zeros(T, dtype=torch.int32, device=self.dev)
         self.tokens = torch.randint(0, c.vocab, (T,), generator=gen, device=self.dev)
         self.ws = torch.empty(64 << 20, dtype=torch.uint8, device=self.dev)      # attention plan
+        # split-K partials of the QKV / output projections (grown on demand)
+        self.ws_gemm = torch.empty(256, dtype=torch.uint8, device=self.dev)
         # an append item covers one row's tokens inside one block: at most
         # max_tokens + max_seqs items of 16 bytes, so the append never needs more
         self.ws_append = torch.empty(16 * (max_tokens + max_seqs) + 256, dtype=torch.uint8,
@@ -274,14 +319,18 @@ class Model:
                 self.ws = torch.empty(cp.workspace_bytes(self.desc, rows), dtype=torch.uint8,
                                       device=self.dev)
                 plan = cp.attn_prepare(self.desc, rows, self.ws, stream=s)
+            need = max(gemm_workspace_bytes(T, qkv.shape[1], c.hidden),
+                       gemm_workspace_bytes(T, c.hidden, c.hq * c.head_dim)) if T > 32 else 0
+            if need > self.ws_gemm.numel():
+                self.ws_gemm = torch.empty(need, dtype=torch.uint8, device=self.dev)
             for L, kc, vc in zip(self.layers, self.kc, self.vc):
                 rmsnorm(x, L["in_norm"], h, c.eps, s)
-                project(h, L["qkv"], qkv, None, s)
+                project_attn(h, L["qkv"], qkv, None, s, self.ws_gemm)
                 qkv_rope(qkv, L["q_norm"], L["k_norm"], self.pos, c.hq, c.hkv, c.head_dim,
                          c.theta, c.eps, q, k, v, s)
                 cp.kv_append(self.desc, k, v, kc, vc, self.bt, rows, self.ws_append, stream=s)
                 cp.attn_run(plan, q, kc, vc, self.bt, attn, self.ws, stream=s)
-                project(attn.view(T, c.hq * c.head_dim), L["o"], x, x, s)
+                project_attn(attn.view(T, c.hq * c.head_dim), L["o"], x, x, s, self.ws_gemm)
                 rmsnorm(x, L["post_norm"], h, c.eps, s)
                 project(h, L["gate_up"], gu, None, s)
                 swiglu(gu, act, s)

@@ -226,3 +226,51 @@ def test_gemm_skinny_rejects_unsupported_shapes():
     assert lib.cpl_gemm_skinny(p, p, None, p + 1024, 8, 48, 256, None) != 0     # N % 32
     assert lib.cpl_gemm_skinny(p, p, None, p + 1024, 8, 32, 320, None) != 0    # K % 256
     assert lib.cpl_gemm_skinny(p, p, None, p, 8, 32, 256, None) != 0           # a aliases c
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 128, 32), (33, 256, 64), (64, 384, 4096), (65, 128, 96),
+                                   (130, 6144, 4096), (257, 4096, 4096), (1000, 512, 1024),
+                                   (128, 1024, 1024), (4096, 256, 128), (200, 24576, 64)])
+@pytest.mark.parametrize("residual", ["none", "separate", "in_place"])
+@pytest.mark.parametrize("split", ["auto", "none"])
+def test_gemm_matches_reference(monkeypatch, M, N, K, residual, split):
+    """cpl_gemm against the fp64 product of the same bf16 inputs: ragged row
+    counts (tiles past M), one and many K stages, the layer's QKV (N 6144) and
+    output (N 4096) shapes, residual read from another tensor or from the
+    output itself; K split into slices summed by a second kernel (auto) or
+    not split."""
+    print(f"gemm M={M} N={N} K={K} residual={residual} split={split}", flush=True)
+    if split == "none":
+        monkeypatch.setenv("CPL_GEMM_SPLIT", "1")
+    from paper_2606_09061_amd import model as MM
+    a = _bf16((M, K), 41)
+    w = _bf16((N, K), 42, 0.05)
+    r = _bf16((M, N), 43) if residual != "none" else None
+    ad, wd = a.to(DEV), w.to(DEV)
+    if residual == "in_place":
+        out = r.clone().to(DEV)
+        MM.gemm(ad, wd, out, out)
+    else:
+        out = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device=DEV)
+        MM.gemm(ad, wd, out, r.to(DEV) if r is not None else None)
+    torch.cuda.synchronize()
+    want = _f64(a) @ _f64(w).T + (_f64(r) if r is not None else 0.0)
+    slack = 2.0 ** -20 * (np.abs(_f64(a)) @ np.abs(_f64(w)).T)
+    got = _f64(out)
+    assert np.isfinite(got).all()
+    err = np.abs(got - want)
+    assert np.all(err <= 2.0 ** -8 * np.abs(want) + slack + 1e-6), f"max err {err.max():.3e}"
+
+
+def test_gemm_rejects_unsupported_shapes():
+    lib = M.load()
+    x = torch.zeros(512, 512, dtype=torch.bfloat16, device=DEV)
+    p = x.data_ptr()
+    c = p + 256 * 512 * 2
+    assert lib.cpl_gemm(p, p, None, c, 0, 128, 32, None, 0, None) != 0        # M = 0
+    assert lib.cpl_gemm(p, p, None, c, 8, 96, 32, None, 0, None) != 0         # N % 128
+    assert lib.cpl_gemm(p, p, None, c, 8, 128, 48, None, 0, None) != 0        # K % 32
+    assert lib.cpl_gemm(p, p, None, p, 8, 128, 32, None, 0, None) != 0        # a aliases c
+    assert lib.cpl_gemm(p + 8, p, None, c, 8, 128, 32, None, 0, None) != 0    # misaligned a
+    assert lib.cpl_gemm(p, p, None, c, 8, 128, 32, None, 0, None) == 0
+    torch.cuda.synchronize()

@@ -131,3 +131,27 @@ def test_skinny_dispatch_follows_measured_table():
         assert not skinny_faster(33, n, k) and not skinny_faster(128, n, k)
     assert skinny_faster(32, *qkv) and skinny_faster(32, *gate_up) and skinny_faster(32, *down)
     assert not skinny_faster(1, 1000, 256) and not skinny_faster(1, 64, 320)   # unsupported shapes
+
+
+def test_gemm_validates_before_launching():
+    """cpl_gemm refuses unsupported shapes, aliasing and misalignment on the
+    host, before touching the device (so this runs without a GPU)."""
+    from paper_2606_09061_amd import model as M
+    lib = M.load()
+    a, w, c = 1 << 20, 2 << 20, 3 << 20      # aligned stand-in addresses, never dereferenced
+
+    def bad(a_, w_, r_, c_, m, n, k, ws=None):
+        return lib.cpl_gemm(a_, w_, r_, c_, m, n, k, ws, 1 << 20, None)
+    assert bad(a, w, None, c, 0, 128, 32) != 0       # M = 0
+    assert bad(a, w, None, c, 8, 96, 32) != 0        # N % 128
+    assert bad(a, w, None, c, 8, 128, 48) != 0       # K % 32
+    assert bad(a, w, None, a, 8, 128, 32) != 0       # a aliases c
+    assert bad(a, w, None, w, 8, 128, 32) != 0       # w aliases c
+    assert bad(a + 8, w, None, c, 8, 128, 32) != 0   # misaligned a
+    assert bad(a, w, c + 4, c, 8, 128, 32) != 0      # misaligned residual
+    assert bad(a, w, None, c, 8, 128, 32, ws=c + 8) != 0   # misaligned workspace
+    assert bad(None, w, None, c, 8, 128, 32) != 0    # null
+    # the workspace a full split needs: none for a grid that fills the GPU
+    assert lib.cpl_gemm_workspace_bytes(4096, 6144, 4096) == 0
+    assert lib.cpl_gemm_workspace_bytes(64, 4096, 4096) > 0
+    assert lib.cpl_gemm_workspace_bytes(8, 96, 32) == 0
