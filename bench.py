@@ -294,6 +294,17 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
     # headline region: only the two bracketing events
     total_ms, wall, _, _ = timed(steps_n, "total")
     issue = timed.issue_s
+    # host cost of a step when nothing throttles the host: groups of 6 steps
+    # issued onto an idle stream (the library stages up to 8 plans ahead, so
+    # none of these waits for the GPU)
+    free = []
+    for i in range(0, min(steps_n, 60), 6):
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for k in range(6):
+            step(i + k)
+        free.append((time.perf_counter() - w0) / 6)
+    torch.cuda.synchronize()
     # per-step latencies (at least 100 steps), then per-kernel durations
     n_lat = max(steps_n, 100)
     _, _, per_step, _ = timed(n_lat, "steps")
@@ -389,6 +400,7 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
                        "p90": float(np.percentile(per_step, 90)), "reps": n_lat},
         "wall_ms_per_step": wall * 1e3 / steps_n,
         "host_issue_ms_per_step": issue * 1e3 / steps_n,
+        "host_ms_per_step_unthrottled": float(np.median(free)) * 1e3,
         "kernels": kern,
         "roofline": roof,
         "roofline_step": roof_step,

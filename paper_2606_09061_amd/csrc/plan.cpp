@@ -312,6 +312,14 @@ static int64_t choose_split_steps(const cp_attn_desc& d, const Tuning& t,
     max_steps = std::max<int64_t>(max_steps, ceil_div(tl.kv_end, kPrefillKeys));
     has[tl.wide ? 1 : 0] = true;
   }
+  // decode units that join the last prefill launch (sc.dec_groups, in tile
+  // steps): they fill its slots too, so they weigh in the estimate
+  const int wdec = has[0] ? 0 : 1;
+  int64_t dec_total = 0, dec_longest = 0;
+  for (const auto& g : sc.dec_groups) {
+    dec_total += g.first * g.second;
+    dec_longest = std::max(dec_longest, g.first);
+  }
   const int64_t min_split = std::max(1, t.prefill_min_split);
   if (t.prefill_target_items > 0) {
     int64_t cost = 0;
@@ -368,6 +376,8 @@ static int64_t choose_split_steps(const cp_attn_desc& d, const Tuning& t,
       if (cuts > 0) partial_rows += Hkv * (1 + cuts) * tl.n_tok * G;
     }
     const double merge = (double)partial_rows * (d.head_dim + 1) * 8 / merge_bytes_per_step;
+    total[wdec] += dec_total;
+    longest[wdec] = std::max(longest[wdec], dec_longest);
     for (int w = 0; w < 2; ++w) {
       if (!has[w]) continue;
       const int64_t slots = (int64_t)t.num_cus * (w ? 1 : 2);
@@ -385,6 +395,7 @@ static int64_t choose_split_steps(const cp_attn_desc& d, const Tuning& t,
         groups.push_back({ceil_div(tl.kv_end - cuts * split_keys, kPrefillKeys) + kItemOverhead, Hkv});
       }
       if (full[w] > 0) groups.push_back({S + kItemOverhead, full[w] * Hkv});
+      if (w == wdec) groups.insert(groups.end(), sc.dec_groups.begin(), sc.dec_groups.end());
       const int64_t slots = (int64_t)t.num_cus * (w ? 1 : 2);
       est += (double)lpt_makespan(groups, slots, sc.load_hist);
     }
@@ -463,6 +474,64 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     }
     chunks.push_back(ch);
   }
+  // ---- decode sizing ----------------------------------------------------
+  // Rows shorter than prefill_min_len run on the split-K decode kernel, one
+  // item list per query token: token j of a row sits at position
+  // chunk_start + j and sees keys [0, chunk_start + j + 1), so each token is
+  // its own "decode row" with its own causal limit (a one-token row is the
+  // usual case; few-token chunks read their request's K/V once per token).
+  auto each_decode_token = [&](auto&& f) {
+    for (int32_t r = 0; r < n_rows; ++r) {
+      const cp_row_meta& m = rows[r];
+      if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
+      for (int32_t j = 0; j < m.chunk_len; ++j)
+        f(m, (int32_t)(off[r] + j), m.chunk_start + j + 1);
+    }
+  };
+  sc.dec_groups.clear();
+  int64_t dec_blocks = 0;
+  each_decode_token([&](const cp_row_meta&, int32_t, int32_t kv_end) {
+    dec_blocks += ceil_div(kv_end, B) * Hkv;
+  });
+  if (dec_blocks > 0) {
+    // Items per CU grow with the decode bytes: ~3 per CU (the kernel keeps
+    // three workgroups resident) for small loads, where every extra item costs
+    // plan upload, partial rows for the merge and a workgroup's start-up,
+    // rising to 6 per CU at 4 GB and above, where finer items balance the
+    // tail better (measured on the 0.1, 0.8, 1.8 and 5.5 GB mixes).
+    const double dec_bytes = (double)dec_blocks * B * d.head_dim * 4.0;
+    double per_cu = 3.0 + 3.0 * std::min(1.0, dec_bytes / 4.0e9);
+    // Inside a prefill-dominated launch, fewer and longer decode units: each
+    // one streams beside the tiles for much of the launch (measured best at
+    // about one per CU on the 2k-token prefill-heavy mix and the 70B replay;
+    // decode-dominated steps keep the rule above).
+    const double pf_flops = 4.0 * d.head_dim * d.num_q_heads * pf_keys;
+    if (fused && pf_flops > t.fuse_flops_per_byte * dec_bytes) per_cu = t.fuse_units_per_cu;
+    const int64_t target = t.decode_target_items > 0
+                               ? t.decode_target_items
+                               : std::max<int64_t>(1, (int64_t)(t.num_cus * per_cu));
+    int64_t sb = ceil_div(dec_blocks, target);
+    sb = std::max<int64_t>(sb, 8);
+    sb = ceil_div(sb, kDecodeWaves) * kDecodeWaves;
+    p.decode_split_blocks = (int32_t)sb;
+    // with the decode rows inside the prefill launch, their units (in tile
+    // steps) join the split estimate of that launch
+    if (fused) {
+      auto& hist = sc.dec_hist;
+      hist.assign((size_t)sb + 2, 0);
+      each_decode_token([&](const cp_row_meta&, int32_t, int32_t kv_end) {
+        const int64_t nb = ceil_div(kv_end, B);
+        const int64_t ns = std::max<int64_t>(1, ceil_div(nb, sb));
+        for (int64_t s = 0; s < ns; ++s) ++hist[nb * (s + 1) / ns - nb * s / ns];
+      });
+      for (int64_t b = 1; b < (int64_t)hist.size(); ++b)
+        if (hist[b] > 0)
+          sc.dec_groups.push_back(
+              {(int64_t)std::ceil((double)(b * B) / std::max(1.0, t.fuse_keys_per_step)) + 1,
+               hist[b] * Hkv});
+    }
+  }
+
   // Key ranges longer than split_keys are cut on a grid of multiples of
   // split_keys, the same grid for every tile, so the tiles of one chunk share
   // their split ranges exactly.  No cut lies past a tile's first query
@@ -517,45 +586,9 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     interleave_by_xcd(sc.items[w], Hkv, t.num_xcds, sc, w ? p.prefill_wide : p.prefill);
   }
 
-  // ---- decode ranges --------------------------------------------------
-  // Rows shorter than prefill_min_len run on the split-K decode kernel, one
-  // item list per query token: token j of a row sits at position
-  // chunk_start + j and sees keys [0, chunk_start + j + 1), so each token is
-  // its own "decode row" with its own causal limit (a one-token row is the
-  // usual case; few-token chunks read their request's K/V once per token).
-  auto each_decode_token = [&](auto&& f) {
-    for (int32_t r = 0; r < n_rows; ++r) {
-      const cp_row_meta& m = rows[r];
-      if (m.chunk_len <= 0 || m.chunk_len >= t.prefill_min_len) continue;
-      for (int32_t j = 0; j < m.chunk_len; ++j)
-        f(m, (int32_t)(off[r] + j), m.chunk_start + j + 1);
-    }
-  };
-  int64_t dec_blocks = 0;
-  each_decode_token([&](const cp_row_meta&, int32_t, int32_t kv_end) {
-    dec_blocks += ceil_div(kv_end, B) * Hkv;
-  });
+  // ---- decode ranges (sized above) ------------------------------------
   if (dec_blocks > 0) {
-    // Items per CU grow with the decode bytes: ~3 per CU (the kernel keeps
-    // three workgroups resident) for small loads, where every extra item costs
-    // plan upload, partial rows for the merge and a workgroup's start-up,
-    // rising to 6 per CU at 4 GB and above, where finer items balance the
-    // tail better (measured on the 0.1, 0.8, 1.8 and 5.5 GB mixes).
-    const double dec_bytes = (double)dec_blocks * B * d.head_dim * 4.0;
-    double per_cu = 3.0 + 3.0 * std::min(1.0, dec_bytes / 4.0e9);
-    // Inside a prefill-dominated launch, fewer and longer decode units: each
-    // one streams beside the tiles for much of the launch (measured best at
-    // about one per CU on the 2k-token prefill-heavy mix and the 70B replay;
-    // decode-dominated steps keep the rule above).
-    const double pf_flops = 4.0 * d.head_dim * d.num_q_heads * pf_keys;
-    if (fused && pf_flops > t.fuse_flops_per_byte * dec_bytes) per_cu = t.fuse_units_per_cu;
-    const int64_t target = t.decode_target_items > 0
-                               ? t.decode_target_items
-                               : std::max<int64_t>(1, (int64_t)(t.num_cus * per_cu));
-    int64_t sb = ceil_div(dec_blocks, target);
-    sb = std::max<int64_t>(sb, 8);
-    sb = ceil_div(sb, kDecodeWaves) * kDecodeWaves;
-    p.decode_split_blocks = (int32_t)sb;
+    const int64_t sb = p.decode_split_blocks;
     // Items are placed longest first (a stable counting sort on their block
     // count, which is at most sb): first count, then place.
     auto& count = sc.count;

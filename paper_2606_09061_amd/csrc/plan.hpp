@@ -148,6 +148,8 @@ struct PlanScratch {
   std::vector<std::pair<int64_t, int64_t>> groups2;  // (cost, count) of one split candidate
   std::vector<std::pair<int64_t, int64_t>> load_hist; // (slot load, slots), by load
   std::vector<PrefillRec> recs_tmp;                   // a record list being re-laid out
+  std::vector<int64_t> dec_hist;                      // decode units per block count
+  std::vector<std::pair<int64_t, int64_t>> dec_groups; // (cost, count) of fused decode units
 };
 
 struct Plan {
