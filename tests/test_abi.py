@@ -242,6 +242,26 @@ def test_prefill_tile_width_follows_the_step_key_range():
     assert widest([[0, 0, 2000, 2000], [1, 1200, 8, 1208]]) == 32   # (2000*1000 + 8*1204)/2008
 
 
+def test_fused_split_estimate_counts_the_decode_units(monkeypatch):
+    """With the decode rows inside the prefill launch, their units fill the
+    launch's slots too, so a step whose decode work dominates keeps its
+    prefill tiles unsplit (no merge traffic) where the prefill rows alone
+    would have been split; a prefill-heavy step still splits."""
+    b = make_config(2)   # 2 x 192-token chunks + 128 decode rows (decode-heavy)
+    d = cp.desc_for(b)
+    monkeypatch.setenv("CP_FUSE_NARROW", "0")
+    fused = cp.plan_summary(d, b.rows)
+    monkeypatch.setenv("CP_FUSE_DECODE", "0")
+    alone = cp.plan_summary(d, b.rows)
+    assert fused["prefill_items"] < alone["prefill_items"]
+    monkeypatch.delenv("CP_FUSE_DECODE")
+    monkeypatch.delenv("CP_FUSE_NARROW")
+    b3 = make_config(3)  # prefill-heavy: long prior contexts still split (128-row tiles)
+    s3 = cp.plan_summary(cp.desc_for(b3), b3.rows)
+    tiles3 = 4 * -(-480 * 4 // 128) * 8
+    assert s3["prefill_items"] > tiles3
+
+
 def test_fused_steps_use_128_row_tiles_and_fewer_decode_units(monkeypatch):
     """A step whose decode rows run inside the prefill launch takes 128-row
     tiles (unless CP_FUSE_NARROW=0) and, when its prefill flops dominate,
@@ -373,10 +393,11 @@ def test_compute_calls_reject_bad_tables_under_debug_only_after_validation(monke
 # ------------------------------------------------- decode blocks in the prefill launch
 
 def _layouts(batch, monkeypatch, mode):
-    # same tile widths and decode split in every mode, so that only the
-    # placement differs
+    # same tile widths, prefill split and decode split in every mode, so that
+    # only the placement differs
     monkeypatch.setenv("CP_FUSE_NARROW", "0")
     monkeypatch.setenv("CP_DECODE_TARGET_ITEMS", "700")
+    monkeypatch.setenv("CP_PREFILL_TARGET_ITEMS", "600")
     monkeypatch.setenv("CP_FUSE_DECODE", str(mode))
     d = cp.desc_for(batch)
     return [cp.plan_records(d, batch.rows, w) for w in (0, 1)], cp.plan_items(d, batch.rows)
