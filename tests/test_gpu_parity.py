@@ -183,9 +183,10 @@ def test_decode_inside_the_prefill_launch(monkeypatch, geom, width):
     tiles; 4-wave workgroups with one unit,
     8-wave ones with two, an odd unit count leaving one group idle) or in
     their own launch (0): every mode matches the oracle element by element and
-    gives the same output bits as the others (the decode split is pinned: a
-    fused prefill-heavy step otherwise takes fewer, longer decode units)."""
+    gives the same output bits as the others (the decode and prefill splits
+    are pinned: fused, a step otherwise splits both differently)."""
     monkeypatch.setenv("CP_DECODE_TARGET_ITEMS", "300")
+    monkeypatch.setenv("CP_PREFILL_TARGET_ITEMS", "400")
     hq, hkv, d, b = geom
     G = hq // hkv
     if width == "wide":
