@@ -228,13 +228,21 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
             for b in batches]
     stream = torch.cuda.current_stream()
 
+    two_calls = os.environ.get("CP_BENCH_TWO_CALLS") == "1"
+
     def step(i):
+        # one step: the paged append, then the attention, as cp_step_mixed
+        # (one call; CP_BENCH_TWO_CALLS=1: cp_kv_append then cp_attn_mixed)
         j = i % len(batches)
         b, d, t = batches[j], descs[j], steps[j]
-        cp.kv_append(d, t["k_new"], t["v_new"], shared["k_cache"], shared["v_cache"], tables[j],
-                     b.rows, ws, stream=stream)
-        cp.attn_mixed(d, t["q"], shared["k_cache"], shared["v_cache"], tables[j], b.rows, outs[j],
-                      ws, stream=stream)
+        if two_calls:
+            cp.kv_append(d, t["k_new"], t["v_new"], shared["k_cache"], shared["v_cache"],
+                         tables[j], b.rows, ws, stream=stream)
+            cp.attn_mixed(d, t["q"], shared["k_cache"], shared["v_cache"], tables[j], b.rows,
+                          outs[j], ws, stream=stream)
+        else:
+            cp.step_mixed(d, t["q"], t["k_new"], t["v_new"], shared["k_cache"], shared["v_cache"],
+                          tables[j], b.rows, outs[j], ws, stream=stream)
 
     if prime:
         # the replay's caches are built by its own appends: run the full

@@ -153,6 +153,18 @@ int cp_attn_mixed(const cp_attn_desc *desc, const void *q, const void *k_cache,
                   const void *v_cache, const int32_t *block_tables, const cp_row_meta *rows,
                   int32_t n_rows, void *out, void *ws, size_t ws_bytes, void *stream);
 
+/* One step: cp_kv_append followed by cp_attn_mixed on the same rows, with
+ * the same results bit for bit, in fewer launches: when the append's span
+ * list fits the kernel arguments (at most 200 spans of one request and block),
+ * the attention plan's copy into ws runs inside the append launch, so its
+ * trip over PCIe overlaps the append; otherwise the two calls run in turn.
+ * Arguments as for the two calls (one workspace for both, sized by
+ * cp_workspace_bytes); same checks and codes, nothing enqueued on error. */
+int cp_step_mixed(const cp_attn_desc *desc, const void *q, const void *k_new, const void *v_new,
+                  void *k_cache, void *v_cache, const int32_t *block_tables,
+                  const cp_row_meta *rows, int32_t n_rows, void *out, void *ws, size_t ws_bytes,
+                  void *stream);
+
 /* A batch's attention plan, made once and run several times: the layers of
  * one model iteration share rows, block tables and plan, and only q, the
  * caches and out change.  Plain data filled by cp_attn_prepare and owned by

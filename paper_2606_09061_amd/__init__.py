@@ -23,6 +23,7 @@ from .binding import (  # noqa: F401
     plan_items,
     plan_records,
     plan_summary,
+    step_mixed,
     version,
     workspace_bytes,
 )

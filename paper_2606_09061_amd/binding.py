@@ -90,6 +90,8 @@ def load():
     lib.cp_plan_summary.restype = ctypes.c_int
     lib.cp_plan_items.argtypes = [dp, vp, i32, vp, i64]
     lib.cp_plan_items.restype = i64
+    lib.cp_step_mixed.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, i32, vp, vp, ctypes.c_size_t, vp]
+    lib.cp_step_mixed.restype = ctypes.c_int
     lib.cp_plan_records.argtypes = [dp, vp, i32, i32, vp, i64]
     lib.cp_plan_records.restype = i64
     lib.cp_noalloc_init.argtypes, lib.cp_noalloc_init.restype = [], ctypes.c_int
@@ -105,7 +107,7 @@ def exported_symbols():
     return ["cp_version", "cp_strerror", "cp_workspace_bytes", "cp_check_batch",
             "cp_check_block_tables", "cp_kv_append",
             "cp_attn_mixed", "cp_attn_prepare", "cp_attn_run", "cp_plan_summary", "cp_plan_items",
-            "cp_plan_records",
+            "cp_plan_records", "cp_step_mixed",
             "cp_noalloc_init", "cp_attn_mixed_noalloc", "cp_profile_begin", "cp_profile_end"]
 
 
@@ -197,6 +199,19 @@ def attn_mixed(desc: Desc, q, k_cache, v_cache, block_tables, rows, out, ws, ws_
                               nbytes, _stream(stream))
     if rc != CP_OK:
         raise CpError(rc, "cp_attn_mixed")
+
+
+def step_mixed(desc: Desc, q, k_new, v_new, k_cache, v_cache, block_tables, rows, out, ws,
+               ws_bytes=None, stream=None) -> None:
+    """cp_step_mixed: kv_append then attn_mixed in one call (the attention
+    plan's copy shares the append's launch)."""
+    r = _rows(rows)
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    rc = load().cp_step_mixed(ctypes.byref(desc), _ptr(q), _ptr(k_new), _ptr(v_new),
+                              _ptr(k_cache), _ptr(v_cache), _ptr(block_tables), r.ctypes.data,
+                              r.shape[0], _ptr(out), _ptr(ws), nbytes, _stream(stream))
+    if rc != CP_OK:
+        raise CpError(rc, "cp_step_mixed")
 
 
 def attn_prepare(desc: Desc, rows, ws, ws_bytes=None, stream=None) -> AttnPlan:

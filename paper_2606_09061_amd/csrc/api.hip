@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "cp_attn.h"
+#include "copy_body.hpp"
 #include "kernels.hpp"
 #include "plan.hpp"
 
@@ -60,24 +61,8 @@ __global__ __launch_bounds__(1024) void plan_copy_kernel(const uint4* __restrict
                                                          uint4* __restrict__ dst, int n16,
                                                          uint32_t* __restrict__ done,
                                                          uint32_t seq) {
-  for (int base = blockIdx.x * kCopyPiece + (int)threadIdx.x; base < n16;
-       base += gridDim.x * kCopyPiece) {
-    uint4 v[kCopyPer];
-#pragma unroll
-    for (int k = 0; k < kCopyPer; ++k) {
-      const int i = base + k * 1024;
-      v[k] = i < n16 ? src[i] : make_uint4(0, 0, 0, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first store
-#pragma unroll
-    for (int k = 0; k < kCopyPer; ++k) {
-      const int i = base + k * 1024;
-      if (i < n16) dst[i] = v[k];
-    }
-  }
-  __syncthreads();  // every read of this workgroup has returned
-  if (threadIdx.x == 0)
-    __hip_atomic_store(done + blockIdx.x, seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  plan_copy_body<1024, kCopyPer>(src, dst, n16, done, seq, (int)blockIdx.x, (int)gridDim.x,
+                                 (int)threadIdx.x);
 }
 
 // Waits until the slot's last copy has read it (normally long done: a slot
@@ -218,12 +203,11 @@ DeviceCtx* device_ctx(int* err) {
 }
 
 // Takes a free ring slot of the current device (waiting for its previous
-// copy if that is still pending), fills it through `fill(host)` and enqueues
-// the plan copy into dst.  The slot stays busy until release_stage.
+// copy if that is still pending), fills it through `fill(host)` and draws the
+// sequence number of its copy.  The slot stays busy until release_stage.
 template <class Fill>
-int upload(void* dst, size_t bytes, hipStream_t s, Stage** taken, Fill&& fill) {
+int take_stage(size_t bytes, Stage** taken, uint32_t* seq, Fill&& fill) {
   *taken = nullptr;
-  if (bytes == 0) return CP_OK;
   for (;;) {
     std::unique_lock<std::mutex> lk(g_mu);
     int err = CP_OK;
@@ -246,11 +230,28 @@ int upload(void* dst, size_t bytes, hipStream_t s, Stage** taken, Fill&& fill) {
     if (rc == CP_OK) rc = stage_reserve(*st, bytes);
     if (rc != CP_OK) return rc;
     fill(st->host);
-    if (launch_plan_copy(*st, dst, bytes, next_seq(c), s) != CP_OK) return CP_ERR_HIP;
+    *seq = next_seq(c);
     st->busy = true;
     *taken = st;
     return CP_OK;
   }
+}
+
+// take_stage, then the copy of the slot into dst on stream s.
+template <class Fill>
+int upload(void* dst, size_t bytes, hipStream_t s, Stage** taken, Fill&& fill) {
+  *taken = nullptr;
+  if (bytes == 0) return CP_OK;
+  uint32_t seq = 0;
+  const int rc = take_stage(bytes, taken, &seq, fill);
+  if (rc != CP_OK) return rc;
+  if (launch_plan_copy(**taken, dst, bytes, seq, s) != CP_OK) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    (*taken)->busy = false;
+    *taken = nullptr;
+    return CP_ERR_HIP;
+  }
+  return CP_OK;
 }
 
 // After the call's last launch the slot may be taken again (its completion
@@ -708,6 +709,83 @@ int cp_attn_mixed(const cp_attn_desc* desc, const void* q, const void* k_cache,
   const int rr = cp_attn_run(&plan, q, k_cache, v_cache, block_tables, out, ws, ws_bytes, stream);
   const int rs = release_stage(st, s);
   return rr != CP_OK ? rr : rs;
+}
+
+int cp_step_mixed(const cp_attn_desc* desc, const void* q, const void* k_new, const void* v_new,
+                  void* k_cache, void* v_cache, const int32_t* block_tables,
+                  const cp_row_meta* rows, int32_t n_rows, void* out, void* ws, size_t ws_bytes,
+                  void* stream) {
+  const int v = validate(desc, rows, n_rows);
+  if (v != CP_OK) return v;
+  const int64_t tokens = total_tokens(rows, n_rows);
+  if (tokens == 0) return CP_OK;
+  if (!q || !k_new || !v_new || !k_cache || !v_cache || !block_tables || !out || !ws)
+    return CP_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) ||
+      !aligned(v_cache, 16) || !aligned(out, 16) || !aligned(ws, 256) || !aligned(block_tables, 4))
+    return CP_ERR_INVALID_ARG;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  try {
+    AppendPlan& ap = thread_append_plan();
+    build_append_plan(*desc, rows, n_rows, ap);
+    if (ap.items.size() > (size_t)kAppendInlineItems) {
+      // a long span list is uploaded itself: the two calls in turn
+      const int ra = cp_kv_append(desc, k_new, v_new, k_cache, v_cache, block_tables, rows,
+                                  n_rows, ws, ws_bytes, stream);
+      if (ra != CP_OK) return ra;
+      return cp_attn_mixed(desc, q, k_cache, v_cache, block_tables, rows, n_rows, out, ws,
+                           ws_bytes, stream);
+    }
+    if (debug_mode()) {
+      const int rc = debug_check_tables(desc, block_tables, rows, n_rows, s);
+      if (rc != CP_OK) return rc;
+    }
+    Plan& p = thread_plan();
+    build_plan(*desc, rows, n_rows, tuning_from_env(num_cus_setting()), p);
+    if (ws_bytes < p.ws_bytes) return CP_ERR_WORKSPACE;
+    Stage* st = nullptr;
+    uint32_t seq = 0;
+    int rc = take_stage(p.plan_bytes, &st, &seq, [&](uint8_t* h) { serialize_into(p, h); });
+    if (rc != CP_OK) return rc;
+    thread_local AppendInline inl;
+    std::memcpy(inl.items, ap.items.data(), ap.items.size() * sizeof(AppendItem));
+    AppendArgs a;
+    a.items = nullptr;
+    a.n_items = (int)ap.items.size();
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
+    a.k_cache = static_cast<uint16_t*>(k_cache);
+    a.v_cache = static_cast<uint16_t*>(v_cache);
+    a.bt = block_tables;
+    a.hkv = desc->num_kv_heads;
+    a.mbr = desc->max_blocks_per_req;
+    PlanCopyArgs cpa;
+    cpa.src = static_cast<const uint4*>(st->dev);
+    cpa.dst = static_cast<uint4*>(ws);
+    cpa.n16 = (int)(p.plan_bytes / 16);
+    cpa.done = st->done_dev;
+    cpa.seq = seq;
+    cpa.n_blocks = std::min(kCopyBlocksMax, (cpa.n16 + 8 * 256 - 1) / (8 * 256));
+    const long pi = prof_open(0, s);
+    const hipError_t e = launch_append_copy(desc->head_dim, desc->block_size, a, inl, cpa, s);
+    prof_close(pi, s);
+    if (e == hipSuccess) {  // the slot's completion words now belong to this copy
+      st->seq = seq;
+      st->blocks = cpa.n_blocks;
+    }
+    rc = finish(e, s);
+    if (rc == CP_OK) {
+      cp_attn_plan pl{};
+      pl.desc = *desc;
+      pl.tokens = tokens;
+      fill_plan(p, pl);
+      rc = cp_attn_run(&pl, q, k_cache, v_cache, block_tables, out, ws, ws_bytes, stream);
+    }
+    const int rs = release_stage(st, s);
+    return rc != CP_OK ? rc : rs;
+  } catch (...) {
+    return CP_ERR_INVALID_ARG;
+  }
 }
 
 int cp_noalloc_init(void) {

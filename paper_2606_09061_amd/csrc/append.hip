@@ -2,25 +2,25 @@
 //
 // One workgroup per (request, logical block) span of new tokens and kv head;
 // the span list comes from device memory or, when short, from the kernel
-// arguments.
+// arguments (where a step's attention plan copy can share the launch).
 // K rows are token-major inside a block, so each 16-byte chunk of a new K row
 // is one aligned vector copy.  V is feature-major inside a block ([D][B]): a
 // thread transposes an 8-slot x 8-feature tile in registers, reading token
 // rows and writing feature runs with 16-byte accesses.  Every load is issued
 // before the first store.
+#include "copy_body.hpp"
 #include "device.hpp"
 #include "kernels.hpp"
 
 namespace cpattn {
 
 template <int D, int B>
-__device__ __forceinline__ void append_span(const AppendItem& it,
+__device__ __forceinline__ void append_span(const AppendItem& it, int h,
                                             const uint16_t* __restrict__ k_new,
                                             const uint16_t* __restrict__ v_new,
                                             uint16_t* __restrict__ k_cache,
                                             uint16_t* __restrict__ v_cache,
                                             const int32_t* __restrict__ bt, int hkv, int mbr) {
-  const int h = blockIdx.y;
   const int req = it.req_slot0 >> 8;
   const int slot0 = it.req_slot0 & 0xff;
   const int64_t blk = bt[(int64_t)req * mbr + it.block];
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const AppendItem* __rest
                                                         uint16_t* __restrict__ v_cache,
                                                         const int32_t* __restrict__ bt, int hkv,
                                                         int mbr) {
-  append_span<D, B>(items[blockIdx.x], k_new, v_new, k_cache, v_cache, bt, hkv, mbr);
+  append_span<D, B>(items[blockIdx.x], blockIdx.y, k_new, v_new, k_cache, v_cache, bt, hkv, mbr);
 }
 
 template <int D, int B>
@@ -110,7 +110,27 @@ __global__ __launch_bounds__(256) void kv_append_inline_kernel(const AppendInlin
                                                                uint16_t* __restrict__ v_cache,
                                                                const int32_t* __restrict__ bt,
                                                                int hkv, int mbr) {
-  append_span<D, B>(inl.items[blockIdx.x], k_new, v_new, k_cache, v_cache, bt, hkv, mbr);
+  append_span<D, B>(inl.items[blockIdx.x], blockIdx.y, k_new, v_new, k_cache, v_cache, bt, hkv,
+                    mbr);
+}
+
+// The append of a step together with the copy of its attention plan, one
+// launch: workgroups [0, n_copy) copy the staged plan (host round trips),
+// the rest append (item (b - n_copy) / hkv, kv head (b - n_copy) % hkv), so
+// the plan's trip over PCIe overlaps the append instead of following it.
+template <int D, int B>
+__global__ __launch_bounds__(256) void kv_append_copy_kernel(
+    const AppendInline inl, const uint16_t* __restrict__ k_new,
+    const uint16_t* __restrict__ v_new, uint16_t* __restrict__ k_cache,
+    uint16_t* __restrict__ v_cache, const int32_t* __restrict__ bt, int hkv, int mbr,
+    PlanCopyArgs cp) {
+  const int b = blockIdx.x;
+  if (b < cp.n_blocks) {
+    plan_copy_body<256>(cp.src, cp.dst, cp.n16, cp.done, cp.seq, b, cp.n_blocks, threadIdx.x);
+    return;
+  }
+  const int a = b - cp.n_blocks;
+  append_span<D, B>(inl.items[a / hkv], a % hkv, k_new, v_new, k_cache, v_cache, bt, hkv, mbr);
 }
 
 template <int D, int B>
@@ -124,6 +144,25 @@ static hipError_t launch_append_t(const AppendArgs& a, const AppendInline* inl, 
                        a.k_new, a.v_new, a.k_cache, a.v_cache, a.bt, a.hkv, a.mbr);
   }
   return hipGetLastError();
+}
+
+template <int D, int B>
+static hipError_t launch_append_copy_t(const AppendArgs& a, const AppendInline& inl,
+                                       const PlanCopyArgs& cp, hipStream_t s) {
+  if (a.n_items > kAppendInlineItems) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((kv_append_copy_kernel<D, B>), dim3(cp.n_blocks + a.n_items * a.hkv),
+                     dim3(256), 0, s, inl, a.k_new, a.v_new, a.k_cache, a.v_cache, a.bt, a.hkv,
+                     a.mbr, cp);
+  return hipGetLastError();
+}
+
+hipError_t launch_append_copy(int D, int B, const AppendArgs& a, const AppendInline& inl,
+                              const PlanCopyArgs& cp, hipStream_t s) {
+  if (D == 128 && B == 16) return launch_append_copy_t<128, 16>(a, inl, cp, s);
+  if (D == 128 && B == 32) return launch_append_copy_t<128, 32>(a, inl, cp, s);
+  if (D == 64 && B == 16) return launch_append_copy_t<64, 16>(a, inl, cp, s);
+  if (D == 64 && B == 32) return launch_append_copy_t<64, 32>(a, inl, cp, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_append(int D, int B, const AppendArgs& a, const AppendInline* inl,

@@ -47,10 +47,24 @@ struct AttnArgs {
   float scale_log2;  // sm_scale * log2(e)
 };
 
+// A staged plan's copy: n16 16-byte words from src (pinned host memory) to
+// dst by n_blocks workgroups, each writing seq to done[its index] at the end.
+struct PlanCopyArgs {
+  const uint4* src;
+  uint4* dst;
+  int n16;
+  uint32_t* done;
+  uint32_t seq;
+  int n_blocks;
+};
+
 // `inl` non-null: the items are taken from it (a.n_items <= kAppendInlineItems)
 // and a.items is ignored.
 hipError_t launch_append(int D, int B, const AppendArgs& a, const AppendInline* inl,
                          hipStream_t s);
+// the inline append and a plan copy in one launch (256-thread workgroups)
+hipError_t launch_append_copy(int D, int B, const AppendArgs& a, const AppendInline& inl,
+                              const PlanCopyArgs& cp, hipStream_t s);
 hipError_t launch_prefill(int D, int G, const AttnArgs& a, hipStream_t s);
 hipError_t launch_decode(int D, int B, int G, const AttnArgs& a, hipStream_t s);
 hipError_t launch_merge(int D, int G, const AttnArgs& a, hipStream_t s);

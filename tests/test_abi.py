@@ -110,8 +110,20 @@ def test_compute_calls_reject_before_touching_anything():
     rc = lib.cp_kv_append(ctypes.byref(d), fake, fake, fake, fake, fake, good.ctypes.data, 2,
                           fake, 0, None)
     assert rc == binding.CP_ERR_WORKSPACE
+    # the one-call step: the same checks, before anything is enqueued
+    step = lib.cp_step_mixed
+    assert step(ctypes.byref(d), fake, fake, fake, fake, fake, fake, bad.ctypes.data, 1, fake,
+                fake, 1 << 30, None) == binding.CP_ERR_BAD_META
+    assert step(ctypes.byref(d), fake, None, fake, fake, fake, fake, good.ctypes.data, 2, fake,
+                fake, 1 << 30, None) == binding.CP_ERR_INVALID_ARG
+    assert step(ctypes.byref(d), fake, fake, fake + 8, fake, fake, fake, good.ctypes.data, 2,
+                fake, fake, 1 << 30, None) == binding.CP_ERR_INVALID_ARG  # misaligned v_new
+    assert step(ctypes.byref(d), fake, fake, fake, fake, fake, fake, good.ctypes.data, 2, fake,
+                fake, need - 1, None) == binding.CP_ERR_WORKSPACE
     # an empty batch succeeds without touching its (null) buffers
     empty = np.zeros((0, 4), np.int32)
+    assert step(ctypes.byref(d), None, None, None, None, None, None, empty.ctypes.data, 0, None,
+                None, 0, None) == 0
     assert lib.cp_attn_mixed(ctypes.byref(d), None, None, None, None, empty.ctypes.data, 0, None,
                              None, 0, None) == 0
     assert lib.cp_kv_append(ctypes.byref(d), None, None, None, None, None, empty.ctypes.data, 0,

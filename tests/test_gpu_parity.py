@@ -220,3 +220,52 @@ def test_decode_inside_the_prefill_launch(monkeypatch, geom, width):
         outs[mode] = words(out)
     for mode in (1, 2, 3, 4):
         assert np.array_equal(outs[mode], outs[0]), f"mode {mode} differs from its own launch"
+
+
+def _step_batches():
+    rng = np.random.default_rng(77)
+    yield "tiny", make_config(1)
+    yield "ragged-70b", make_batch("step", 64, 8, 128, 32,
+                                   [(3000, 60), (0, 150), (40, 2), (31, 1), (64, 1), (0, 1),
+                                    (6000, 1)], rng)
+    # more than 200 spans: the long span list is uploaded and the two calls run in turn
+    yield "many-spans", make_batch("spans", 32, 8, 128, 16,
+                                   [(int(c), 1) for c in rng.integers(0, 3000, 230)] +
+                                   [(100, 40)], rng)
+
+
+@pytest.mark.parametrize("which", ["tiny", "ragged-70b", "many-spans"])
+def test_step_matches_append_then_attention(which):
+    """cp_step_mixed (the plan copy inside the append launch) writes the same
+    pools and the same output bits as cp_kv_append then cp_attn_mixed, and
+    matches the oracle; two steps in a row reuse the staging slots."""
+    import paper_2606_09061_amd as cp
+    batch = dict(_step_batches())[which]
+    tens = make_tensors(batch, seed=8800 + len(which))
+    say(f"[gpu] step {which}: rows={batch.n_rows} T={batch.num_tokens}")
+    kc_ref, vc_ref = oracle.kv_append(batch, tens["k_new"], tens["v_new"], tens["k_cache"],
+                                      tens["v_cache"])
+    ref = oracle.attn(batch, tens["q"], kc_ref, vc_ref)
+    d = cp.desc_for(batch)
+    a, b = to_dev(tens), to_dev(tens)
+    ws_a = torch.empty(cp.workspace_bytes(d, batch.rows), dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty_like(ws_a)
+    outs = []
+    for t, ws, one_call in ((a, ws_a, False), (b, ws_b, True)):
+        out = torch.empty(batch.num_tokens, batch.num_q_heads, batch.head_dim,
+                          dtype=torch.bfloat16, device="cuda")
+        for _ in range(2):   # the second pass appends the same tokens again (same bits)
+            if one_call:
+                cp.step_mixed(d, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                              t["block_tables"], batch.rows, out, ws)
+            else:
+                cp.kv_append(d, t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                             t["block_tables"], batch.rows, ws)
+                cp.attn_mixed(d, t["q"], t["k_cache"], t["v_cache"], t["block_tables"],
+                              batch.rows, out, ws)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert np.array_equal(words(b["k_cache"]).reshape(-1), kc_ref.reshape(-1))
+    assert np.array_equal(words(b["v_cache"]).reshape(-1), vc_ref.reshape(-1))
+    assert np.array_equal(words(outs[0]), words(outs[1])), "step differs from the two calls"
+    assert_close(outs[1], ref, f"step {which}")
