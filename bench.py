@@ -2,14 +2,15 @@
 """Benchmark of one chunked-prefill scheduling iteration's attention step on MI355X.
 
 A step is cp_kv_append + cp_attn_mixed over one batch of synthetic input (the
-whole hot path: planner, append, prefill-MFMA, decode split-K, merge).  With
+whole hot path: planner, append, prefill-MFMA, decode split-K, merge), issued
+as one cp_step_mixed call.  With
 no flags it runs the 70B-shaped mix (64 q / 8 kv heads, head_dim 128, block
 32, token budget 4096): a 20-iteration replay of an aging/APC schedule over
 64 requests, one iteration per step, cycling, on one GPU, and prints one JSON
 line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--config N] [--all]
-                  [--sub prefill|decode] [--cold N] [--no-cpu]
+                  [--sub prefill|decode] [--cold N] [--no-cpu] [--settle S]
   python bench.py --peaks
   python bench.py --latency-table out.csv
   python bench.py --fit out.csv
@@ -17,7 +18,10 @@ line.
 ``--config N`` picks another mix (1 tiny, 2 Llama-3-8B budget 512, 3 prefill-
 heavy, 4 decode-dominated).  ``--all`` prints one line per mix.  ``--sub``
 times only the prefill rows or only the decode rows of the mix (same pools);
-``--cold`` adds steps timed after flushing the caches.
+``--cold`` adds steps timed after flushing the caches.  Before the warm-up the
+steps run back to back for ``--settle`` seconds (default 1) so that the timed
+region starts at the clock the GPU holds under load, not during its ramp from
+idle.
 """
 
 from __future__ import annotations
@@ -89,9 +93,23 @@ def decode_fused(batch):
     return any((cp.plan_records(d, batch.rows, w)[:, 1] == -1).any() for w in (0, 1))
 
 
-def kernel_sha(name):
-    with open(os.path.join(ROOT, "paper_2606_09061_amd", "csrc", name), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def kernel_sha(*names):
+    """Hash of the given sources and of every local header they include, so
+    counters taken on other code are never reported."""
+    import re
+    csrc = os.path.join(ROOT, "paper_2606_09061_amd", "csrc")
+    h, seen, todo = hashlib.sha256(), set(), list(names)
+    while todo:
+        fn = todo.pop(0)
+        if fn in seen:
+            continue
+        seen.add(fn)
+        with open(os.path.join(csrc, fn), "rb") as f:
+            text = f.read()
+        h.update(fn.encode() + b"\0" + text)
+        todo += [m.decode() for m in re.findall(rb'#include\s+"([^"]+)"', text)
+                 if os.path.exists(os.path.join(csrc, m.decode()))]
+    return h.hexdigest()[:16]
 
 
 def traffic_for(kernel, workload):
@@ -104,7 +122,9 @@ def traffic_for(kernel, workload):
     except (OSError, ValueError):
         return None
     ent = rec.get(f"{kernel}:{workload}")
-    if not ent or ent.get("src_sha") != kernel_sha(f"{kernel}.hip"):
+    # the kernel's source with its headers, and the planner that sizes its
+    # work items and key splits (both change the bytes a launch moves)
+    if not ent or ent.get("src_sha") != kernel_sha(f"{kernel}.hip", "plan.cpp"):
         return None
     return ent.get("bytes_per_launch")
 
@@ -209,7 +229,8 @@ def build_inputs(cfg, device, sub=None):
     return [sb], [{"q": q, "k_new": kn, "v_new": vn}], shared, []
 
 
-def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, cold=0):
+def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, cold=0,
+               settle_s=1.0):
     import numpy as np
     import torch
     import paper_2606_09061_amd as cp
@@ -270,10 +291,25 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
             host = (batches, (shared["k_cache"].cpu().view(torch.int16).numpy().view(np.uint16),
                               shared["v_cache"].cpu().view(torch.int16).numpy().view(np.uint16)),
                     [{k: v.cpu() for k, v in steps[0].items()}])
+    # Clock settling: the GPU idles at ~0.1 GHz and its governor takes a few
+    # hundred milliseconds of continuous work to reach the clock it holds under
+    # this load (~2.1 GHz on the MFMA-heavy mixes, set by the power limit;
+    # up to 2.4 GHz when lightly loaded).  A timed region of a few milliseconds
+    # started from idle would measure that ramp, so whole cycles of the same
+    # steps run back to back for `settle_s` first (untimed, like the warm-up).
+    n_settle = 0
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < settle_s:
+        for _ in range(len(batches)):
+            step(n_settle)
+            n_settle += 1
+    torch.cuda.synchronize()
+    settle_wall = time.perf_counter() - t_settle
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    log(f"[bench] warmup done ({warmup} steps); timing {steps_n} steps")
+    log(f"[bench] clock settling {n_settle} steps in {settle_wall:.2f} s; "
+        f"warmup done ({warmup} steps); timing {steps_n} steps")
     def timed(n, mode):
         """n steps on the step stream.  mode "total": only two bracketing
         events; "steps": an event after every step as well; "kernels": the
@@ -413,6 +449,7 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
         "roofline": roof,
         "roofline_step": roof_step,
         "other_kernel": other,
+        "clock_settle": {"seconds": settle_wall, "steps": n_settle},
     }
     if cold:
         # cold steps: a 1 GiB buffer is rewritten before each (outside its
@@ -1212,6 +1249,9 @@ def main():
     ap.add_argument("--all", action="store_true", help="one JSON line per mix")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--settle", type=float, default=1.0, metavar="SECONDS",
+                    help="run the steps back to back this long before the warm-up, so the "
+                         "timed region starts at the clock the GPU holds under load (0: off)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain copies of MIB MiB (counter calibration)")
     ap.add_argument("--sub", choices=["prefill", "decode"], default=None,
@@ -1279,7 +1319,8 @@ def main():
     cfgs = [1, 2, 3, 4, 5] if args.all else [args.config]
     for c in cfgs:
         res = run_config(c, args.steps, args.warmup, with_cpu=not args.no_cpu,
-                         cpu_budget=args.cpu_seconds, sub=args.sub, cold=args.cold)
+                         cpu_budget=args.cpu_seconds, sub=args.sub, cold=args.cold,
+                         settle_s=args.settle)
         print(json.dumps(res), flush=True)
 
 
