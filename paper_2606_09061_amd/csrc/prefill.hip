@@ -4,11 +4,13 @@
 // queries over s prior keys costs ~c*s + c^2/2 query-key pairs per head (the
 // prefill_interaction feature of Table 2 tracks exactly that product).
 //
-// Work item: a tile of up to 64*NW query rows of one chunk, where a row is a
-// (token, q head) pair of the G q heads that share one kv head, so K and V
-// are gathered once for all G heads (GQA sharing); plus a key range.  One
-// wave per SIMD; each wave owns 64 rows as two 32-row groups that share
-// every K and V operand read.  Per 64-key step and row group a wave computes
+// Work item: a tile of up to 32*RG*NW query rows of one chunk, where a row is
+// a (token, q head) pair of the G q heads that share one kv head, so K and V
+// are gathered once for all G heads (GQA sharing); plus a key range.  Each
+// wave owns RG groups of 32 rows that share every K and V operand read.  The
+// build uses RG = 1 (RG = 2 needs more registers than a wave can hold without
+// spilling the scores), NW = 4 or 8, and two workgroups per CU, so two waves
+// share each SIMD.  Per 64-key step and row group a wave computes
 //     S^T (64 keys x 32 queries) = K . Q^T      MFMA, fp32 accumulators
 //     online softmax down each query column     fp32, base 2
 //     O^T (D x 32 queries)     += V^T . P^T     MFMA, P rounded to bf16
