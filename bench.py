@@ -1044,7 +1044,7 @@ def model_bench(reps=5, max_seqs=128, only=None):
     return out
 
 
-def per_iteration(cfg, reps=7):
+def per_iteration(cfg, reps=7, settle_s=1.0):
     """Prefill and decode kernel time of every batch of mix ``cfg`` (the 20
     iterations of the replay for mix 5), measured one batch at a time with the
     library's per-kernel events after the batches have run once in order,
@@ -1076,6 +1076,11 @@ def per_iteration(cfg, reps=7):
 
     for j in range(len(batches)):       # every batch once, in order (fills the replay's pools)
         step(j)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()            # clock settling, as in run_config
+    while time.perf_counter() - t0 < settle_s:
+        for j in range(len(batches)):
+            step(j)
     torch.cuda.synchronize()
     times = [{"prefill": [], "decode": []} for _ in batches]
     for rep in range(reps):
@@ -1306,7 +1311,7 @@ def main():
         print(json.dumps(gemm_table()), flush=True)
         return
     if args.per_iteration:
-        print(json.dumps(per_iteration(args.config)), flush=True)
+        print(json.dumps(per_iteration(args.config, settle_s=args.settle)), flush=True)
         return
     if args.model:
         print(json.dumps(model_bench(only=args.model_case)), flush=True)

@@ -501,9 +501,11 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
     // tail better (measured on the 0.1, 0.8, 1.8 and 5.5 GB mixes).
     const double dec_bytes = (double)dec_blocks * B * d.head_dim * 4.0;
     double per_cu = 3.0 + 3.0 * std::min(1.0, dec_bytes / 4.0e9);
-    // Inside a prefill-dominated launch, fewer and longer decode units: each
-    // one streams beside the tiles for much of the launch (measured best at
-    // about one per CU on the 2k-token prefill-heavy mix and the 70B replay;
+    // Inside a prefill-dominated launch, longer decode ranges: each unit
+    // streams beside the tiles for much of the launch.  Only rows longer than
+    // the cut are split, so this sets the longest unit (measured best at
+    // 0.5-1 ranges per CU on the 2k-token prefill-heavy mix and the 70B
+    // replay, with a cliff below 0.5 where whole long rows outlast the tiles;
     // decode-dominated steps keep the rule above).
     const double pf_flops = 4.0 * d.head_dim * d.num_q_heads * pf_keys;
     if (fused && pf_flops > t.fuse_flops_per_byte * dec_bytes) per_cu = t.fuse_units_per_cu;

@@ -108,7 +108,8 @@ struct Tuning {
   double fuse_spread = 1.0;     // mode 3: decode blocks spread over this fraction of the tiles
   double fuse_keys_per_step = 64.0;  // mode 4: decode keys worth one 64-key step of a tile
   bool fuse_narrow = true;      // a step with decode blocks in its prefill launch: 128-row tiles
-  double fuse_units_per_cu = 1.0;    // decode units per CU when prefill dominates a fused step
+  double fuse_units_per_cu = 0.75;   // decode ranges per CU that set the split length when
+                                     // prefill dominates a fused step
   double fuse_flops_per_byte = 180.0;  // prefill dominates: its flops > this x decode bytes
 };
 
