@@ -34,8 +34,10 @@ def check_shapes(batch, t):
         assert (btn[req, :nb] >= 0).all() and (btn[req, :nb] < NB).all()
 
 
-def run_step(batch, t, out=None, ws=None, stream=None):
-    """cp_kv_append then cp_attn_mixed on device tensors ``t`` (caches updated in place)."""
+def run_step(batch, t, out=None, ws=None, stream=None, one_call=False):
+    """cp_kv_append then cp_attn_mixed on device tensors ``t`` (caches updated
+    in place); with ``one_call``, the same step as one cp_step_mixed call, the
+    call the benchmark times."""
     check_shapes(batch, t)
     d = cp.desc_for(batch)
     if out is None:
@@ -44,6 +46,10 @@ def run_step(batch, t, out=None, ws=None, stream=None):
     if ws is None:
         ws = torch.empty(max(256, cp.workspace_bytes(d, batch.rows)), dtype=torch.uint8,
                          device=t["q"].device)
+    if one_call:
+        cp.step_mixed(d, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                      t["block_tables"], batch.rows, out, ws, stream=stream)
+        return out
     cp.kv_append(d, t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["block_tables"],
                  batch.rows, ws, stream=stream)
     cp.attn_mixed(d, t["q"], t["k_cache"], t["v_cache"], t["block_tables"], batch.rows, out, ws,

@@ -1,6 +1,6 @@
 """Full-size GPU parity: the benchmark's mixes in the benchmark's launch
-configuration (same C ABI calls, same plans), checked against the fp64
-oracle.  Whole K/V pools are compared bit for bit after the append, and every
+configuration (the same cp_step_mixed call, the same plans), checked against
+the fp64 oracle; the large-pool and long-context cases take the two calls.  Whole K/V pools are compared bit for bit after the append, and every
 output element (all T x Hq x D of each mix and of each of the replay's 20
 iterations) is compared with the oracle's; max and mean errors are printed
 per mix and per iteration.
@@ -32,7 +32,7 @@ def test_full_size_mix(n):
     t = make_tensors(batch, seed=7000 + n, device=dev)
     host = {k: v.cpu() for k, v in t.items() if k in ("q", "k_new", "v_new")}
     kc0, vc0 = words(t["k_cache"]), words(t["v_cache"])
-    out = run_step(batch, t)
+    out = run_step(batch, t, one_call=True)
     torch.cuda.synchronize()
     kc_ref, vc_ref = oracle.kv_append(batch, host["k_new"], host["v_new"], kc0, vc0)
     del kc0, vc0
@@ -51,7 +51,7 @@ def test_replay_twenty_iterations_lockstep():
         t = {"q": q, "k_new": kn, "v_new": vn, "k_cache": kc, "v_cache": vc,
              "block_tables": torch.from_numpy(b.block_tables).to(dev)}
         say(f"[gpu] replay iteration {i}: rows={b.n_rows} T={b.num_tokens}")
-        out = run_step(b, t)
+        out = run_step(b, t, one_call=True)
         torch.cuda.synchronize()
         kc_ref, vc_ref = oracle.kv_append(b, kn.cpu(), vn.cpu(), kc_ref, vc_ref, inplace=True)
         check_all(b, out, q.cpu(), kc_ref, vc_ref, f"replay it {i}")
