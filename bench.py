@@ -198,13 +198,29 @@ def cpu_baseline(batches, pools0, steps_host, budget_s=10.0, seed=0):
 SUB_MASKS = {"prefill": lambda rows: rows[:, 2] >= 2, "decode": lambda rows: rows[:, 2] == 1}
 
 
-def build_inputs(cfg, device, sub=None):
+def shard_heads(b, shard):
+    """The batch as one GPU of a head-sharded (tensor-parallel) group of
+    ``shard`` GPUs sees it: Hq / shard q heads and Hkv / shard kv heads of
+    every row, same rows, block tables and scale."""
+    import dataclasses
+    if shard == 1:
+        return b
+    if b.num_kv_heads % shard:
+        raise SystemExit(f"--shard {shard} does not divide {b.num_kv_heads} kv heads")
+    return dataclasses.replace(b, name=f"{b.name}-tp{shard}",
+                               num_q_heads=b.num_q_heads // shard,
+                               num_kv_heads=b.num_kv_heads // shard)
+
+
+def build_inputs(cfg, device, sub=None, shard=1):
     """Batches, per-batch step tensors, the shared pools, and for the replay
     the full batches that fill its pools (``prime``).  ``sub`` keeps only the
-    prefill rows or only the decode rows of every batch (same pools)."""
+    prefill rows or only the decode rows of every batch (same pools);
+    ``shard`` gives one GPU's heads of a head-sharded group."""
     import workloads as wl
     if cfg == 5:
         full, _ = wl.replay_schedule()
+        full = [shard_heads(b, shard) for b in full]
         kc, vc = wl.make_caches(full[0], device=device, fill_prior=False, seed=5000)
         prime = []
         for i, b in enumerate(full):
@@ -219,7 +235,7 @@ def build_inputs(cfg, device, sub=None):
             batches.append(sb)
             steps.append({"q": q, "k_new": kn, "v_new": vn})
         return batches, steps, {"k_cache": kc, "v_cache": vc}, prime
-    b = wl.make_config(cfg)
+    b = shard_heads(wl.make_config(cfg), shard)
     t = wl.make_tensors(b, seed=1000 + cfg, device=device)
     shared = {"k_cache": t["k_cache"], "v_cache": t["v_cache"]}
     if sub is None:
@@ -230,7 +246,7 @@ def build_inputs(cfg, device, sub=None):
 
 
 def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, cold=0,
-               settle_s=1.0):
+               settle_s=1.0, shard=1):
     import numpy as np
     import torch
     import paper_2606_09061_amd as cp
@@ -239,7 +255,7 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     log(f"[bench] building inputs for mix {cfg}" + (f" ({sub} rows only)" if sub else ""))
-    batches, steps, shared, prime = build_inputs(cfg, dev, sub)
+    batches, steps, shared, prime = build_inputs(cfg, dev, sub, shard)
     descs = [cp.desc_for(b) for b in batches]
     tables = [torch.from_numpy(b.block_tables).to(dev) for b in batches]
     ws_bytes = max([cp.workspace_bytes(d, b.rows) for d, b in zip(descs, batches)] +
@@ -400,7 +416,9 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
         roof = {"bound": "hbm", "kernel": "decode", "achieved": achieved, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "avg_launch_ms": avg_ms,
                 "work_per_launch": per_launch}
-    roof["traffic"] = traffic_for(roof["kernel"].split()[0], wl_name)
+    # stored counter figures belong to the whole mix at its full head count
+    roof["traffic"] = (traffic_for(roof["kernel"].split()[0], wl_name)
+                       if sub is None and shard == 1 else None)
     # the other kernel's fraction, for mixes where both matter
     other = {}
     # the step against the roofline: t_pf = prefill flops at the MFMA peak,
@@ -434,7 +452,8 @@ def run_config(cfg, steps_n, warmup, with_cpu=True, cpu_budget=10.0, sub=None, c
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) bf16 q/k/v, seeded batch metadata and block tables)",
-        "config": {"workload": f"{wl_name}: {CONFIG_DESC[cfg]}" + (f" [{sub} rows only]" if sub else ""),
+        "config": {"workload": f"{wl_name}: {CONFIG_DESC[cfg]}" + (f" [{sub} rows only]" if sub else "")
+                   + (f" [one GPU of a {shard}-way head shard]" if shard > 1 else ""),
                    "heads_q_kv": [b0.num_q_heads, b0.num_kv_heads], "head_dim": b0.head_dim,
                    "block_size": b0.block_size,
                    "tokens_per_step": tokens / steps_n, "iterations": len(batches),
@@ -1254,6 +1273,9 @@ def main():
     ap.add_argument("--all", action="store_true", help="one JSON line per mix")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--shard", type=int, default=1, choices=[1, 2, 4, 8],
+                    help="run one GPU's share of a head-sharded (tensor-parallel) group of "
+                         "this many GPUs: Hq / N and Hkv / N heads, same rows")
     ap.add_argument("--settle", type=float, default=1.0, metavar="SECONDS",
                     help="run the steps back to back this long before the warm-up, so the "
                          "timed region starts at the clock the GPU holds under load (0: off)")
@@ -1325,7 +1347,7 @@ def main():
     for c in cfgs:
         res = run_config(c, args.steps, args.warmup, with_cpu=not args.no_cpu,
                          cpu_budget=args.cpu_seconds, sub=args.sub, cold=args.cold,
-                         settle_s=args.settle)
+                         settle_s=args.settle, shard=args.shard)
         print(json.dumps(res), flush=True)
 
 
