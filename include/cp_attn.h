@@ -147,8 +147,12 @@ int cp_kv_append(const cp_attn_desc *desc, const void *k_new, const void *v_new,
  * a log-sum-exp pass.  When a step has both kinds of rows, the decode work
  * runs inside the prefill launch (workgroups streaming K/V beside the
  * workgroups on the matrix cores) unless CP_FUSE_DECODE=0 gives it a launch
- * of its own; CP_FUSE_DECODE 1 / 2 / 3 place those workgroups after / before /
- * among the prefill tiles (3 is the default); outputs are the same bits. */
+ * of its own; CP_FUSE_DECODE 1 / 2 / 3 / 4 place those workgroups after /
+ * before / spread among / merged longest first with the prefill tiles (4 is
+ * the default); outputs are the same bits.  Workgroups sharing a K/V range
+ * are dealt to one XCD unless that leaves the XCDs unbalanced (few kv heads),
+ * when the planner cuts them into runs (CP_XCD_BALANCE_TOL, CP_XCD_PIECE_DIV;
+ * placement only, outputs are the same bits). */
 int cp_attn_mixed(const cp_attn_desc *desc, const void *q, const void *k_cache,
                   const void *v_cache, const int32_t *block_tables, const cp_row_meta *rows,
                   int32_t n_rows, void *out, void *ws, size_t ws_bytes, void *stream);

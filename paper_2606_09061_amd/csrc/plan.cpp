@@ -35,10 +35,16 @@ void add_merge(Plan& p, int32_t tok0, int32_t n_tok, int32_t ns, int32_t part0, 
 // so that slots sharing a K/V range -- the tiles of one chunk in one split,
 // for one kv head -- run on one XCD (a workgroup runs on XCD w mod
 // num_xcds), each XCD's slots longest first.  Groups are dealt to the
-// least-loaded XCD, largest group first.  Result: sc.flat holds XCD 0's
-// slots, then XCD 1's, ...; sc.xcd_len[x] how many.
+// least-loaded XCD, largest group first.  When that leaves the busiest XCD
+// more than (1 + balance_tol) times the mean load -- few groups (few kv
+// heads, few chunks) cannot balance eight XCDs -- every group costlier than
+// 1 / (piece_div * num_xcds) of the launch is cut into runs of consecutive
+// tiles of about that cost and the pieces are dealt instead; a piece's K/V
+// then comes from the shared last-level cache rather than its XCD's L2.
+// Result: sc.flat holds XCD 0's slots, then XCD 1's, ...; sc.xcd_len[x] how
+// many.
 void lists_by_xcd(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_xcds,
-                  PlanScratch& sc) {
+                  int piece_div, double balance_tol, PlanScratch& sc) {
   auto& groups = sc.groups;
   groups.clear();
   const int X = std::max(1, num_xcds);
@@ -55,16 +61,50 @@ void lists_by_xcd(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_
           gc += cost[sc.tiles[i].item0 + s];
           max_cost = std::max(max_cost, cost[sc.tiles[i].item0 + s]);
         }
-      for (int32_t h = 0; h < Hkv; ++h) groups.push_back({c, h, s, gc, 0});
+      for (int32_t h = 0; h < Hkv; ++h) groups.push_back({c, h, s, gc, 0, 0, ch.n_tiles});
     }
   }
   if (groups.empty()) return;
-  std::stable_sort(groups.begin(), groups.end(),
-                   [](const detail::Group& a, const detail::Group& b) { return a.cost > b.cost; });
-  sc.load.assign(X, 0);
-  for (detail::Group& g : groups) {
-    g.xcd = (int32_t)(std::min_element(sc.load.begin(), sc.load.end()) - sc.load.begin());
-    sc.load[g.xcd] += g.cost;
+  // longest-first dealing to the least-loaded XCD; returns the largest load
+  auto deal = [&]() {
+    std::stable_sort(groups.begin(), groups.end(),
+                     [](const detail::Group& a, const detail::Group& b) { return a.cost > b.cost; });
+    sc.load.assign(X, 0);
+    for (detail::Group& g : groups) {
+      g.xcd = (int32_t)(std::min_element(sc.load.begin(), sc.load.end()) - sc.load.begin());
+      sc.load[g.xcd] += g.cost;
+    }
+    return *std::max_element(sc.load.begin(), sc.load.end());
+  };
+  int64_t total = 0;
+  for (const detail::Group& g : groups) total += g.cost;
+  const int64_t busiest = deal();
+  if (piece_div > 0 && (double)busiest * X > (1.0 + balance_tol) * (double)total) {
+    const int64_t piece = std::max<int64_t>(1, total / ((int64_t)piece_div * X));
+    auto& pieces = sc.pieces;
+    pieces.clear();
+    for (const detail::Group& g : groups) {
+      if (g.cost <= piece) {
+        pieces.push_back(g);
+        continue;
+      }
+      const detail::Chunk& ch = sc.chunks[g.chunk];
+      int32_t a = 0;
+      int64_t acc = 0;
+      for (int32_t i = 0; i < ch.n_tiles; ++i) {
+        const detail::Tile& tl = sc.tiles[ch.tile0 + i];
+        if (tl.ns <= g.split) continue;
+        acc += cost[tl.item0 + g.split];
+        if (acc >= piece) {
+          pieces.push_back({g.chunk, g.kvh, g.split, acc, 0, a, i + 1});
+          a = i + 1;
+          acc = 0;
+        }
+      }
+      if (acc > 0) pieces.push_back({g.chunk, g.kvh, g.split, acc, 0, a, ch.n_tiles});
+    }
+    groups.swap(pieces);
+    deal();
   }
   // Each XCD's slots, longest first, equal costs in the order their groups
   // were dealt: a counting sort keyed on (XCD, max_cost - cost).
@@ -74,7 +114,7 @@ void lists_by_xcd(bool wide, const std::vector<int64_t>& cost, int Hkv, int num_
   auto for_each_slot = [&](auto&& f) {
     for (const detail::Group& g : groups) {
       const detail::Chunk& ch = sc.chunks[g.chunk];
-      for (int32_t i = ch.tile0; i < ch.tile0 + ch.n_tiles; ++i) {
+      for (int32_t i = ch.tile0 + g.t0; i < ch.tile0 + g.t1; ++i) {
         const detail::Tile& tl = sc.tiles[i];
         if (tl.ns <= g.split) continue;
         const int32_t item = tl.item0 + g.split;
@@ -286,6 +326,8 @@ Tuning tuning_from_env(int num_cus) {
   if (const char* s = std::getenv("CP_FUSE_UNITS_PER_CU")) t.fuse_units_per_cu = atof(s);
   if (const char* s = std::getenv("CP_FUSE_FLOPS_PER_BYTE")) t.fuse_flops_per_byte = atof(s);
   if (const char* s = std::getenv("CP_NUM_XCDS")) t.num_xcds = std::min(64, std::max(1, atoi(s)));
+  if (const char* s = std::getenv("CP_XCD_PIECE_DIV")) t.xcd_piece_div = std::max(0, atoi(s));
+  if (const char* s = std::getenv("CP_XCD_BALANCE_TOL")) t.xcd_balance_tol = std::max(-1.0, atof(s));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_ROWS"))
     t.prefill_wide_min_rows = std::max<int64_t>(1, atoll(s));
   if (const char* s = std::getenv("CP_PREFILL_WIDE_MIN_KEYS"))
@@ -584,7 +626,8 @@ void build_plan(const cp_attn_desc& d, const cp_row_meta* rows, int32_t n_rows, 
   if ((int64_t)std::max(sc.items[0].size(), sc.items[1].size()) * Hkv > INT32_MAX)
     throw std::length_error("prefill slot index overflows int32");
   for (int w = 0; w < 2; ++w) {
-    lists_by_xcd(w == 1, sc.item_cost[w], Hkv, t.num_xcds, sc);
+    lists_by_xcd(w == 1, sc.item_cost[w], Hkv, t.num_xcds, t.xcd_piece_div, t.xcd_balance_tol,
+                 sc);
     interleave_by_xcd(sc.items[w], Hkv, t.num_xcds, sc, w ? p.prefill_wide : p.prefill);
   }
 

@@ -111,6 +111,10 @@ struct Tuning {
   double fuse_units_per_cu = 0.75;   // decode ranges per CU that set the split length when
                                      // prefill dominates a fused step
   double fuse_flops_per_byte = 180.0;  // prefill dominates: its flops > this x decode bytes
+  int xcd_piece_div = 4;        // K/V groups costlier than 1/(this x XCDs) of a launch's work
+                                // are cut into runs of tiles of about that cost (0: never) ...
+  double xcd_balance_tol = 0.25;  // ... when whole groups leave the busiest XCD more than
+                                  // this fraction above the mean (negative: always)
 };
 
 namespace detail {
@@ -123,10 +127,11 @@ struct Chunk {        // the tiles of one chunk, cut on one split grid
   int32_t tile0, n_tiles, max_ns;
   bool wide;
 };
-struct Group {        // items sharing one kv head's K/V range: (chunk, kv head, split)
-  int32_t chunk, kvh, split;
+struct Group {        // items sharing one kv head's K/V range: (chunk, kv head, split),
+  int32_t chunk, kvh, split;  // tiles [t0, t1) of the chunk
   int64_t cost;
   int32_t xcd;        // the XCD it is dealt to
+  int32_t t0, t1;
 };
 }  // namespace detail
 
@@ -138,7 +143,7 @@ struct PlanScratch {
   std::vector<detail::Chunk> chunks;
   std::vector<int32_t> bounds;
   std::vector<int64_t> item_cost[2];
-  std::vector<detail::Group> groups;
+  std::vector<detail::Group> groups, pieces;
   std::vector<int64_t> load;
   std::vector<int64_t> count;
   std::vector<int32_t> flat;                          // slots grouped by XCD, longest first

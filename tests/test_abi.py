@@ -472,3 +472,66 @@ def test_decode_blocks_in_the_prefill_launch(monkeypatch, mode):
             pos = np.flatnonzero(fused[:, 1] == -1)
             assert pos.min() < len(fused) // 2 < pos.max()
         assert len(fused) == 0 or fused[-1, 1] != 0   # no trailing idle records
+
+
+def _xcd_loads(recs, X=8):
+    """Key steps of the tile records dealt to each XCD (record i runs on XCD
+    i mod X)."""
+    loads = np.zeros(X)
+    for i, r in enumerate(recs.tolist()):
+        if r[1] > 0:
+            loads[i % X] += -(-(r[5] - r[4]) // 64) + 3
+    return loads
+
+
+def test_few_kv_groups_are_cut_across_xcds(monkeypatch):
+    """With one kv head (an 8-way head shard of the 70B layer) the K/V groups
+    are too few and too unequal to balance eight XCDs whole; the planner then
+    cuts them into runs of tiles.  The launch keeps exactly the same tiles
+    (only their positions move), every token stays covered, and the busiest
+    XCD's load falls toward the mean.  Full-head batches, whose groups
+    balance, keep their layout."""
+    import bench
+    batches, _ = replay_schedule()
+    for j in (0, 3, 9, 15, 19):
+        b = bench.shard_heads(batches[j], 8)
+        d = cp.desc_for(b)
+        monkeypatch.setenv("CP_XCD_PIECE_DIV", "0")
+        whole = cp.plan_records(d, b.rows, 0)
+        monkeypatch.delenv("CP_XCD_PIECE_DIV")
+        cut = cp.plan_records(d, b.rows, 0)
+        tiles = lambda r: sorted(map(tuple, r[r[:, 1] > 0].tolist()))
+        dec = lambda r: sorted(map(tuple, r[r[:, 1] == -1].tolist()))
+        assert tiles(whole) == tiles(cut), j
+        assert dec(whole) == dec(cut), j
+        lw, lc = _xcd_loads(whole), _xcd_loads(cut)
+        assert lw.max() > 1.25 * lw.mean(), (j, lw)
+        assert lc.max() < 0.8 * lw.max(), (j, lw, lc)
+        _check_coverage(b)
+    for j in (0, 15):
+        d = cp.desc_for(batches[j])
+        monkeypatch.setenv("CP_XCD_PIECE_DIV", "0")
+        whole = cp.plan_records(d, batches[j].rows, 0)
+        monkeypatch.delenv("CP_XCD_PIECE_DIV")
+        assert np.array_equal(whole, cp.plan_records(d, batches[j].rows, 0)), j
+
+
+def test_forced_xcd_pieces_keep_every_tile(monkeypatch):
+    """Cutting every group (a negative tolerance: always; eighth-size pieces)
+    on the other mixes moves tiles between XCDs but adds, drops and changes
+    none."""
+    monkeypatch.setenv("CP_XCD_BALANCE_TOL", "-1")
+    monkeypatch.setenv("CP_XCD_PIECE_DIV", "8")
+    cut = {(n, w): cp.plan_records(cp.desc_for(make_config(n)), make_config(n).rows, w)
+           for n in (2, 3, 4) for w in (0, 1)}
+    moved = 0
+    monkeypatch.setenv("CP_XCD_PIECE_DIV", "0")
+    for (n, w), recs in cut.items():
+        whole = cp.plan_records(cp.desc_for(make_config(n)), make_config(n).rows, w)
+        key = lambda r: sorted(map(tuple, r[r[:, 1] != 0].tolist()))
+        assert key(whole) == key(recs), (n, w)
+        moved += len(whole) != len(recs) or not np.array_equal(whole, recs)
+    assert moved > 0
+    monkeypatch.delenv("CP_XCD_PIECE_DIV")
+    for n in (2, 3, 4):
+        _check_coverage(make_config(n))

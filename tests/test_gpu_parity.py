@@ -12,7 +12,7 @@ import torch
 
 import oracle
 from gpu_util import assert_close, run_step, say, to_dev, words
-from workloads import Batch, make_batch, make_config, make_tensors
+from workloads import Batch, make_batch, make_config, make_tensors, replay_schedule
 
 pytestmark = pytest.mark.gpu
 
@@ -269,3 +269,29 @@ def test_step_matches_append_then_attention(which):
     assert np.array_equal(words(b["v_cache"]).reshape(-1), vc_ref.reshape(-1))
     assert np.array_equal(words(outs[0]), words(outs[1])), "step differs from the two calls"
     assert_close(outs[1], ref, f"step {which}")
+
+
+@pytest.mark.parametrize("it,shard", [(9, 8), (4, 4), (0, 8)])
+def test_xcd_pieces_change_no_output_bit(monkeypatch, it, shard):
+    """A head-sharded replay iteration (1 or 2 kv heads) has too few K/V groups
+    to balance the XCDs whole, so the planner cuts them into runs of tiles:
+    the output matches the oracle element by element and equals the uncut
+    layout's bit for bit (workgroups move, no work changes)."""
+    import bench
+    batches, _ = replay_schedule()
+    batch = bench.shard_heads(batches[it], shard)
+    tens = make_tensors(batch, seed=4400 + it)
+    kc_ref, vc_ref = oracle.kv_append(batch, tens["k_new"], tens["v_new"], tens["k_cache"],
+                                      tens["v_cache"])
+    ref = oracle.attn(batch, tens["q"], kc_ref, vc_ref)
+    outs = {}
+    for div in ("0", "4"):
+        monkeypatch.setenv("CP_XCD_PIECE_DIV", div)
+        say(f"[gpu] replay it {it} shard {shard}: CP_XCD_PIECE_DIV={div}")
+        t = to_dev(tens)
+        out = run_step(batch, t, one_call=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(words(t["k_cache"]).reshape(-1), kc_ref.reshape(-1))
+        assert_close(out, ref, f"replay it {it} shard {shard} div {div}")
+        outs[div] = words(out)
+    assert np.array_equal(outs["0"], outs["4"])
