@@ -93,12 +93,24 @@ __device__ __forceinline__ uint32_t get_word(const uint4& v, int e) {
   return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w;
 }
 
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
-// (global_load_lds_dwordx4); `lds` must be wave-uniform.  The address-space
-// cast exists only in the device pass.
-__device__ __forceinline__ void copy16_to_lds(const void* src, uint8_t* lds) {
+// 16 bytes per lane from global memory (uniform base + this lane's byte
+// offset) straight into LDS at lds + 16 * lane (`lds` wave-uniform, in M0),
+// written as the instruction itself.  Built from the compiler's intrinsic,
+// the copies were tracked by its wait insertion, which cannot tell which of
+// the four LDS tiles a copy in flight fills: it waited for every copy,
+// including the K tile issued 1.5 iterations ahead, before the V operand
+// reads of every other iteration.  Untracked, the copies are awaited only by
+// the explicit vmcnt waits below (no other vector-memory loads run in the
+// loop, so the counts are exact; the compiler's own waits for the Q loads
+// issued before them only ever wait longer).  The s_nop is the wait state a
+// copy needs after M0 is written, which the compiler inserts only for its own.
+__device__ __forceinline__ void copy16_to_lds(const uint16_t* base, uint32_t byte_off,
+                                              uint8_t* lds) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)lds, 16, 0, 0);
+  const uint32_t dst = (uint32_t)(uintptr_t)(lds_ptr_t)lds;
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(byte_off), "s"(base),
+               "{m0}"(dst)
+               : "memory");
 #endif
 }
 
@@ -263,7 +275,7 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
       const uint16_t* src = base + (int64_t)blk.b[j] * blk_elems;
       static_for<j * (PW / NBW), (j + 1) * (PW / NBW)>([&](auto i_c) {
         constexpr int i = decltype(i_c)::value;
-        copy16_to_lds(src + off[i], buf + (wave * PW + i) * 1024);
+        copy16_to_lds(src, off[i] * 2u, buf + (wave * PW + i) * 1024);
       });
     });
   };
