@@ -33,10 +33,10 @@
 // wave a few 1 KiB pieces of one or two blocks per step, with wave-uniform
 // block-table entries.  Per-lane source addresses are permuted so the LDS
 // tiles land XOR-swizzled (conflict-free MFMA operand reads).  K and V each
-// have two LDS buffers, declared as separate arrays so the compiler can tell
-// the in-flight copies from the reads.  The copy of a tile is issued 1.5
-// iterations before it is read; every phase starts with a wait on the copies
-// it needs and one barrier.
+// have two LDS buffers, separate arrays so that every access names its buffer
+// at compile time.  The copy of a tile is issued 1.5 iterations before it is
+// read; every phase starts with a wait on the copies it needs (the only
+// waits on them: see copy16_to_lds) and one barrier.
 #include "decode_body.hpp"
 #include "device.hpp"
 #include "kernels.hpp"
