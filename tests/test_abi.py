@@ -535,3 +535,18 @@ def test_forced_xcd_pieces_keep_every_tile(monkeypatch):
     monkeypatch.delenv("CP_XCD_PIECE_DIV")
     for n in (2, 3, 4):
         _check_coverage(make_config(n))
+
+
+def test_shard_heads_divides_heads_and_keeps_rows():
+    """`bench.py --shard N` runs one GPU's share: Hq/N and Hkv/N heads, the
+    same rows, block tables and scale; N must divide the kv heads."""
+    import bench
+    batches, _ = replay_schedule()
+    b = batches[3]
+    for n in (1, 2, 4, 8):
+        s = bench.shard_heads(b, n)
+        assert (s.num_q_heads, s.num_kv_heads) == (b.num_q_heads // n, b.num_kv_heads // n)
+        assert s.group == b.group and s.sm_scale == b.sm_scale and s.head_dim == b.head_dim
+        assert np.array_equal(s.rows, b.rows) and np.array_equal(s.block_tables, b.block_tables)
+    with pytest.raises(SystemExit):
+        bench.shard_heads(make_config(1), 4)   # 2 kv heads

@@ -123,3 +123,28 @@ def test_long_context_prefill_unsplit(monkeypatch):
     assert np.array_equal(words(t["k_cache"]).reshape(-1), kc_ref.reshape(-1)), "K pool differs"
     assert np.array_equal(words(t["v_cache"]).reshape(-1), vc_ref.reshape(-1)), "V pool differs"
     check_all(batch, out, host["q"], kc_ref, vc_ref, "long context")
+
+
+@pytest.mark.parametrize("shard", [8, 2])
+def test_replay_head_shard_lockstep(shard):
+    """One GPU's share of the replay under an N-way head shard (the shapes
+    `bench.py --shard N` measures: 64/N q heads, 8/N kv heads, where few K/V
+    groups make the planner cut them across XCDs), all 20 iterations in
+    order through cp_step_mixed, every output element against the oracle."""
+    import bench
+    batches, _ = replay_schedule()
+    batches = [bench.shard_heads(b, shard) for b in batches]
+    dev = torch.device("cuda", 0)
+    kc, vc = make_caches(batches[0], device=dev, fill_prior=False)
+    kc_ref, vc_ref = words(kc), words(vc)
+    for i, b in enumerate(batches):
+        q, kn, vn, _ = make_step_tensors(b, 9500 + i, dev)
+        t = {"q": q, "k_new": kn, "v_new": vn, "k_cache": kc, "v_cache": vc,
+             "block_tables": torch.from_numpy(b.block_tables).to(dev)}
+        say(f"[gpu] replay shard {shard} iteration {i}: rows={b.n_rows} T={b.num_tokens}")
+        out = run_step(b, t, one_call=True)
+        torch.cuda.synchronize()
+        kc_ref, vc_ref = oracle.kv_append(b, kn.cpu(), vn.cpu(), kc_ref, vc_ref, inplace=True)
+        check_all(b, out, q.cpu(), kc_ref, vc_ref, f"replay shard {shard} it {i}")
+    assert np.array_equal(words(kc).reshape(-1), kc_ref.reshape(-1))
+    assert np.array_equal(words(vc).reshape(-1), vc_ref.reshape(-1))
