@@ -550,3 +550,17 @@ def test_shard_heads_divides_heads_and_keeps_rows():
         assert np.array_equal(s.rows, b.rows) and np.array_equal(s.block_tables, b.block_tables)
     with pytest.raises(SystemExit):
         bench.shard_heads(make_config(1), 4)   # 2 kv heads
+
+
+# ------------------------------------------------- the GPU fuzz cases, planned on the host
+
+def test_gpu_fuzz_cases_plan_exactly(monkeypatch):
+    """Every batch the GPU fuzz test runs, under the planner settings it runs
+    it with, plans to an exact cover of its (token, kv head) key ranges."""
+    from fuzz_cases import apply_settings, draw_case, draw_settings
+    for seed in range(40):
+        _check_coverage(draw_case(seed))
+    for seed in range(24):
+        env = draw_settings(seed)
+        apply_settings(monkeypatch, env)
+        _check_coverage(draw_case(100 + seed), int(env["CP_PREFILL_MIN_LEN"]))
