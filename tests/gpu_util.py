@@ -72,8 +72,24 @@ def errors(gpu_out, ref):
     return float(e.max()) if e.size else 0.0, float(e.mean()) if e.size else 0.0
 
 
+def bf16_rne(x):
+    """fp64 values rounded once to the nearest bfloat16 (8 significant bits),
+    ties to even; exact for the normal range the attention outputs live in."""
+    m, e = np.frexp(np.asarray(x, dtype=np.float64))
+    return np.ldexp(np.round(np.ldexp(m, 8)), e - 8)
+
+
+def floor_errors(ref):
+    """max and mean |bf16(oracle) - oracle|: the error of a perfectly rounded
+    bf16 output, the floor under any bf16 result."""
+    e = np.abs(bf16_rne(ref) - ref)
+    return float(e.max()) if e.size else 0.0, float(e.mean()) if e.size else 0.0
+
+
 def assert_close(gpu_out, ref, what=""):
     mx, mean = errors(gpu_out, ref)
-    say(f"  {what}: max_abs={mx:.3e} mean_abs={mean:.3e}")
+    fmx, fmean = floor_errors(ref)
+    say(f"  {what}: max_abs={mx:.3e} mean_abs={mean:.3e} "
+        f"(oracle rounded to bf16: max {fmx:.3e} mean {fmean:.3e})")
     assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{what}: max {mx:.3e} mean {mean:.3e}"
     return mx, mean
