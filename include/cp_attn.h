@@ -204,7 +204,11 @@ int cp_attn_prepare(const cp_attn_desc *desc, const cp_row_meta *rows, int32_t n
  * the prepare before the run.  Every list the plan names (its offset plus
  * its length times the item size) must lie inside plan->ws_bytes, else
  * CP_ERR_INVALID_ARG and nothing is enqueued; a decode block of a prefill
- * record list that names no decode unit of the plan does nothing. */
+ * record list that names no decode unit of the plan does nothing.  It only
+ * enqueues kernel launches (no copy, allocation or wait, unless CP_DEBUG or
+ * the per-kernel profile is on), so a caller may capture it in a HIP graph
+ * and replay it while the plan, the workspace and the buffers stay where they
+ * were at capture. */
 int cp_attn_run(const cp_attn_plan *plan, const void *q, const void *k_cache,
                 const void *v_cache, const int32_t *block_tables, void *out, void *ws,
                 size_t ws_bytes, void *stream);

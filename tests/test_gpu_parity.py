@@ -126,6 +126,55 @@ def test_prepared_plan_runs_match_attn_mixed_bit_for_bit():
                     layers[0]["block_tables"], outs_plan[0], ws_b[:256])
 
 
+@pytest.mark.parametrize("fuse", ["4", "0"])
+def test_prepared_plan_replays_in_a_hip_graph(monkeypatch, fuse):
+    """cp_attn_run only enqueues kernels, so a caller can capture it in a HIP
+    graph (the layers of a model iteration share one plan).  Each replay, with
+    new q written into the captured buffer between replays and eager work and
+    synchronisations around it, equals an eager run bit for bit, and the last
+    equals the oracle.  fuse "4": decode rows inside the prefill launch, then
+    the merge; "0": prefill, decode and merge launches."""
+    import paper_2606_09061_amd as cp
+    monkeypatch.setenv("CP_FUSE_DECODE", fuse)
+    rng = np.random.default_rng(19)
+    rows = [(3000, 96), (0, 130), (8000, 1), (5000, 1), (300, 1), (12000, 40)]
+    batch = make_batch("graph", 32, 8, 128, 16, rows, rng)
+    d = cp.desc_for(batch)
+    say(f"[gpu] graph replay, CP_FUSE_DECODE={fuse}: rows={batch.n_rows} T={batch.num_tokens}")
+    tens = make_tensors(batch, seed=5201)
+    t = to_dev(tens)
+    ws_app = torch.empty(cp.workspace_bytes(d, batch.rows), dtype=torch.uint8, device="cuda")
+    cp.kv_append(d, t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["block_tables"],
+                 batch.rows, ws_app)
+    ws = torch.empty_like(ws_app)
+    plan = cp.attn_prepare(d, batch.rows, ws)
+    assert plan.n_merge > 0 and plan.n_decode > 0
+    assert plan.decode_in_prefill == (0 if fuse == "0" else 1)
+    shape = (batch.num_tokens, 32, 128)
+    out_e = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    out_g = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    run = lambda o: cp.attn_run(plan, t["q"], t["k_cache"], t["v_cache"], t["block_tables"], o, ws)
+    run(out_e)  # first use of the kernels outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(out_g)
+    gen = torch.Generator().manual_seed(5202)
+    for r in range(4):
+        q_new = torch.randn(shape, generator=gen).to(torch.bfloat16)
+        t["q"].copy_(q_new.to("cuda"))
+        out_g.fill_(float("nan"))  # a replay must write every element
+        g.replay()
+        torch.cuda.synchronize()
+        run(out_e)
+        torch.cuda.synchronize()
+        assert torch.equal(out_g, out_e), f"replay {r} differs from the eager run"
+    kc_ref, vc_ref = oracle.kv_append(batch, tens["k_new"], tens["v_new"], tens["k_cache"],
+                                      tens["v_cache"])
+    ref = oracle.attn(batch, q_new, kc_ref, vc_ref)
+    assert_close(out_g, ref, f"graph replay (CP_FUSE_DECODE={fuse})")
+
+
 def test_debug_mode_rejects_out_of_range_block_ids(monkeypatch):
     """CP_DEBUG=1: a table entry outside [0, num_blocks) is found on the host
     before anything is enqueued.  The pools hold 4 blocks past the num_blocks
