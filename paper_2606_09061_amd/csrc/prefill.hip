@@ -37,6 +37,12 @@
 // at compile time.  The copy of a tile is issued 1.5 iterations before it is
 // read; every phase starts with a wait on the copies it needs (the only
 // waits on them: see copy16_to_lds) and one barrier.
+//
+// Output.  A lane's accumulators hold half the features of one row, in runs of four;
+// stored directly, every store instruction would touch 32 rows.  Instead each
+// wave writes its normalised rows into a private slice of the (then idle) K/V
+// buffers and stores them back as whole rows, consecutive lanes taking
+// consecutive 16-byte pieces of a row.
 #include "decode_body.hpp"
 #include "device.hpp"
 #include "kernels.hpp"
@@ -656,7 +662,78 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
     iter(st, F_(), T_());
   }
 
-  // ---- finish: the two lane halves hold disjoint keys of the same query
+  // ---- finish: the two lane halves hold disjoint keys of the same query.
+  // Each wave stages its rows through LDS (a slice of the four tile buffers,
+  // free once every wave is past the last step) and stores whole rows: 16
+  // lanes per 256-byte run, instead of 16-byte pieces of 32 rows per store.
+  if constexpr (RG == 1) {
+    constexpr int SLICE = 4 * C::TILE_BYTES / NW;   // staging bytes per wave
+    barrier();  // every wave has read its last V tile
+    const int bsel = (wave * SLICE) / C::TILE_BYTES;
+    uint8_t* const st = (bsel == 0 ? kb0 : bsel == 1 ? kb1 : bsel == 2 ? vb0 : vb1) +
+                        (wave * SLICE) % C::TILE_BYTES;
+    const float l_tot = halves_sum(l_run[0]);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const int wrow0 = wave * 32;  // first tile row of this wave
+    if (it.part < 0) {
+      // bf16 rows of D * 2 bytes; 16-byte unit u of row r stored at u ^ (r % U)
+      constexpr int RB = D * 2, U = RB / 16;
+      static_assert(32 * RB <= SLICE, "bf16 staging");
+      static_for<0, NDT>([&](auto dt_c) {
+        constexpr int dt = decltype(dt_c)::value;
+        static_for<0, 4>([&](auto i_c) {
+          constexpr int i = decltype(i_c)::value;
+          uint2 w;
+          w.x = pack_bf16x2(oacc[0][dt][4 * i + 0] * inv, oacc[0][dt][4 * i + 1] * inv);
+          w.y = pack_bf16x2(oacc[0][dt][4 * i + 2] * inv, oacc[0][dt][4 * i + 3] * inv);
+          constexpr int u = dt * 4 + i;  // features [8u, 8u + 8): this lane's half g
+          *reinterpret_cast<uint2*>(st + col * RB + ((u ^ (col % U)) * 16) + 8 * g) = w;
+        });
+      });
+      constexpr int RPI = 64 / U;  // rows per store instruction
+      static_for<0, 32 / RPI>([&](auto k_c) {
+        constexpr int k = decltype(k_c)::value;
+        const int r = k * RPI + lane / U, c = lane % U;
+        const uint4 v = *reinterpret_cast<const uint4*>(st + r * RB + ((c ^ (r % U)) * 16));
+        const int row = wrow0 + r, t = row / G;
+        if (t < it.n_tok)
+          *reinterpret_cast<uint4*>(
+              out + ((int64_t)(it.tok0 + t) * hq + kvh * G + row % G) * D + c * 8) = v;
+      });
+    } else {
+      // fp32 rows in PASSES column passes of DP features (RB bytes a row)
+      constexpr int PASSES = 32 * D * 4 > SLICE ? 2 : 1;
+      constexpr int DP = D / PASSES, RB = DP * 4, U = RB / 16;
+      static_assert(32 * RB <= SLICE && U <= 32, "fp32 staging");
+      static_for<0, PASSES>([&](auto p_c) {
+        constexpr int pass = decltype(p_c)::value;
+        static_for<pass * NDT / PASSES, (pass + 1) * NDT / PASSES>([&](auto dt_c) {
+          constexpr int dt = decltype(dt_c)::value;
+          static_for<0, 4>([&](auto i_c) {
+            constexpr int i = decltype(i_c)::value;
+            const int u = (dt - pass * NDT / PASSES) * 8 + 2 * i + g;  // features [4u, 4u + 4)
+            *reinterpret_cast<float4*>(st + col * RB + ((u ^ (col % U)) * 16)) =
+                make_float4(oacc[0][dt][4 * i + 0] * inv, oacc[0][dt][4 * i + 1] * inv,
+                            oacc[0][dt][4 * i + 2] * inv, oacc[0][dt][4 * i + 3] * inv);
+          });
+        });
+        constexpr int RPI = 64 / U;
+        static_for<0, 32 / RPI>([&](auto k_c) {
+          constexpr int k = decltype(k_c)::value;
+          const int r = k * RPI + lane / U, c = lane % U;
+          const float4 v = *reinterpret_cast<const float4*>(st + r * RB + ((c ^ (r % U)) * 16));
+          const int row = wrow0 + r;
+          if (row / G < it.n_tok)
+            *reinterpret_cast<float4*>(part_o + (int64_t)(it.part + row) * D + pass * DP + c * 4) =
+                v;
+        });
+      });
+      if (g == 0 && row_valid[0]) part_lse[it.part + wrow0 + col] =
+          l_tot > 0.f ? m_run[0] + __log2f(l_tot) : -INFINITY;
+    }
+    return;
+  }
+  // row groups of more than one: each lane stores its own pieces
   static_for<0, RG>([&](auto rg_c) {
     constexpr int rg = decltype(rg_c)::value;
     const float l_tot = halves_sum(l_run[rg]);
