@@ -97,7 +97,7 @@ struct Tuning {
                                 // rows to the decode kernel token by token (2..kMaxPrefillMinLen)
   int decode_target_items = 0;  // 0: derived from the CU count and the decode bytes
   int prefill_target_items = 0; // 0: split length chosen by the run-time estimate
-  int prefill_min_split = 8;    // shortest prefill split, in kPrefillKeys steps
+  int prefill_min_split = 10;   // shortest prefill split, in kPrefillKeys steps
   int num_cus = 256;
   int num_xcds = 8;             // workgroups are dealt round-robin over the XCDs
   int64_t prefill_wide_min_rows = 129;  // chunks with chunk_len * G >= this use 256-row tiles,
