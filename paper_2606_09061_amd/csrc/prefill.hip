@@ -731,42 +731,42 @@ __global__ __launch_bounds__(NW * 64, RG == 1 ? 2 : 1) void prefill_kernel(
       if (g == 0 && row_valid[0]) part_lse[it.part + wrow0 + col] =
           l_tot > 0.f ? m_run[0] + __log2f(l_tot) : -INFINITY;
     }
-    return;
+  } else {
+    // row groups of more than one: each lane stores its own pieces
+    static_for<0, RG>([&](auto rg_c) {
+      constexpr int rg = decltype(rg_c)::value;
+      const float l_tot = halves_sum(l_run[rg]);
+      if (!row_valid[rg]) return;
+      const int row = (wave * RG + rg) * 32 + col;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      if (it.part < 0) {
+        uint16_t* op = out + ((int64_t)(it.tok0 + tl[rg]) * hq + kvh * G + row % G) * D + 4 * g;
+        static_for<0, NDT>([&](auto dt_c) {
+          constexpr int dt = decltype(dt_c)::value;
+          static_for<0, 4>([&](auto i_c) {
+            constexpr int i = decltype(i_c)::value;
+            uint2 w;
+            w.x = pack_bf16x2(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv);
+            w.y = pack_bf16x2(oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
+            *reinterpret_cast<uint2*>(op + dt * 32 + 8 * i) = w;
+          });
+        });
+      } else {
+        const int prow = it.part + row;
+        float* pp = part_o + (int64_t)prow * D + 4 * g;
+        static_for<0, NDT>([&](auto dt_c) {
+          constexpr int dt = decltype(dt_c)::value;
+          static_for<0, 4>([&](auto i_c) {
+            constexpr int i = decltype(i_c)::value;
+            *reinterpret_cast<float4*>(pp + dt * 32 + 8 * i) =
+                make_float4(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv,
+                            oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
+          });
+        });
+        if (g == 0) part_lse[prow] = l_tot > 0.f ? m_run[rg] + __log2f(l_tot) : -INFINITY;
+      }
+    });
   }
-  // row groups of more than one: each lane stores its own pieces
-  static_for<0, RG>([&](auto rg_c) {
-    constexpr int rg = decltype(rg_c)::value;
-    const float l_tot = halves_sum(l_run[rg]);
-    if (!row_valid[rg]) return;
-    const int row = (wave * RG + rg) * 32 + col;
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    if (it.part < 0) {
-      uint16_t* op = out + ((int64_t)(it.tok0 + tl[rg]) * hq + kvh * G + row % G) * D + 4 * g;
-      static_for<0, NDT>([&](auto dt_c) {
-        constexpr int dt = decltype(dt_c)::value;
-        static_for<0, 4>([&](auto i_c) {
-          constexpr int i = decltype(i_c)::value;
-          uint2 w;
-          w.x = pack_bf16x2(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv);
-          w.y = pack_bf16x2(oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
-          *reinterpret_cast<uint2*>(op + dt * 32 + 8 * i) = w;
-        });
-      });
-    } else {
-      const int prow = it.part + row;
-      float* pp = part_o + (int64_t)prow * D + 4 * g;
-      static_for<0, NDT>([&](auto dt_c) {
-        constexpr int dt = decltype(dt_c)::value;
-        static_for<0, 4>([&](auto i_c) {
-          constexpr int i = decltype(i_c)::value;
-          *reinterpret_cast<float4*>(pp + dt * 32 + 8 * i) =
-              make_float4(oacc[rg][dt][4 * i + 0] * inv, oacc[rg][dt][4 * i + 1] * inv,
-                          oacc[rg][dt][4 * i + 2] * inv, oacc[rg][dt][4 * i + 3] * inv);
-        });
-      });
-      if (g == 0) part_lse[prow] = l_tot > 0.f ? m_run[rg] + __log2f(l_tot) : -INFINITY;
-    }
-  });
 }
 
 template <int D, int B, int G, int NW>
